@@ -1,0 +1,182 @@
+/*
+ * q4nx.h -- C ABI of libq4nx.so: the Q4NX 4-bit weight format and its
+ * dequantization fused with the linear projection, for AMD Instinct MI355X
+ * (gfx950).
+ *
+ * The format and the operations follow "Mapping Gemma3 onto an Edge Dataflow
+ * Architecture" (arXiv 2602.06063):
+ *   - Q4NX block (Sec. 3.1.1, Dequantization Engine): 32 x 256 int4 weights,
+ *     256 bf16 scales and 256 bf16 minimal-value offsets, 5120 bytes; one
+ *     scale/offset pair per group of 32 weights.
+ *   - Dequantization, Eq. 3: w = d_g * q + m_g, q in {0..15}.
+ *   - Decode projection (FusedDQP, Sec. 3.2.1, Eq. 14/15): y = W x with the
+ *     dequantization fused into the mat-vec.
+ *   - Prefill projection (Sec. 3.1.2): the tiled matrix product C = A x B,
+ *     here Y = X W^T with W dequantized to bf16 on the fly.
+ *
+ * Conventions used by every function:
+ *   - Shapes: M = token rows, N = output features, K = input features.  The
+ *     weight matrix W is N x K.  K must be a multiple of 32 (the group size).
+ *   - bf16 values travel as raw uint16_t bit patterns.
+ *   - Layout of a packed matrix ("blob"): ceil(N/32) * ceil(K/256) blocks of
+ *     5120 bytes, strip-major: block (i, j) -- rows 32i..32i+31, columns
+ *     256j..256j+255 -- starts at byte (i * ceil(K/256) + j) * 5120.  Inside a
+ *     block: 4096 bytes of codes (row r at byte 128r; byte c of a row holds
+ *     column 2c in bits 0-3 and column 2c+1 in bits 4-7), then 256 scales,
+ *     then 256 offsets, each indexed 8r + g for group g (columns 32g..32g+31)
+ *     of row r, little-endian bf16.  Rows >= N and columns >= K are padding
+ *     with code 0, scale +0 and offset +0.
+ *   - Value domain of scales and offsets: zero, or a finite bf16 whose
+ *     magnitude lies in [2^-100, 2^101).  Inside it Eq. 3 is exact up to one
+ *     rounding in float32 and never produces a subnormal, so results do not
+ *     depend on denormal flushing or on FMA contraction.
+ *   - Ownership: the caller owns every buffer; the library never frees or
+ *     retains caller memory.  Device pointers come from hipMalloc (or a
+ *     framework allocator built on it).
+ *   - Device calls validate their arguments synchronously on the host, before
+ *     any HIP call, then only enqueue work on `stream` (NULL = the default
+ *     stream) and return; they never synchronize the device.  A launch failure
+ *     is reported as Q4NX_ERR_HIP (details in q4nx_last_error()).
+ *   - The library keeps one small scratch area per device (split-K partial
+ *     sums and arrival counters of q4nx_gemv / q4nx_gemv_batched), allocated
+ *     and zeroed on the first call that needs it on that device; make that
+ *     first call outside HIP graph capture.  Calls that use it must not run
+ *     concurrently on one device (e.g. on two streams at once).
+ *   - No C++ exception crosses this interface.
+ */
+#ifndef Q4NX_H
+#define Q4NX_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+struct ihipStream_t;
+typedef struct ihipStream_t* hipStream_t;
+
+typedef enum q4nx_status {
+  Q4NX_OK = 0,
+  Q4NX_ERR_INVALID_ARG = 1,      /* NULL pointer, unknown dtype, code > 15, scale/offset outside the domain */
+  Q4NX_ERR_SHAPE = 2,            /* M, N or K <= 0, K % 32 != 0, or a size beyond the supported range */
+  Q4NX_ERR_ALIGNMENT = 3,        /* device pointer not aligned as documented */
+  Q4NX_ERR_BUFFER_TOO_SMALL = 4, /* blob_bytes < q4nx_packed_size(N, K) */
+  Q4NX_ERR_HIP = 5               /* a HIP runtime call or kernel launch failed */
+} q4nx_status;
+
+typedef enum q4nx_dtype {
+  Q4NX_F32 = 0,  /* float32 */
+  Q4NX_BF16 = 1  /* bfloat16, round to nearest even from the float32 value */
+} q4nx_dtype;
+
+/* Largest N and K accepted by every call (both < 2^31). */
+#define Q4NX_MAX_DIM ((int64_t)1 << 30)
+
+/*
+ * Bytes of a packed N x K matrix: ceil(N/32) * ceil(K/256) * 5120 (Sec. 3.1.1:
+ * 5120 bytes per 32 x 256 block).  Returns 0 if N <= 0, K <= 0, K % 32 != 0
+ * or either exceeds Q4NX_MAX_DIM.
+ */
+size_t q4nx_packed_size(int64_t N, int64_t K);
+
+/*
+ * Host, synchronous.  Packs a quantized matrix into the Q4NX layout above --
+ * the offline conversion of Sec. 3.1.1 (offsets pre-converted to bf16).
+ *   codes   : N*K bytes, row-major [N][K], each 0..15 (q of Eq. 3)
+ *   scales  : N*(K/32) bf16 bit patterns, row-major [N][K/32] (d_g of Eq. 3)
+ *   offsets : N*(K/32) bf16 bit patterns, row-major [N][K/32] (m_g of Eq. 3)
+ *   blob    : host buffer of blob_bytes >= q4nx_packed_size(N, K); all of
+ *             its first q4nx_packed_size(N, K) bytes are written (padding 0).
+ * Errors: Q4NX_ERR_INVALID_ARG (NULL pointer, code > 15, scale or offset
+ * outside the value domain -- checked before anything is written),
+ * Q4NX_ERR_SHAPE, Q4NX_ERR_BUFFER_TOO_SMALL.  Uses several host threads.
+ */
+q4nx_status q4nx_pack(const uint8_t* codes, const uint16_t* scales, const uint16_t* offsets,
+                      int64_t N, int64_t K, void* blob, size_t blob_bytes);
+
+/*
+ * Host, synchronous.  The inverse of q4nx_pack (a test and inspection aid):
+ * reads blob (blob_bytes >= q4nx_packed_size(N, K)) and writes codes [N][K],
+ * scales [N][K/32] and offsets [N][K/32].  Errors: Q4NX_ERR_INVALID_ARG,
+ * Q4NX_ERR_SHAPE, Q4NX_ERR_BUFFER_TOO_SMALL.
+ */
+q4nx_status q4nx_unpack(const void* blob, size_t blob_bytes, int64_t N, int64_t K,
+                        uint8_t* codes, uint16_t* scales, uint16_t* offsets);
+
+/*
+ * Device.  The dequantization engine of Sec. 3.1.1: writes every weight of
+ * the packed matrix, dequantized with Eq. 3, to d_W (row-major [N][K]).
+ *   d_blob  : device, q4nx_packed_size(N, K) bytes, 16-byte aligned
+ *   d_W     : device, N*K elements of w_dtype, 16-byte aligned
+ *   w_dtype : Q4NX_F32 -> RN_fp32(d*q + m) exactly;
+ *             Q4NX_BF16 -> that value rounded to bf16 (nearest even)
+ * Errors: Q4NX_ERR_INVALID_ARG, Q4NX_ERR_SHAPE, Q4NX_ERR_ALIGNMENT, Q4NX_ERR_HIP.
+ */
+q4nx_status q4nx_dequant(const void* d_blob, int64_t N, int64_t K,
+                         void* d_W, q4nx_dtype w_dtype, hipStream_t stream);
+
+/*
+ * Device.  FusedDQP (Sec. 3.2.1, Eq. 14/15): y[n] = sum_k w[n][k] * x[k] with
+ * w from Eq. 3, dequantized in registers and never written to memory; float32
+ * accumulation.
+ *   d_blob : device, packed N x K matrix, 16-byte aligned
+ *   d_x    : device, K bf16 values, 16-byte aligned
+ *   d_y    : device, N values of y_dtype, 4-byte aligned; fully overwritten
+ *            (no zeroing needed); nothing beyond N is written
+ * Errors: Q4NX_ERR_INVALID_ARG, Q4NX_ERR_SHAPE, Q4NX_ERR_ALIGNMENT, Q4NX_ERR_HIP.
+ */
+q4nx_status q4nx_gemv(const void* d_blob, const uint16_t* d_x, void* d_y, q4nx_dtype y_dtype,
+                      int64_t N, int64_t K, hipStream_t stream);
+
+/*
+ * One independent projection for q4nx_gemv_batched: y = W x as in q4nx_gemv.
+ */
+typedef struct q4nx_gemv_desc {
+  const void* blob;   /* device, packed N x K matrix, 16-byte aligned */
+  const uint16_t* x;  /* device, K bf16 values, 16-byte aligned */
+  void* y;            /* device, N outputs of the batch's y_dtype, 4-byte aligned */
+  int64_t N;
+  int64_t K;
+} q4nx_gemv_desc;
+
+#define Q4NX_MAX_BATCH 8
+
+/*
+ * Device.  Runs 1..Q4NX_MAX_BATCH independent FusedDQP projections in one
+ * launch -- e.g. the q/k/v projections of a layer, or gate/up, which read the
+ * same activation.  Each result equals what q4nx_gemv gives for that
+ * descriptor (bit for bit).  Outputs must not overlap inputs or each other.
+ * Errors: as q4nx_gemv, for any descriptor; Q4NX_ERR_INVALID_ARG for a
+ * count outside 1..Q4NX_MAX_BATCH.
+ */
+q4nx_status q4nx_gemv_batched(const q4nx_gemv_desc* descs, int32_t count, q4nx_dtype y_dtype,
+                              hipStream_t stream);
+
+/*
+ * Device.  Prefill projection (Sec. 3.1.2, C = A x B with A = X, B = W^T):
+ * Y[m][n] = sum_k X[m][k] * w[n][k], where each weight is dequantized with
+ * Eq. 3 and rounded to bf16 (the paper dequantizes to bf16 before its MM),
+ * the products are bf16 x bf16 on the matrix cores and the sums are float32.
+ *   d_X : device, row-major [M][K] bf16, 16-byte aligned, K*2 % 16 == 0
+ *         holds because K % 32 == 0
+ *   d_blob : device, packed N x K matrix, 16-byte aligned
+ *   d_Y : device, row-major [M][N] of y_dtype, 16-byte aligned; fully
+ *         overwritten, nothing outside [M][N] is written
+ * Errors: Q4NX_ERR_INVALID_ARG, Q4NX_ERR_SHAPE, Q4NX_ERR_ALIGNMENT, Q4NX_ERR_HIP.
+ */
+q4nx_status q4nx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_blob,
+                      void* d_Y, q4nx_dtype y_dtype, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* q4nx_status_str(q4nx_status status);
+
+/* Details of the last error reported on the calling thread ("" if none). */
+const char* q4nx_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* Q4NX_H */

@@ -1,0 +1,183 @@
+"""Python binding of libq4nx.so (ctypes): argument marshalling only.
+
+Every function has the name of the C entry point it calls (include/q4nx.h).
+Host functions take and return NumPy arrays; device functions take torch
+tensors that live on the GPU (torch provides device memory and streams) and
+enqueue the library's HIP kernels on the current torch stream, or on the
+stream passed explicitly.  Nothing here computes any part of the projection.
+
+If the shared library is missing this module raises at import: there is no
+fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libq4nx.so")
+
+Q4NX_OK = 0
+Q4NX_ERR_INVALID_ARG = 1
+Q4NX_ERR_SHAPE = 2
+Q4NX_ERR_ALIGNMENT = 3
+Q4NX_ERR_BUFFER_TOO_SMALL = 4
+Q4NX_ERR_HIP = 5
+Q4NX_F32 = 0
+Q4NX_BF16 = 1
+Q4NX_MAX_BATCH = 8
+
+EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_dequant", "q4nx_gemv",
+            "q4nx_gemv_batched", "q4nx_gemm", "q4nx_status_str", "q4nx_last_error"]
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2602_06063_amd.build`")
+
+lib = ctypes.CDLL(LIB_PATH)
+
+_vp, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t
+
+
+class q4nx_gemv_desc(ctypes.Structure):
+    _fields_ = [("blob", _vp), ("x", _vp), ("y", _vp), ("N", _i64), ("K", _i64)]
+
+
+lib.q4nx_packed_size.argtypes = [_i64, _i64]
+lib.q4nx_packed_size.restype = _sz
+lib.q4nx_pack.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp, _sz]
+lib.q4nx_pack.restype = ctypes.c_int
+lib.q4nx_unpack.argtypes = [_vp, _sz, _i64, _i64, _vp, _vp, _vp]
+lib.q4nx_unpack.restype = ctypes.c_int
+lib.q4nx_dequant.argtypes = [_vp, _i64, _i64, _vp, ctypes.c_int, _vp]
+lib.q4nx_dequant.restype = ctypes.c_int
+lib.q4nx_gemv.argtypes = [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _vp]
+lib.q4nx_gemv.restype = ctypes.c_int
+lib.q4nx_gemv_batched.argtypes = [ctypes.POINTER(q4nx_gemv_desc), _i32, ctypes.c_int, _vp]
+lib.q4nx_gemv_batched.restype = ctypes.c_int
+lib.q4nx_gemm.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp]
+lib.q4nx_gemm.restype = ctypes.c_int
+lib.q4nx_status_str.argtypes = [ctypes.c_int]
+lib.q4nx_status_str.restype = ctypes.c_char_p
+lib.q4nx_last_error.argtypes = []
+lib.q4nx_last_error.restype = ctypes.c_char_p
+
+
+class Q4NXError(RuntimeError):
+    def __init__(self, status: int, fn: str):
+        self.status = status
+        msg = lib.q4nx_status_str(status).decode()
+        detail = lib.q4nx_last_error().decode()
+        super().__init__(f"{fn}: {msg} ({detail})" if detail else f"{fn}: {msg}")
+
+
+def _check(status: int, fn: str):
+    if status != Q4NX_OK:
+        raise Q4NXError(status, fn)
+
+
+def _np_ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+# ------------------------------------------------------------------ host
+def q4nx_packed_size(N: int, K: int) -> int:
+    return int(lib.q4nx_packed_size(N, K))
+
+
+def q4nx_pack(codes: np.ndarray, scales: np.ndarray, offsets: np.ndarray) -> np.ndarray:
+    """codes u8[N][K], scales/offsets bf16 bits u16[N][K/32] -> blob u8."""
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    N, K = codes.shape
+    scales = np.ascontiguousarray(scales, dtype=np.uint16)
+    offsets = np.ascontiguousarray(offsets, dtype=np.uint16)
+    if scales.size != N * (K // 32) or offsets.size != N * (K // 32):
+        raise ValueError("scales and offsets need N * K/32 entries")
+    size = q4nx_packed_size(N, K)
+    blob = np.empty(max(size, 1), dtype=np.uint8)
+    _check(lib.q4nx_pack(_np_ptr(codes), _np_ptr(scales), _np_ptr(offsets), N, K, _np_ptr(blob), size),
+           "q4nx_pack")
+    return blob[:size]
+
+
+def q4nx_unpack(blob: np.ndarray, N: int, K: int):
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    codes = np.empty((N, K), np.uint8)
+    scales = np.empty((N, max(K // 32, 1)), np.uint16)
+    offsets = np.empty((N, max(K // 32, 1)), np.uint16)
+    _check(lib.q4nx_unpack(_np_ptr(blob), blob.size, N, K, _np_ptr(codes), _np_ptr(scales), _np_ptr(offsets)),
+           "q4nx_unpack")
+    return codes, scales, offsets
+
+
+# ------------------------------------------------------------------ device
+def _stream(stream):
+    if stream is None:
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if hasattr(stream, "cuda_stream"):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _dptr(t) -> int:
+    if not t.is_cuda:
+        raise ValueError("expected a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError("expected a contiguous tensor")
+    return t.data_ptr()
+
+
+def _need(t, nbytes: int, what: str):
+    have = t.numel() * t.element_size()
+    if have < nbytes:
+        raise ValueError(f"{what}: {have} bytes, need {nbytes}")
+
+
+def _dtype_code(t) -> int:
+    import torch
+    if t.dtype == torch.float32:
+        return Q4NX_F32
+    if t.dtype == torch.bfloat16:
+        return Q4NX_BF16
+    raise ValueError("outputs must be float32 or bfloat16")
+
+
+def q4nx_dequant(blob, N: int, K: int, W, stream=None):
+    """W[N][K] (float32 or bfloat16 tensor) <- Eq. 3 of every packed weight."""
+    _need(blob, q4nx_packed_size(N, K), "blob")
+    _need(W, N * K * W.element_size(), "W")
+    _check(lib.q4nx_dequant(_dptr(blob), N, K, _dptr(W), _dtype_code(W), _stream(stream)), "q4nx_dequant")
+
+
+def q4nx_gemv(blob, x, y, N: int, K: int, stream=None):
+    """y[N] <- W x; x is a bf16 (or 16-bit bit-pattern) tensor of K values."""
+    _need(blob, q4nx_packed_size(N, K), "blob")
+    _need(x, 2 * K, "x")
+    _need(y, N * y.element_size(), "y")
+    _check(lib.q4nx_gemv(_dptr(blob), _dptr(x), _dptr(y), _dtype_code(y), N, K, _stream(stream)), "q4nx_gemv")
+
+
+def q4nx_gemv_batched(items, stream=None):
+    """items: sequence of (blob, x, y, N, K); all y share one dtype."""
+    items = list(items)
+    arr = (q4nx_gemv_desc * max(len(items), 1))()
+    for i, (blob, x, y, N, K) in enumerate(items):
+        _need(blob, q4nx_packed_size(N, K), "blob")
+        _need(x, 2 * K, "x")
+        _need(y, N * y.element_size(), "y")
+        arr[i] = q4nx_gemv_desc(_dptr(blob), _dptr(x), _dptr(y), N, K)
+    ydt = _dtype_code(items[0][2]) if items else Q4NX_F32
+    if any(_dtype_code(it[2]) != ydt for it in items):
+        raise ValueError("all outputs of a batch must share one dtype")
+    _check(lib.q4nx_gemv_batched(arr, len(items), ydt, _stream(stream)), "q4nx_gemv_batched")
+
+
+def q4nx_gemm(M: int, N: int, K: int, X, blob, Y, stream=None):
+    """Y[M][N] <- X[M][K] W^T with W dequantized to bf16."""
+    _need(blob, q4nx_packed_size(N, K), "blob")
+    _need(X, 2 * M * K, "X")
+    _need(Y, M * N * Y.element_size(), "Y")
+    _check(lib.q4nx_gemm(M, N, K, _dptr(X), _dptr(blob), _dptr(Y), _dtype_code(Y), _stream(stream)),
+           "q4nx_gemm")

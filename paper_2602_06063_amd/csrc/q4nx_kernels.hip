@@ -1,0 +1,617 @@
+// Device half of libq4nx for gfx950: the Q4NX dequantization kernel
+// (Sec. 3.1.1), the fused dequant mat-vec of the decode phase (FusedDQP,
+// Sec. 3.2.1, Eq. 14/15) and the fused dequant matrix product of the prefill
+// phase (Sec. 3.1.2), with their C-ABI launchers.
+//
+// Common lane mapping inside a 32 x 256 block: a 16-byte load by lane l at
+// byte 1024t + 16l of the block holds the 32 codes of one quantization group,
+// row r = 8t + l/8, group c = l%8 (columns 32c..32c+31).  So a wave reads a
+// whole block with four fully coalesced 1 KiB loads, and the scale/offset of
+// the lane's group sits at index 8r + c = 64t + l of the block's tables.
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "q4nx_internal.h"
+
+namespace q4nx {
+
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+// ---------------------------------------------------------------------------
+// device helpers
+// ---------------------------------------------------------------------------
+
+// Hides the known bits of a value from the optimizer, so that byte extraction
+// of a masked word maps onto v_cvt_f32_ubyte{0..3} (one op per code) instead
+// of a per-code AND followed by a convert.
+__device__ __forceinline__ uint32_t opaque(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  bf16x2 p = __builtin_convertvector((float __attribute__((ext_vector_type(2)))){a, b}, bf16x2);
+  return __builtin_bit_cast(uint32_t, p);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_bits(float a) {
+  return (uint16_t)(pack_bf16x2(a, 0.0f) & 0xFFFFu);
+}
+
+// Streaming loads of the packed weights (read once per call).
+__device__ __forceinline__ u32x4 load_codes(const uint8_t* p) {
+  return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
+}
+__device__ __forceinline__ uint32_t load_u16(const uint8_t* p) {
+  return (uint32_t)__builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(p));
+}
+
+// The 32 codes of one group as float32 (exact), in column order.
+__device__ __forceinline__ void codes_to_f32(u32x4 q, float (&f)[32]) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const uint32_t lo = opaque(q[u] & 0x0F0F0F0Fu);   // even columns
+    const uint32_t hi = opaque((q[u] >> 4) & 0x0F0F0F0Fu);  // odd columns
+    f[8 * u + 0] = (float)(lo & 0xFFu);
+    f[8 * u + 1] = (float)(hi & 0xFFu);
+    f[8 * u + 2] = (float)((lo >> 8) & 0xFFu);
+    f[8 * u + 3] = (float)((hi >> 8) & 0xFFu);
+    f[8 * u + 4] = (float)((lo >> 16) & 0xFFu);
+    f[8 * u + 5] = (float)((hi >> 16) & 0xFFu);
+    f[8 * u + 6] = (float)(lo >> 24);
+    f[8 * u + 7] = (float)(hi >> 24);
+  }
+}
+
+// sum_i q_i * x_i over one group: even columns from the low nibbles, odd
+// columns from the high nibbles kept in place (16 q), rescaled by 2^-4 once
+// (exact), two independent accumulation chains.
+__device__ __forceinline__ float group_dot(u32x4 q, const float (&x)[32]) {
+  float a = 0.0f, b = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const uint32_t lo = opaque(q[u] & 0x0F0F0F0Fu);
+    const uint32_t hi = opaque(q[u] & 0xF0F0F0F0u);
+    a = fmaf((float)(lo & 0xFFu), x[8 * u + 0], a);
+    b = fmaf((float)(hi & 0xFFu), x[8 * u + 1], b);
+    a = fmaf((float)((lo >> 8) & 0xFFu), x[8 * u + 2], a);
+    b = fmaf((float)((hi >> 8) & 0xFFu), x[8 * u + 3], b);
+    a = fmaf((float)((lo >> 16) & 0xFFu), x[8 * u + 4], a);
+    b = fmaf((float)((hi >> 16) & 0xFFu), x[8 * u + 5], b);
+    a = fmaf((float)(lo >> 24), x[8 * u + 6], a);
+    b = fmaf((float)(hi >> 24), x[8 * u + 7], b);
+  }
+  return fmaf(b, 0.0625f, a);
+}
+
+// ---------------------------------------------------------------------------
+// q4nx_dequant: Eq. 3 for every weight, written row-major [N][K]
+// ---------------------------------------------------------------------------
+// One workgroup of 256 threads per block; thread (t, l) handles the group at
+// row 8t + l/8, columns 32(l%8)..+31.  Eight lanes write one row's 256
+// contiguous outputs.  d*q is exact, so fmaf(q, d, m) == RN(d*q + m).
+__global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict__ blob, int64_t N, int64_t K,
+                                                      int64_t KB, int64_t nblocks, void* __restrict__ W,
+                                                      int w_bf16) {
+  const int t = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = 8 * t + (lane >> 3), c = lane & 7;
+  for (int64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
+    const int64_t i = b / KB, j = b - i * KB;
+    const int64_t n = i * kBlockRows + r;
+    const int64_t k0 = j * kBlockCols + kGroup * c;
+    if (n >= N || k0 >= K) continue;
+    const uint8_t* blk = blob + b * kBlockBytes;
+    const u32x4 q = load_codes(blk + 1024 * t + 16 * lane);
+    const float d = bf16_to_f32(load_u16(blk + kCodeBytes + 2 * (64 * t + lane)));
+    const float m = bf16_to_f32(load_u16(blk + kCodeBytes + kScaleBytes + 2 * (64 * t + lane)));
+    float f[32];
+    codes_to_f32(q, f);
+#pragma unroll
+    for (int e = 0; e < 32; ++e) f[e] = fmaf(f[e], d, m);
+    if (w_bf16) {
+      u32x4* out = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(W) + n * K + k0);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        u32x4 o;
+        o[0] = pack_bf16x2(f[8 * v + 0], f[8 * v + 1]);
+        o[1] = pack_bf16x2(f[8 * v + 2], f[8 * v + 3]);
+        o[2] = pack_bf16x2(f[8 * v + 4], f[8 * v + 5]);
+        o[3] = pack_bf16x2(f[8 * v + 6], f[8 * v + 7]);
+        __builtin_nontemporal_store(o, out + v);
+      }
+    } else {
+      f32x4* out = reinterpret_cast<f32x4*>(static_cast<float*>(W) + n * K + k0);
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        f32x4 o = {f[4 * v + 0], f[4 * v + 1], f[4 * v + 2], f[4 * v + 3]};
+        __builtin_nontemporal_store(o, out + v);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// q4nx_gemv / q4nx_gemv_batched: FusedDQP
+// ---------------------------------------------------------------------------
+// A workgroup of 4 waves owns 4 consecutive 32-row strips and one range of
+// blocks along K (a "split").  The split's slice of x is staged once in LDS as
+// float32 together with its group sums S_g = sum_{k in g} x_k, so that each
+// row accumulates
+//     y_n += d_g * (sum_{k in g} q_k x_k) + m_g * S_g          (Eq. 3 in Eq. 15)
+// and the per-weight work is one convert and one FMA.  Each wave streams its
+// strip's blocks (four 1 KiB loads per block), prefetching the next block
+// while it computes the current one.  Lane l accumulates rows 8t + l/8
+// (t = 0..3) for group l%8; a 3-step butterfly adds the 8 groups of a row.
+// With several splits per strip, each wave stores its 32 partial sums, and
+// the last wave to arrive at the strip's counter adds the partials in split
+// order (so the result is deterministic) and resets the counter.
+constexpr int kGemvWaves = 4;
+constexpr int kGemvThreads = 64 * kGemvWaves;
+constexpr int kGemvMaxBpw = 16;  // blocks per split: LDS holds 16 x 256 floats
+
+struct GemvJob {
+  const uint8_t* blob;
+  const uint16_t* x;
+  void* y;
+  float* partial;      // [NS][ksplit][32] if ksplit > 1
+  unsigned* counter;   // [NS] if ksplit > 1, all zero between calls
+  int N, K, NS, KB;
+  int ksplit, bpw;
+  int wg_begin;        // first workgroup of this job in the launch
+  int pad;
+};
+
+struct GemvArgs {
+  GemvJob job[Q4NX_MAX_BATCH];
+  int njobs;
+  int y_bf16;
+};
+
+struct GemvBlockRegs {
+  u32x4 q[4];
+  uint32_t s[4], m[4];
+};
+
+__device__ __forceinline__ void gemv_load_block(const uint8_t* blk, bool ok, int lane, GemvBlockRegs& R) {
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    if (ok) {
+      R.q[t] = load_codes(blk + 1024 * t + 16 * lane);
+      R.s[t] = load_u16(blk + kCodeBytes + 2 * (64 * t + lane));
+      R.m[t] = load_u16(blk + kCodeBytes + kScaleBytes + 2 * (64 * t + lane));
+    } else {
+      R.q[t] = (u32x4){0u, 0u, 0u, 0u};
+      R.s[t] = 0u;
+      R.m[t] = 0u;
+    }
+  }
+}
+
+__device__ __forceinline__ void gemv_compute_block(const GemvBlockRegs& R, const float* __restrict__ xg, float S,
+                                                   float (&acc)[4]) {
+  float x[32];
+#pragma unroll
+  for (int v = 0; v < 8; ++v) {
+    const f32x4 xv = *reinterpret_cast<const f32x4*>(xg + 4 * v);
+    x[4 * v + 0] = xv[0];
+    x[4 * v + 1] = xv[1];
+    x[4 * v + 2] = xv[2];
+    x[4 * v + 3] = xv[3];
+  }
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    const float dot = group_dot(R.q[t], x);
+    acc[t] = fmaf(bf16_to_f32(R.s[t]), dot, acc[t]);
+    acc[t] = fmaf(bf16_to_f32(R.m[t]), S, acc[t]);
+  }
+}
+
+__global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const GemvArgs args) {
+  __shared__ float xs[kGemvMaxBpw * kBlockCols];
+  __shared__ float ssum[kGemvMaxBpw * kGroupsPerRow];
+
+  const int wg = blockIdx.x;
+  int jb = 0;
+#pragma unroll
+  for (int t = 1; t < Q4NX_MAX_BATCH; ++t)
+    if (t < args.njobs && wg >= args.job[t].wg_begin) jb = t;
+  const GemvJob& J = args.job[jb];
+
+  const int local = wg - J.wg_begin;
+  const int sg = local / J.ksplit;
+  const int sp = local - sg * J.ksplit;
+  const int j0 = sp * J.bpw;
+  const int nb = min(J.KB, j0 + J.bpw) - j0;
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = lane & 7;
+  const int strip = sg * kGemvWaves + w;
+  const bool active = strip < J.NS;  // wave-uniform
+  const bool loads = active && nb > 0;
+  const uint8_t* sblob = J.blob + (size_t)strip * J.KB * kBlockBytes;
+
+  // Issue the first block's loads before staging x so both latencies overlap.
+  GemvBlockRegs A, B;
+  gemv_load_block(sblob + (size_t)j0 * kBlockBytes, loads && (j0 * kBlockCols + kGroup * c < J.K), lane, A);
+
+  // Stage x[j0*256 .. (j0+nb)*256) as float32 (zero beyond K) and the group sums.
+  {
+    const int kbeg = j0 * kBlockCols;
+    const uint32_t* x2 = reinterpret_cast<const uint32_t*>(J.x);
+    for (int e = threadIdx.x; e < nb * (kBlockCols / 2); e += kGemvThreads) {
+      const int k = kbeg + 2 * e;
+      const uint32_t v = (k < J.K) ? x2[k >> 1] : 0u;
+      const float xa = __uint_as_float(v << 16), xb = __uint_as_float(v & 0xFFFF0000u);
+      xs[2 * e] = xa;
+      xs[2 * e + 1] = xb;
+      float s = xa + xb;
+      s += __shfl_xor(s, 1);
+      s += __shfl_xor(s, 2);
+      s += __shfl_xor(s, 4);
+      s += __shfl_xor(s, 8);
+      if ((threadIdx.x & 15) == 0) ssum[e >> 4] = s;
+    }
+  }
+  __syncthreads();
+
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  for (int jj = 0; jj < nb; jj += 2) {
+    const int k1 = (j0 + jj + 1) * kBlockCols + kGroup * c;
+    if (jj + 1 < nb) gemv_load_block(sblob + (size_t)(j0 + jj + 1) * kBlockBytes, active && k1 < J.K, lane, B);
+    gemv_compute_block(A, xs + jj * kBlockCols + kGroup * c, ssum[jj * kGroupsPerRow + c], acc);
+    if (jj + 1 < nb) {
+      const int k2 = (j0 + jj + 2) * kBlockCols + kGroup * c;
+      if (jj + 2 < nb) gemv_load_block(sblob + (size_t)(j0 + jj + 2) * kBlockBytes, active && k2 < J.K, lane, A);
+      gemv_compute_block(B, xs + (jj + 1) * kBlockCols + kGroup * c, ssum[(jj + 1) * kGroupsPerRow + c], acc);
+    }
+  }
+
+  // Add the 8 groups of each row (lanes 8s..8s+7 hold row 8t + s).
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    acc[t] += __shfl_xor(acc[t], 1);
+    acc[t] += __shfl_xor(acc[t], 2);
+    acc[t] += __shfl_xor(acc[t], 4);
+  }
+  // Lane with c < 4 owns row 8c + l/8 of the strip.
+  const float v = (c == 0) ? acc[0] : (c == 1) ? acc[1] : (c == 2) ? acc[2] : acc[3];
+  const int row = 8 * c + (lane >> 3);
+  const int64_t n = (int64_t)strip * kBlockRows + row;
+
+  if (J.ksplit == 1) {
+    if (active && c < 4 && n < J.N) {
+      if (args.y_bf16)
+        static_cast<uint16_t*>(J.y)[n] = f32_to_bf16_bits(v);
+      else
+        static_cast<float*>(J.y)[n] = v;
+    }
+    return;
+  }
+  if (!active) return;  // wave-uniform
+
+  float* P = J.partial + (size_t)strip * J.ksplit * kBlockRows;
+  if (c < 4) __hip_atomic_store(P + (size_t)sp * kBlockRows + row, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __threadfence();
+  unsigned old = 0;
+  if (lane == 0) old = atomicAdd(J.counter + strip, 1u);
+  old = __shfl(old, 0);
+  if (old != (unsigned)(J.ksplit - 1)) return;
+  __threadfence();
+  if (lane < kBlockRows) {
+    float s = 0.0f;
+    for (int q = 0; q < J.ksplit; ++q)
+      s += __hip_atomic_load(P + (size_t)q * kBlockRows + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int64_t nn = (int64_t)strip * kBlockRows + lane;
+    if (nn < J.N) {
+      if (args.y_bf16)
+        static_cast<uint16_t*>(J.y)[nn] = f32_to_bf16_bits(s);
+      else
+        static_cast<float*>(J.y)[nn] = s;
+    }
+  }
+  if (lane == 0) __hip_atomic_store(J.counter + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------------------
+// q4nx_gemm: fused dequant + bf16 MFMA matrix product
+// ---------------------------------------------------------------------------
+// Workgroup tile 128 (tokens) x 128 (outputs), K step 64 (two groups), four
+// waves in a 2 x 2 arrangement, each owning 64 x 64 outputs as 2 x 2 tiles of
+// v_mfma_f32_32x32x16_bf16.  Per K step every thread stages 32 bf16 of X and
+// dequantizes one group (32 weights) of W -- Eq. 3 in float32, rounded to bf16
+// -- into LDS.  Rows are padded to 72 bf16 (144 B) so the 16-byte fragment
+// reads of 8 consecutive rows fall in distinct banks.
+constexpr int kBM = 128, kBN = 128, kBK = 64;
+constexpr int kLdsStride = kBK + 8;  // bf16 elements per LDS row
+
+__global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ X, const uint8_t* __restrict__ blob,
+                                                   void* __restrict__ Y, int M, int N, int K, int KB, int NS,
+                                                   int tiles_n, int y_bf16) {
+  __shared__ __attribute__((aligned(16))) uint16_t xs[kBM * kLdsStride];
+  __shared__ __attribute__((aligned(16))) uint16_t ws[kBN * kLdsStride];
+
+  const int tile = blockIdx.x;
+  const int bn = tile % tiles_n, bm = tile / tiles_n;
+  const int m0 = bm * kBM, n0 = bn * kBN;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  // staging role: row lr of the tile, half h (columns 32h..32h+31 of the K step)
+  const int lr = tid >> 1, h = tid & 1;
+  const int gm = m0 + lr, gn = n0 + lr;
+  const int strip = gn >> 5, r = gn & 31;
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
+
+  for (int k0 = 0; k0 < K; k0 += kBK) {
+    const int gk = k0 + 32 * h;
+    u32x4 xv[4];
+    if (gm < M && gk < K) {
+      const u32x4* src = reinterpret_cast<const u32x4*>(X + (size_t)gm * K + gk);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) xv[v] = src[v];
+    } else {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) xv[v] = (u32x4){0u, 0u, 0u, 0u};
+    }
+    u32x4 wv[4];
+    if (strip < NS && gk < K) {
+      const int j = gk >> 8, c = (gk & 255) >> 5;
+      const uint8_t* blk = blob + ((size_t)strip * KB + j) * kBlockBytes;
+      const u32x4 q = load_codes(blk + 128 * r + 16 * c);
+      const float d = bf16_to_f32(load_u16(blk + kCodeBytes + 2 * (8 * r + c)));
+      const float m = bf16_to_f32(load_u16(blk + kCodeBytes + kScaleBytes + 2 * (8 * r + c)));
+      float f[32];
+      codes_to_f32(q, f);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        wv[v][0] = pack_bf16x2(fmaf(f[8 * v + 0], d, m), fmaf(f[8 * v + 1], d, m));
+        wv[v][1] = pack_bf16x2(fmaf(f[8 * v + 2], d, m), fmaf(f[8 * v + 3], d, m));
+        wv[v][2] = pack_bf16x2(fmaf(f[8 * v + 4], d, m), fmaf(f[8 * v + 5], d, m));
+        wv[v][3] = pack_bf16x2(fmaf(f[8 * v + 6], d, m), fmaf(f[8 * v + 7], d, m));
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < 4; ++v) wv[v] = (u32x4){0u, 0u, 0u, 0u};
+    }
+    __syncthreads();
+    {
+      u32x4* xd = reinterpret_cast<u32x4*>(xs + lr * kLdsStride + 32 * h);
+      u32x4* wd = reinterpret_cast<u32x4*>(ws + lr * kLdsStride + 32 * h);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        xd[v] = xv[v];
+        wd[v] = wv[v];
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      const int kk = ks * 16 + 8 * (lane >> 5);
+      bf16x8 af[2], bfr[2];
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+        af[a] = *reinterpret_cast<const bf16x8*>(xs + (64 * wm + 32 * a + (lane & 31)) * kLdsStride + kk);
+#pragma unroll
+      for (int b = 0; b < 2; ++b)
+        bfr[b] = *reinterpret_cast<const bf16x8*>(ws + (64 * wn + 32 * b + (lane & 31)) * kLdsStride + kk);
+#pragma unroll
+      for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+          acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
+    }
+  }
+
+  // Accumulator element e of lane l: column l%32, row 8(e/4) + 4(l/32) + e%4.
+#pragma unroll
+  for (int a = 0; a < 2; ++a)
+#pragma unroll
+    for (int b = 0; b < 2; ++b) {
+      const int col = n0 + 64 * wn + 32 * b + (lane & 31);
+      if (col >= N) continue;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = m0 + 64 * wm + 32 * a + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        if (row < M) {
+          if (y_bf16)
+            static_cast<uint16_t*>(Y)[(size_t)row * N + col] = f32_to_bf16_bits(acc[a][b][e]);
+          else
+            static_cast<float*>(Y)[(size_t)row * N + col] = acc[a][b][e];
+        }
+      }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// per-device scratch for the split-K partial sums
+// ---------------------------------------------------------------------------
+constexpr size_t kPartialCap = size_t(1) << 22;  // floats (16 MiB)
+constexpr size_t kCounterCap = size_t(1) << 20;  // counters (4 MiB)
+
+struct Scratch {
+  float* partial = nullptr;
+  unsigned* counter = nullptr;
+};
+
+static std::mutex g_scratch_mu;
+static std::vector<Scratch> g_scratch;
+
+static q4nx_status get_scratch(Scratch& out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(Q4NX_ERR_HIP, "hipGetDevice failed");
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if ((int)g_scratch.size() <= dev) g_scratch.resize(dev + 1);
+  Scratch& s = g_scratch[dev];
+  if (!s.partial) {
+    void *p = nullptr, *c = nullptr;
+    if (hipMalloc(&p, kPartialCap * sizeof(float)) != hipSuccess)
+      return fail(Q4NX_ERR_HIP, "scratch allocation failed");
+    if (hipMalloc(&c, kCounterCap * sizeof(unsigned)) != hipSuccess) {
+      (void)hipFree(p);
+      return fail(Q4NX_ERR_HIP, "scratch allocation failed");
+    }
+    if (hipMemset(c, 0, kCounterCap * sizeof(unsigned)) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+      (void)hipFree(p);
+      (void)hipFree(c);
+      return fail(Q4NX_ERR_HIP, "scratch initialisation failed");
+    }
+    s.partial = static_cast<float*>(p);
+    s.counter = static_cast<unsigned*>(c);
+  }
+  out = s;
+  return Q4NX_OK;
+}
+
+static q4nx_status check_launch(const char* fn) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(Q4NX_ERR_HIP, std::string(fn) + ": " + hipGetErrorString(e));
+  return Q4NX_OK;
+}
+
+// Chooses blocks-per-split for one projection so that it alone launches
+// about `target_waves` waves: at least 2 blocks per wave (to amortise the x
+// staging and the reduction), at most kGemvMaxBpw (the LDS slice), balanced
+// across the splits of a strip.  The plan depends only on (N, K), so a
+// projection is summed in the same order whether launched alone or batched.
+// A split plan (ksplit > 1) implies bpw < KB and bpw >= NS*KB/2048, hence
+// NS < 2048: its scratch needs stay far below the scratch capacity.
+static void plan_split(int NS, int KB, int& ksplit, int& bpw) {
+  const int64_t target_waves = 2048;
+  const int64_t total_blocks = (int64_t)NS * KB;
+  int64_t b = (total_blocks + target_waves - 1) / target_waves;
+  b = std::max<int64_t>(2, std::min<int64_t>(kGemvMaxBpw, b));
+  b = std::min<int64_t>(b, KB);
+  ksplit = (int)((KB + b - 1) / b);
+  bpw = (KB + ksplit - 1) / ksplit;
+}
+
+static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtype y_dtype, hipStream_t stream,
+                               const char* fn) {
+  clear_error();
+  if (!descs || count < 1 || count > Q4NX_MAX_BATCH)
+    return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": need 1..8 descriptors");
+  if (y_dtype != Q4NX_F32 && y_dtype != Q4NX_BF16)
+    return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": unknown y_dtype");
+  bool need_split = false;
+  for (int i = 0; i < count; ++i) {
+    const q4nx_gemv_desc& d = descs[i];
+    if (q4nx_status st = check_shape(d.N, d.K, fn)) return st;
+    if (!d.blob || !d.x || !d.y) return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
+    if (!aligned(d.blob, 16) || !aligned(d.x, 16) || !aligned(d.y, 4))
+      return fail(Q4NX_ERR_ALIGNMENT, std::string(fn) + ": blob/x need 16-byte, y 4-byte alignment");
+  }
+  GemvArgs args = {};
+  args.njobs = count;
+  args.y_bf16 = (y_dtype == Q4NX_BF16);
+  int64_t wg = 0;
+  size_t part_off = 0, ctr_off = 0;
+  for (int i = 0; i < count; ++i) {
+    const q4nx_gemv_desc& d = descs[i];
+    GemvJob& J = args.job[i];
+    J.blob = static_cast<const uint8_t*>(d.blob);
+    J.x = d.x;
+    J.y = d.y;
+    J.N = (int)d.N;
+    J.K = (int)d.K;
+    J.NS = (int)ceil_div(d.N, kBlockRows);
+    J.KB = (int)ceil_div(d.K, kBlockCols);
+    plan_split(J.NS, J.KB, J.ksplit, J.bpw);
+    if (J.ksplit > 1) {
+      if (part_off + (size_t)J.NS * J.ksplit * kBlockRows > kPartialCap || ctr_off + (size_t)J.NS > kCounterCap)
+        return fail(Q4NX_ERR_SHAPE, std::string(fn) + ": problem exceeds the split-K scratch");
+      need_split = true;
+      J.partial = reinterpret_cast<float*>(part_off);   // rebased below
+      J.counter = reinterpret_cast<unsigned*>(ctr_off);
+      part_off += (size_t)J.NS * J.ksplit * kBlockRows;
+      ctr_off += (size_t)J.NS;
+    }
+    J.wg_begin = (int)wg;
+    wg += ceil_div(J.NS, kGemvWaves) * (int64_t)J.ksplit;
+    if (wg > 0x7FFFFFFF) return fail(Q4NX_ERR_SHAPE, std::string(fn) + ": grid too large");
+  }
+  if (need_split) {
+    Scratch s;
+    if (q4nx_status st = get_scratch(s)) return st;
+    for (int i = 0; i < count; ++i) {
+      GemvJob& J = args.job[i];
+      if (J.ksplit > 1) {
+        J.partial = s.partial + reinterpret_cast<size_t>(J.partial);
+        J.counter = s.counter + reinterpret_cast<size_t>(J.counter);
+      }
+    }
+  }
+  hipLaunchKernelGGL(gemv_kernel, dim3((unsigned)wg), dim3(kGemvThreads), 0, stream, args);
+  return check_launch(fn);
+}
+
+}  // namespace q4nx
+
+using namespace q4nx;
+
+extern "C" {
+
+q4nx_status q4nx_dequant(const void* d_blob, int64_t N, int64_t K, void* d_W, q4nx_dtype w_dtype,
+                         hipStream_t stream) {
+  clear_error();
+  if (q4nx_status st = check_shape(N, K, "q4nx_dequant")) return st;
+  if (!d_blob || !d_W) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_dequant: NULL pointer");
+  if (w_dtype != Q4NX_F32 && w_dtype != Q4NX_BF16)
+    return fail(Q4NX_ERR_INVALID_ARG, "q4nx_dequant: unknown w_dtype");
+  if (!aligned(d_blob, 16) || !aligned(d_W, 16))
+    return fail(Q4NX_ERR_ALIGNMENT, "q4nx_dequant: blob and W need 16-byte alignment");
+  const int64_t KB = ceil_div(K, kBlockCols);
+  const int64_t nblocks = ceil_div(N, kBlockRows) * KB;
+  const int64_t grid = std::min<int64_t>(nblocks, int64_t(1) << 20);
+  hipLaunchKernelGGL(dequant_kernel, dim3((unsigned)grid), dim3(256), 0, stream,
+                     static_cast<const uint8_t*>(d_blob), N, K, KB, nblocks, d_W, (int)(w_dtype == Q4NX_BF16));
+  return check_launch("q4nx_dequant");
+}
+
+q4nx_status q4nx_gemv(const void* d_blob, const uint16_t* d_x, void* d_y, q4nx_dtype y_dtype, int64_t N,
+                      int64_t K, hipStream_t stream) {
+  q4nx_gemv_desc d = {d_blob, d_x, d_y, N, K};
+  return gemv_launch(&d, 1, y_dtype, stream, "q4nx_gemv");
+}
+
+q4nx_status q4nx_gemv_batched(const q4nx_gemv_desc* descs, int32_t count, q4nx_dtype y_dtype,
+                              hipStream_t stream) {
+  return gemv_launch(descs, count, y_dtype, stream, "q4nx_gemv_batched");
+}
+
+q4nx_status q4nx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_blob, void* d_Y,
+                      q4nx_dtype y_dtype, hipStream_t stream) {
+  clear_error();
+  if (q4nx_status st = check_shape(N, K, "q4nx_gemm")) return st;
+  if (M <= 0 || M > Q4NX_MAX_DIM) return fail(Q4NX_ERR_SHAPE, "q4nx_gemm: M must lie in 1..2^30");
+  if (!d_X || !d_blob || !d_Y) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_gemm: NULL pointer");
+  if (y_dtype != Q4NX_F32 && y_dtype != Q4NX_BF16)
+    return fail(Q4NX_ERR_INVALID_ARG, "q4nx_gemm: unknown y_dtype");
+  if (!aligned(d_X, 16) || !aligned(d_blob, 16) || !aligned(d_Y, 16))
+    return fail(Q4NX_ERR_ALIGNMENT, "q4nx_gemm: X, blob and Y need 16-byte alignment");
+  const int64_t tiles_n = ceil_div(N, kBN), tiles_m = ceil_div(M, kBM);
+  if (tiles_n * tiles_m > 0x7FFFFFFF || M * N > (int64_t(1) << 40))
+    return fail(Q4NX_ERR_SHAPE, "q4nx_gemm: problem too large for one launch");
+  hipLaunchKernelGGL(gemm_kernel, dim3((unsigned)(tiles_n * tiles_m)), dim3(256), 0, stream, d_X,
+                     static_cast<const uint8_t*>(d_blob), d_Y, (int)M, (int)N, (int)K,
+                     (int)ceil_div(K, kBlockCols), (int)ceil_div(N, kBlockRows), (int)tiles_n,
+                     (int)(y_dtype == Q4NX_BF16));
+  return check_launch("q4nx_gemm");
+}
+
+}  // extern "C"

@@ -1,0 +1,178 @@
+"""The C ABI on the host: the library loads and exports every entry point the
+header declares; q4nx_pack / q4nx_unpack agree with the oracle byte for byte;
+every argument error is reported before any HIP call (so these run without a
+GPU: the device entry points are only called with invalid arguments)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+import paper_2602_06063_amd as q4
+from workloads import gen_weights, gen_edge_weights, MODELS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "q4nx.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(q4nx_[a-z_0-9]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared_functions()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(q4.lib, n), n
+    assert sorted(q4.EXPORTED) == names
+
+
+@pytest.mark.parametrize("N,K", [(1, 32), (32, 256), (33, 288), (1024, 1152), (1024, 2560), (300, 5376), (64, 21504)])
+def test_packed_size_matches_oracle(N, K):
+    assert q4.q4nx_packed_size(N, K) == oracle.packed_size(N, K)
+
+
+def test_packed_size_rejects():
+    for N, K in [(0, 256), (-1, 256), (32, 0), (32, 33), (32, 48), (1 << 31, 256), (32, 1 << 31)]:
+        assert q4.q4nx_packed_size(N, K) == 0
+
+
+SHAPES = [(1, 32, "zp"), (32, 256, "zp"), (33, 288, "literal"), (100, 1152, "zp"), (1024, 1152, "zp"),
+          (256, 2560, "literal"), (64, 5376, "zp"), (40, 10240, "zp"), (70, 800, "edge")]
+
+
+@pytest.mark.parametrize("N,K,mode", SHAPES)
+def test_pack_bit_exact_vs_oracle_and_roundtrip(N, K, mode):
+    if mode == "edge":
+        codes, s, o = gen_edge_weights(N, K, seed=1)
+    else:
+        codes, s, o = gen_weights(N, K, seed=N + K, offset_mode=mode)
+    blob = q4.q4nx_pack(codes, s, o)
+    ref = oracle.pack(codes, s, o)
+    assert blob.size == ref.size
+    assert np.array_equal(blob, ref)
+    c2, s2, o2 = q4.q4nx_unpack(blob, N, K)
+    assert np.array_equal(c2, codes) and np.array_equal(s2, s) and np.array_equal(o2, o)
+
+
+def test_pack_full_size_projection_shape_is_bit_exact():
+    # a real Gemma3-4B shape (gate 10240 x 2560) through the threaded packer
+    N, K = MODELS["4b"]["proj"][4][1:]
+    codes, s, o = gen_weights(N, K, seed=0, layer=0, proj=4)
+    assert np.array_equal(q4.q4nx_pack(codes, s, o), oracle.pack(codes, s, o))
+
+
+def _raw_pack(codes, s, o, N, K, blob_bytes):
+    blob = np.zeros(max(blob_bytes, 1), np.uint8)
+    st = q4.lib.q4nx_pack(q4._np_ptr(codes), q4._np_ptr(s), q4._np_ptr(o), N, K, q4._np_ptr(blob), blob_bytes)
+    return st, blob
+
+
+def test_pack_error_paths():
+    N, K = 32, 256
+    codes, s, o = gen_weights(N, K, seed=3)
+    size = q4.q4nx_packed_size(N, K)
+    st, _ = _raw_pack(codes, s, o, N, K, size)
+    assert st == q4.Q4NX_OK
+    # shapes
+    assert _raw_pack(codes, s, o, 0, K, size)[0] == q4.Q4NX_ERR_SHAPE
+    assert _raw_pack(codes, s, o, N, 48, size)[0] == q4.Q4NX_ERR_SHAPE
+    assert _raw_pack(codes, s, o, N, -32, size)[0] == q4.Q4NX_ERR_SHAPE
+    # blob too small
+    assert _raw_pack(codes, s, o, N, K, size - 1)[0] == q4.Q4NX_ERR_BUFFER_TOO_SMALL
+    # NULL pointers
+    blob = np.zeros(size, np.uint8)
+    for args in [(None, q4._np_ptr(s), q4._np_ptr(o)), (q4._np_ptr(codes), None, q4._np_ptr(o)),
+                 (q4._np_ptr(codes), q4._np_ptr(s), None)]:
+        assert q4.lib.q4nx_pack(*args, N, K, q4._np_ptr(blob), size) == q4.Q4NX_ERR_INVALID_ARG
+    assert q4.lib.q4nx_pack(q4._np_ptr(codes), q4._np_ptr(s), q4._np_ptr(o), N, K, None, size) == q4.Q4NX_ERR_INVALID_ARG
+    # a code above 15 anywhere, checked before anything is written
+    bad = codes.copy()
+    bad[17, 201] = 16
+    st, blob = _raw_pack(bad, s, o, N, K, size)
+    assert st == q4.Q4NX_ERR_INVALID_ARG and not blob.any()
+    assert "code" in q4.lib.q4nx_last_error().decode()
+    # scales / offsets outside {0} U [2^-100, 2^101): inf, nan, 2^-101, 2^101, subnormal
+    for bits in (0x7F80, 0xFF80, 0x7FC0, 0x0D00, 0x8D00, 0x7200, 0xF200, 0x0001):
+        s2 = s.copy()
+        s2[5, 3] = bits
+        assert _raw_pack(codes, s2, o, N, K, size)[0] == q4.Q4NX_ERR_INVALID_ARG, hex(bits)
+        o2 = o.copy()
+        o2[31, 7] = bits
+        assert _raw_pack(codes, s, o2, N, K, size)[0] == q4.Q4NX_ERR_INVALID_ARG, hex(bits)
+    # domain edges are accepted: +-0, +-2^-100, just below +-2^101
+    for bits in (0x0000, 0x8000, 0x0D80, 0x8D80, 0x71FF, 0xF1FF):
+        s2 = s.copy()
+        s2[0, 0] = bits
+        assert _raw_pack(codes, s2, o, N, K, size)[0] == q4.Q4NX_OK, hex(bits)
+
+
+def test_unpack_error_paths():
+    N, K = 32, 256
+    codes, s, o = gen_weights(N, K, seed=3)
+    blob = q4.q4nx_pack(codes, s, o)
+    c = np.empty((N, K), np.uint8)
+    ss = np.empty((N, K // 32), np.uint16)
+    oo = np.empty((N, K // 32), np.uint16)
+    P = q4._np_ptr
+    assert q4.lib.q4nx_unpack(P(blob), blob.size - 1, N, K, P(c), P(ss), P(oo)) == q4.Q4NX_ERR_BUFFER_TOO_SMALL
+    assert q4.lib.q4nx_unpack(None, blob.size, N, K, P(c), P(ss), P(oo)) == q4.Q4NX_ERR_INVALID_ARG
+    assert q4.lib.q4nx_unpack(P(blob), blob.size, N, 40, P(c), P(ss), P(oo)) == q4.Q4NX_ERR_SHAPE
+
+
+# Device entry points: only invalid arguments here, which must be rejected on
+# the host before any HIP call (pointers below are never dereferenced).
+A16 = 0x10000
+MIS = 0x10002
+
+
+def test_device_calls_validate_before_hip():
+    L = q4.lib
+    # dequant
+    assert L.q4nx_dequant(None, 32, 256, A16, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_dequant(A16, 32, 250, A16, 0, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_dequant(A16, 0, 256, A16, 0, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_dequant(MIS, 32, 256, A16, 0, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_dequant(A16, 32, 256, MIS, 1, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_dequant(A16, 32, 256, A16, 7, None) == q4.Q4NX_ERR_INVALID_ARG
+    # gemv
+    assert L.q4nx_gemv(None, A16, A16, 0, 32, 256, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_gemv(A16, None, A16, 0, 32, 256, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_gemv(A16, A16, None, 0, 32, 256, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_gemv(A16, A16, A16, 0, 32, 100, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_gemv(A16, A16, A16, 0, -5, 256, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_gemv(A16, A16, A16, 0, 32, (1 << 30) + 32, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_gemv(MIS, A16, A16, 0, 32, 256, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_gemv(A16, MIS, A16, 0, 32, 256, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_gemv(A16, A16, MIS, 0, 32, 256, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_gemv(A16, A16, A16, 2, 32, 256, None) == q4.Q4NX_ERR_INVALID_ARG
+    # gemv_batched
+    arr = (q4.q4nx_gemv_desc * 9)()
+    for i in range(9):
+        arr[i] = q4.q4nx_gemv_desc(A16, A16, A16, 32, 256)
+    assert L.q4nx_gemv_batched(arr, 0, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_gemv_batched(arr, 9, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_gemv_batched(None, 1, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    arr[2] = q4.q4nx_gemv_desc(A16, A16, A16, 32, 40)
+    assert L.q4nx_gemv_batched(arr, 3, 0, None) == q4.Q4NX_ERR_SHAPE
+    arr[2] = q4.q4nx_gemv_desc(A16, MIS, A16, 32, 256)
+    assert L.q4nx_gemv_batched(arr, 3, 0, None) == q4.Q4NX_ERR_ALIGNMENT
+    # gemm
+    assert L.q4nx_gemm(0, 32, 256, A16, A16, A16, 0, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_gemm(4, 32, 80, A16, A16, A16, 0, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_gemm(4, 32, 256, None, A16, A16, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_gemm(4, 32, 256, A16, None, A16, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_gemm(4, 32, 256, A16, A16, None, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_gemm(4, 32, 256, MIS, A16, A16, 0, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_gemm(4, 32, 256, A16, MIS, A16, 0, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_gemm(4, 32, 256, A16, A16, MIS, 0, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_gemm(4, 32, 256, A16, A16, A16, 3, None) == q4.Q4NX_ERR_INVALID_ARG
+
+
+def test_status_strings():
+    for st in range(6):
+        assert q4.lib.q4nx_status_str(st).decode()
+    assert q4.lib.q4nx_status_str(99).decode() == "unknown status"

@@ -1,0 +1,263 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+  * q4nx_dequant: bit-exact, float32 and bf16 outputs.
+  * q4nx_gemv / q4nx_gemv_batched: |y - y_ref| <= 2e-3 * sum_k |x_k w_k| + 1e-5
+    per output (bf16 outputs: plus half a bf16 ulp of y_ref); unit vectors
+    extract a column bit-exactly; batched == single bit for bit; repeated
+    calls are bitwise identical.
+  * q4nx_gemm: the same tolerance against the float64 oracle, and a tighter
+    diagnostic against the float64 product with the bf16-rounded weights the
+    matrix cores consume.
+Shapes: tiny, ragged (N % 32 != 0, K % 256 != 0, M not a tile multiple),
+every Gemma3 projection shape at full size, edge-valued weights.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from workloads import gen_weights, gen_activations, gen_edge_weights, MODELS
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def q4():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2602_06063_amd as mod
+    return mod
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def dev_u8(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def dev_bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def host_f32(t):
+    torch.cuda.synchronize()
+    return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+
+def host_bits16(t):
+    torch.cuda.synchronize()
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def make(N, K, seed=0, mode="zp", layer=0, proj=0):
+    if mode == "edge":
+        codes, s, o = gen_edge_weights(N, K, seed=seed)
+    else:
+        codes, s, o = gen_weights(N, K, seed=seed, layer=layer, proj=proj, offset_mode=mode)
+    return codes, s, o
+
+
+# ----------------------------------------------------------------- dequant
+DEQ_SHAPES = [(1, 32, "zp"), (32, 256, "zp"), (33, 288, "literal"), (1024, 1152, "zp"), (100, 544, "edge"),
+              (2048, 5376, "zp"), (65, 21504, "zp")]
+
+
+@pytest.mark.parametrize("N,K,mode", DEQ_SHAPES)
+def test_dequant_bit_exact(q4, N, K, mode):
+    _say("dequant", N, K, mode)
+    codes, s, o = make(N, K, seed=N + K, mode=mode)
+    blob = q4.q4nx_pack(codes, s, o)
+    w32 = oracle.dequant_f32(codes, s, o)
+    db = dev_u8(blob)
+    W = torch.empty((N, K), dtype=torch.float32, device="cuda")
+    q4.q4nx_dequant(db, N, K, W)
+    assert np.array_equal(host_f32(W).view(np.uint32), w32.view(np.uint32))
+    Wb = torch.empty((N, K), dtype=torch.bfloat16, device="cuda")
+    q4.q4nx_dequant(db, N, K, Wb)
+    assert np.array_equal(host_bits16(Wb), oracle.f32_to_bf16(w32))
+
+
+# ----------------------------------------------------------------- gemv
+def _gemv_case(q4, N, K, seed, mode="zp", bf16_out=False, layer=0, proj=0):
+    codes, s, o = make(N, K, seed=seed, mode=mode, layer=layer, proj=proj)
+    blob = q4.q4nx_pack(codes, s, o)
+    x = gen_activations(K, seed=seed, layer=layer, proj=proj)
+    w32 = oracle.dequant_f32(codes, s, o)
+    y_ref = oracle.gemv_f64(w32, x)
+    bound = oracle.abs_bound(x, w32)
+    y = torch.empty(N, dtype=torch.bfloat16 if bf16_out else torch.float32, device="cuda")
+    q4.q4nx_gemv(dev_u8(blob), dev_bf16(x), y, N, K)
+    ok, worst = oracle.check_close(host_f32(y), y_ref, bound, bf16_out=bf16_out)
+    return ok, worst
+
+
+GEMV_SHAPES = [(1, 32), (32, 256), (33, 288), (64, 512), (1024, 1152), (100, 544), (257, 1184), (8, 4096),
+               (3000, 256), (40, 21504)]
+
+
+@pytest.mark.parametrize("N,K", GEMV_SHAPES)
+@pytest.mark.parametrize("mode", ["zp", "literal", "edge"])
+def test_gemv_parity_small(q4, N, K, mode):
+    _say("gemv", N, K, mode)
+    ok, worst = _gemv_case(q4, N, K, seed=N * 3 + K, mode=mode)
+    assert ok, worst
+
+
+FULL = [(m, p) for m in ("1b", "4b", "27b") for p in range(7)]
+
+
+@pytest.mark.parametrize("model,p", FULL)
+def test_gemv_parity_every_projection_full_size(q4, model, p):
+    name, N, K = MODELS[model]["proj"][p]
+    _say("gemv full", model, name, N, K)
+    ok, worst = _gemv_case(q4, N, K, seed=0, layer=0, proj=p)
+    assert ok, (model, name, worst)
+
+
+def test_gemv_bf16_output(q4):
+    for N, K in [(1024, 1152), (2560, 10240), (33, 288)]:
+        _say("gemv bf16 out", N, K)
+        ok, worst = _gemv_case(q4, N, K, seed=5, bf16_out=True)
+        assert ok, worst
+
+
+def test_gemv_lm_head_sampled_rows(q4):
+    """4B lm_head 262144 x 2560 at full size; the oracle checks sampled strips."""
+    N, K = MODELS["4b"]["lm_head"][1:]
+    _say("gemv lm_head", N, K)
+    codes, s, o = gen_weights(N, K, seed=0, layer=34, proj=7)
+    blob = q4.q4nx_pack(codes, s, o)
+    x = gen_activations(K, seed=0, layer=34, proj=7)
+    y = torch.empty(N, dtype=torch.float32, device="cuda")
+    q4.q4nx_gemv(dev_u8(blob), dev_bf16(x), y, N, K)
+    yh = host_f32(y)
+    rng = np.random.default_rng(0)
+    rows = np.unique(np.concatenate([np.arange(64), N - 64 + np.arange(64), rng.integers(0, N, 2048)]))
+    w32 = oracle.dequant_f32(codes[rows], s[rows], o[rows])
+    ok, worst = oracle.check_close(yh[rows], oracle.gemv_f64(w32, x), oracle.abs_bound(x, w32))
+    assert ok, worst
+
+
+def test_gemv_unit_vectors_extract_columns_bit_exact(q4):
+    N, K = 300, 1184
+    _say("gemv e_k", N, K)
+    codes, s, o = make(N, K, seed=8)
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    w32 = oracle.dequant_f32(codes, s, o)
+    for k in (0, 1, 31, 32, 255, 256, 511, 1024, 1183):
+        e = np.zeros(K, np.uint16)
+        e[k] = 0x3F80
+        y = torch.empty(N, dtype=torch.float32, device="cuda")
+        q4.q4nx_gemv(blob, dev_bf16(e), y, N, K)
+        assert np.array_equal(host_f32(y), w32[:, k]), k  # == treats +0 and -0 alike
+
+
+def test_gemv_integer_case_exact(q4):
+    """d = 1, m = 0 and small integer x: every partial sum is an exact integer."""
+    rng = np.random.default_rng(3)
+    N, K = 200, 2560
+    _say("gemv integer", N, K)
+    codes = rng.integers(0, 16, (N, K)).astype(np.uint8)
+    s = np.full((N, K // 32), 0x3F80, np.uint16)
+    o = np.zeros((N, K // 32), np.uint16)
+    xi = rng.integers(-4, 5, K)
+    x = oracle.f32_to_bf16(xi.astype(np.float32))
+    y = torch.empty(N, dtype=torch.float32, device="cuda")
+    q4.q4nx_gemv(dev_u8(q4.q4nx_pack(codes, s, o)), dev_bf16(x), y, N, K)
+    assert np.array_equal(host_f32(y), (codes.astype(np.int64) @ xi).astype(np.float32))
+
+
+def test_gemv_batched_equals_single_and_is_deterministic(q4):
+    shapes = MODELS["4b"]["proj"][:3] + [("x", 33, 288), ("y", 1000, 21504)]
+    items, singles = [], []
+    for p, (name, N, K) in enumerate(shapes):
+        codes, s, o = make(N, K, seed=p)
+        blob = dev_u8(q4.q4nx_pack(codes, s, o))
+        x = dev_bf16(gen_activations(K, seed=p))
+        yb = torch.empty(N, dtype=torch.float32, device="cuda")
+        ys = torch.empty(N, dtype=torch.float32, device="cuda")
+        items.append((blob, x, yb, N, K))
+        singles.append((blob, x, ys, N, K))
+    _say("gemv batched", [s[1:] for s in shapes])
+    q4.q4nx_gemv_batched(items)
+    for blob, x, ys, N, K in singles:
+        q4.q4nx_gemv(blob, x, ys, N, K)
+    for (_, _, yb, _, _), (_, _, ys, _, _) in zip(items, singles):
+        assert np.array_equal(host_f32(yb).view(np.uint32), host_f32(ys).view(np.uint32))
+    first = [host_f32(it[2]).copy() for it in items]
+    for _ in range(3):
+        q4.q4nx_gemv_batched(items)
+    for f, it in zip(first, items):
+        assert np.array_equal(f.view(np.uint32), host_f32(it[2]).view(np.uint32))
+
+
+# ----------------------------------------------------------------- gemm
+def _gemm_case(q4, M, N, K, seed, mode="zp", bf16_out=False, rows=None, layer=0, proj=0):
+    codes, s, o = make(N, K, seed=seed, mode=mode, layer=layer, proj=proj)
+    blob = q4.q4nx_pack(codes, s, o)
+    X = gen_activations((M, K), seed=seed, layer=layer, proj=proj)
+    Y = torch.empty((M, N), dtype=torch.bfloat16 if bf16_out else torch.float32, device="cuda")
+    q4.q4nx_gemm(M, N, K, dev_bf16(X), dev_u8(blob), Y)
+    Yh = host_f32(Y)
+    if rows is not None:
+        X, Yh = X[rows], Yh[rows]
+    w32 = oracle.dequant_f32(codes, s, o)
+    ref = oracle.gemm_f64(X, w32)
+    ok, worst = oracle.check_close(Yh, ref, oracle.abs_bound(X, w32), bf16_out=bf16_out)
+    # diagnostic: the float64 product with the bf16 weights the MFMA consumes
+    w16 = oracle.bf16_to_f32(oracle.f32_to_bf16(w32))
+    ref16 = oracle.gemm_f64(X, w16)
+    tight = np.abs(Yh.astype(np.float64) - ref16) <= (
+        1e-5 * oracle.abs_bound(X, w16) + 1e-6 + (2.0 ** -8 * np.abs(ref16) if bf16_out else 0))
+    return ok, worst, bool(tight.all())
+
+
+GEMM_SHAPES = [(1, 32, 256), (5, 33, 288), (130, 200, 1152), (64, 1024, 1152), (256, 512, 2560), (129, 257, 1184),
+               (128, 128, 64), (7, 3000, 96), (300, 96, 5376)]
+
+
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+@pytest.mark.parametrize("mode", ["zp", "edge"])
+def test_gemm_parity_small(q4, M, N, K, mode):
+    _say("gemm", M, N, K, mode)
+    ok, worst, tight = _gemm_case(q4, M, N, K, seed=M + N + K, mode=mode)
+    assert ok, worst
+    assert tight
+
+
+def test_gemm_bf16_output(q4):
+    _say("gemm bf16 out")
+    ok, worst, tight = _gemm_case(q4, 96, 320, 1152, seed=1, bf16_out=True)
+    assert ok and tight, worst
+
+
+def test_gemm_single_row_matches_gemv_within_tolerance(q4):
+    M, N, K = 1, 2048, 2560
+    _say("gemm M=1 vs gemv")
+    codes, s, o = make(N, K, seed=12)
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    x = gen_activations(K, seed=12)
+    y = torch.empty(N, dtype=torch.float32, device="cuda")
+    Y = torch.empty((1, N), dtype=torch.float32, device="cuda")
+    q4.q4nx_gemv(blob, dev_bf16(x), y, N, K)
+    q4.q4nx_gemm(M, N, K, dev_bf16(x), blob, Y)
+    w32 = oracle.dequant_f32(codes, s, o)
+    b = oracle.abs_bound(x, w32)
+    assert oracle.check_close(host_f32(Y)[0], host_f32(y), b)[0]
+
+
+@pytest.mark.parametrize("model,p", [(m, p) for m in ("4b", "27b") for p in range(7)])
+def test_gemm_full_size_sampled_rows(q4, model, p):
+    """Every projection shape at the prefill chunk size (4B: 2048 token rows,
+    27B: 4096); the oracle checks the first and last 32 rows and 64 random
+    ones, all N outputs each."""
+    M = 2048 if model == "4b" else 4096
+    name, N, K = MODELS[model]["proj"][p]
+    rng = np.random.default_rng(1)
+    rows = np.unique(np.concatenate([np.arange(32), M - 32 + np.arange(32), rng.integers(0, M, 64)]))
+    _say("gemm full", model, name, M, N, K)
+    ok, worst, tight = _gemm_case(q4, M, N, K, seed=0, rows=rows, layer=0, proj=p)
+    assert ok, (name, worst)
+    assert tight, name
