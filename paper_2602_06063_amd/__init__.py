@@ -35,6 +35,15 @@ EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_dequant", "q4n
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2602_06063_amd.build`")
 
+# torch ships its own HIP runtime under the same soname (libamdhip64.so.7).
+# Loading torch first makes the dynamic loader satisfy libq4nx's dependency
+# with that copy, so the process holds one HIP runtime and device pointers and
+# streams from torch are valid inside the library.
+try:
+    import torch as _torch  # noqa: F401
+except ImportError:  # host-only use (pack / unpack) without torch
+    _torch = None
+
 lib = ctypes.CDLL(LIB_PATH)
 
 _vp, _i64, _i32, _sz = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_size_t

@@ -176,3 +176,13 @@ def test_status_strings():
     for st in range(6):
         assert q4.lib.q4nx_status_str(st).decode()
     assert q4.lib.q4nx_status_str(99).decode() == "unknown status"
+
+
+def test_single_hip_runtime_in_process():
+    """The library must share torch's HIP runtime, not load a second one."""
+    maps = open("/proc/self/maps").read()
+    paths = {line.split()[-1] for line in maps.splitlines() if "libamdhip64" in line}
+    assert len(paths) == 1, paths
+    import torch
+    torch_lib = os.path.join(os.path.dirname(torch.__file__), "lib")
+    assert next(iter(paths)).startswith(torch_lib), paths
