@@ -1,0 +1,308 @@
+#!/usr/bin/env python3
+"""Benchmark of the Q4NX projection path on one MI355X.
+
+One step = one pass of the whole path over one batch of synthetic input:
+  * decode: the FusedDQP mat-vec of every projection of every layer, in layer
+    order -- per layer q/k/v in one batched launch, o, gate/up in one batched
+    launch, down (+ lm_head once for the 4B decode step);
+  * prefill: the fused dequant-GEMM of every projection of every layer on an
+    M-token chunk.
+Inputs (packed weights, activations) are resident in HBM before the timed
+region; every (layer, projection) has its own independently seeded weights and
+activations.  Timing uses HIP events on the stream the kernels run on.
+
+Prints one JSON line: value = decode weight GB/s (0.625 B per weight: the
+4-bit code plus the per-32 bf16 scale and offset); the prefill TFLOP/s
+(2*M*N*K per projection) is reported beside it.
+
+    python bench.py [--config 4] [--steps 5] [--warmup 2] [--gpus 1]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
+BF16_MFMA_PEAK_TFLOPS = 2516.6  # 256 CU x 4096 flop/clk x 2.4 GHz, dense
+WEIGHT_BYTES = 0.625            # per weight: 0.5 code + 1/16 scale + 1/16 offset
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4])
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--offset-mode", default="zp", choices=["zp", "literal"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-layers", type=int, default=1, help="layers of the oracle CPU sample")
+    return ap.parse_args()
+
+
+def build_weights(model, cfg, seed, mode, q4, torch):
+    """Generate, pack (q4nx_pack) and upload every projection's weights."""
+    from workloads import gen_weights
+    L = model["layers"]
+    tasks = [(l, p, N, K) for l in range(L) for p, (_, N, K) in enumerate(model["proj"])]
+    if cfg.get("lm_head"):
+        tasks.append((L, 7, model["lm_head"][1], model["lm_head"][2]))
+
+    def work(t):
+        l, p, N, K = t
+        codes, s, o = gen_weights(N, K, seed=seed, layer=l, proj=p, offset_mode=mode)
+        return q4.q4nx_pack(codes, s, o)
+
+    out = {}
+    t0 = time.time()
+    workers = max(1, min(16, len(os.sched_getaffinity(0))))
+    with ThreadPoolExecutor(workers) as ex:
+        for i, (t, blob) in enumerate(zip(tasks, ex.map(work, tasks))):
+            out[(t[0], t[1])] = torch.from_numpy(blob).cuda()
+            if (i + 1) % 50 == 0 or i + 1 == len(tasks):
+                log(f"weights {i + 1}/{len(tasks)} packed+uploaded ({time.time() - t0:.0f}s)")
+    return out
+
+
+class Step:
+    """Prebuilt C-ABI calls of one step (pointers marshalled once)."""
+
+    def __init__(self, q4, stream):
+        self.q4 = q4
+        self.s = ctypes.c_void_p(stream)
+        self.calls = []
+        self.keep = []
+
+    def gemv_batched(self, items, ydt):
+        arr = (self.q4.q4nx_gemv_desc * len(items))()
+        for i, (blob, x, y, N, K) in enumerate(items):
+            self.q4._need(blob, self.q4.q4nx_packed_size(N, K), "blob")
+            self.q4._need(x, 2 * K, "x")
+            self.q4._need(y, N * y.element_size(), "y")
+            arr[i] = self.q4.q4nx_gemv_desc(blob.data_ptr(), x.data_ptr(), y.data_ptr(), N, K)
+        self.keep.append(arr)
+        self.calls.append((self.q4.lib.q4nx_gemv_batched, (arr, len(items), ydt, self.s)))
+
+    def gemm(self, M, N, K, X, blob, Y, ydt):
+        self.q4._need(blob, self.q4.q4nx_packed_size(N, K), "blob")
+        self.q4._need(X, 2 * M * K, "X")
+        self.q4._need(Y, M * N * Y.element_size(), "Y")
+        self.calls.append((self.q4.lib.q4nx_gemm, (M, N, K, X.data_ptr(), blob.data_ptr(), Y.data_ptr(), ydt, self.s)))
+
+    def run(self):
+        for fn, args in self.calls:
+            st = fn(*args)
+            if st:
+                raise RuntimeError(f"{fn.__name__}: status {st}: {self.q4.lib.q4nx_last_error().decode()}")
+
+
+def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefill):
+    """The oracle, untuned, on a bounded sample: `layers` layer(s) of the
+    workload's projections, timed on this host's cores."""
+    import numpy as np
+    import oracle
+    from workloads import gen_weights, gen_activations
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        blas_threads = 1
+    dec_t = dec_bytes = 0.0
+    pre_t = pre_flops = 0.0
+    rows = 16
+    for l in range(layers):
+        for p, (_, N, K) in enumerate(model["proj"]):
+            codes, s, o = gen_weights(N, K, seed=seed, layer=l, proj=p, offset_mode=mode)
+            blob = oracle.pack(codes, s, o)
+            x = gen_activations(K, seed=seed, layer=l, proj=p)
+            X = gen_activations((rows, K), seed=seed, layer=l, proj=p)
+            t0 = time.perf_counter()
+            w = oracle.dequant_blob_f32(blob, N, K)
+            t_deq = time.perf_counter() - t0
+            if do_decode:
+                t0 = time.perf_counter()
+                oracle.gemv_f64(w, x)
+                dec_t += t_deq + time.perf_counter() - t0
+                dec_bytes += N * K * WEIGHT_BYTES
+            if do_prefill:
+                t0 = time.perf_counter()
+                oracle.gemm_f64(X, w)
+                pre_t += t_deq + time.perf_counter() - t0
+                pre_flops += 2.0 * rows * N * K
+            log(f"oracle sample: layer {l} projection {p} ({N}x{K}) done")
+    out = {"cores": int(blas_threads), "kind": "oracle"}
+    what = f"{layers} layer(s) x {len(model['proj'])} projections of {cfg['name']}"
+    if do_decode:
+        out.update(value=dec_bytes / dec_t / 1e9, unit="GB/s",
+                   sample=f"decode M=1 over {what}: NumPy float32 Eq. 3 dequant + float64 mat-vec "
+                          f"(dequant single-threaded, mat-vec on {blas_threads} BLAS threads)",
+                   seconds=dec_t)
+    if do_prefill:
+        pf = {"value": pre_flops / pre_t / 1e12, "unit": "TFLOP/s", "seconds": pre_t,
+              "sample": f"prefill {rows} of {M_prefill} token rows over {what}: float32 dequant + float64 matmul"}
+        if do_decode:
+            out["prefill"] = pf
+        else:
+            out.update(value=pf["value"], unit=pf["unit"], sample=pf["sample"], seconds=pre_t)
+    return out
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: this build measures the single-GPU path "
+              "(multi-GPU sharding is a design note, not an implementation).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2602_06063_amd as q4
+    from workloads import MODELS, CONFIGS, gen_activations, gen_activations_device
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    cfg = CONFIGS[args.config]
+    model = MODELS[cfg["model"]]
+    L = model["layers"]
+    Ms = cfg["M"]
+    do_decode = 1 in Ms
+    M_pre = max(m for m in Ms) if any(m > 1 for m in Ms) else 0
+    do_prefill = M_pre > 0
+    log(f"config {args.config}: {cfg['name']}, {L} layers, M={Ms}")
+
+    weights = build_weights(model, cfg, args.seed, args.offset_mode, q4, torch)
+    stream = torch.cuda.current_stream()
+    F32 = q4.Q4NX_F32
+
+    # ---------------------------------------------------------------- decode
+    dec = Step(q4, stream.cuda_stream)
+    dec_bytes = 0.0
+    dec_launches = 0
+    if do_decode:
+        xs, ys = {}, {}
+        for l in range(L):
+            for p, (_, N, K) in enumerate(model["proj"]):
+                xs[(l, p)] = torch.from_numpy(gen_activations(K, seed=args.seed, layer=l, proj=p).view("int16")).cuda()
+                ys[(l, p)] = torch.empty(N, dtype=torch.float32, device="cuda")
+                dec_bytes += N * K * WEIGHT_BYTES
+        for l in range(L):
+            it = lambda p: (weights[(l, p)], xs[(l, p)], ys[(l, p)], model["proj"][p][1], model["proj"][p][2])
+            dec.gemv_batched([it(0), it(1), it(2)], F32)   # q, k, v
+            dec.gemv_batched([it(3)], F32)                 # o
+            dec.gemv_batched([it(4), it(5)], F32)          # gate, up
+            dec.gemv_batched([it(6)], F32)                 # down
+        if cfg.get("lm_head"):
+            _, N, K = model["lm_head"]
+            x = torch.from_numpy(gen_activations(K, seed=args.seed, layer=L, proj=7).view("int16")).cuda()
+            y = torch.empty(N, dtype=torch.float32, device="cuda")
+            dec.gemv_batched([(weights[(L, 7)], x, y, N, K)], F32)
+            dec_bytes += N * K * WEIGHT_BYTES
+        dec_launches = len(dec.calls)
+
+    # ---------------------------------------------------------------- prefill
+    pre = Step(q4, stream.cuda_stream)
+    pre_flops = 0.0
+    if do_prefill:
+        Xs = {}
+        Ys = {}
+        for p, (_, N, K) in enumerate(model["proj"]):
+            Ys[p] = torch.empty((M_pre, N), dtype=torch.float32, device="cuda")
+        for l in range(L):
+            for p, (_, N, K) in enumerate(model["proj"]):
+                Xs[(l, p)] = gen_activations_device((M_pre, K), seed=args.seed, layer=l, proj=p)
+                pre.gemm(M_pre, N, K, Xs[(l, p)], weights[(l, p)], Ys[p], F32)
+                pre_flops += 2.0 * M_pre * N * K
+    torch.cuda.synchronize()
+    log(f"inputs resident: {sum(t.numel() for t in weights.values()) / 1e9:.2f} GB of packed weights")
+
+    # ---------------------------------------------------------------- timing
+    for _ in range(args.warmup):
+        dec.run()
+        pre.run()
+    torch.cuda.synchronize()
+    log("warmup done")
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    for e0, e1, e2 in ev:
+        e0.record(stream)
+        dec.run()
+        e1.record(stream)
+        pre.run()
+        e2.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    dec_ms = [a.elapsed_time(b) for a, b, _ in ev]
+    pre_ms = [b.elapsed_time(c) for _, b, c in ev]
+    step_ms = [d + p for d, p in zip(dec_ms, pre_ms)]
+    mean = lambda v: sum(v) / len(v)
+    log(f"timed {args.steps} steps in {wall:.2f}s wall; decode {mean(dec_ms):.3f} ms, prefill {mean(pre_ms):.3f} ms")
+
+    dec_gbs = dec_bytes / (mean(dec_ms) * 1e-3) / 1e9 if do_decode else None
+    pre_tflops = pre_flops / (mean(pre_ms) * 1e-3) / 1e12 if do_prefill else None
+
+    result = {
+        "metric": "Q4NX dequant-GEMV weight GB/s (% HBM peak); dequant-GEMM TFLOP/s (% MFMA)",
+        "value": round(dec_gbs, 2) if do_decode else round(pre_tflops, 2),
+        "unit": "GB/s" if do_decode else "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(mean(step_ms), 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if do_decode else "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": cfg["name"],
+            "layers": L,
+            "projections": [list(p) for p in model["proj"]] + ([list(model["lm_head"])] if cfg.get("lm_head") else []),
+            "M": Ms,
+            "offset_mode": args.offset_mode,
+            "seed": args.seed,
+        },
+    }
+    if do_decode:
+        result["decode"] = {"ms": round(mean(dec_ms), 4), "ms_min": round(min(dec_ms), 4),
+                            "weight_GB": round(dec_bytes / 1e9, 4), "GB_per_s": round(dec_gbs, 2),
+                            "frac_hbm": round(dec_gbs / HBM_PEAK_GBS, 4), "launches": dec_launches,
+                            "dtype": "f32 (exact code->f32 convert, f32 FMA)"}
+    if do_prefill:
+        result["prefill"] = {"ms": round(mean(pre_ms), 4), "ms_min": round(min(pre_ms), 4), "M": M_pre,
+                             "TFLOP": round(pre_flops / 1e12, 4), "TFLOP_per_s": round(pre_tflops, 2),
+                             "frac_mfma": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4),
+                             "launches": len(pre.calls), "dtype": "bf16 MFMA, f32 accumulate"}
+        if do_decode:
+            result["value_gemm"] = round(pre_tflops, 2)
+    # Dominant kernel by time: the GEMM when the step has a prefill chunk.
+    if do_prefill:
+        result["roofline"] = {"kernel": "gemm_kernel", "bound": "mfma", "achieved": round(pre_tflops, 2),
+                              "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                              "frac": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None}
+    if do_decode:
+        r = {"kernel": "gemv_kernel", "bound": "hbm", "achieved": round(dec_gbs, 2), "peak": HBM_PEAK_GBS,
+             "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None}
+        result["roofline" if not do_prefill else "roofline_gemv"] = r
+
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle sample")
+        result["cpu_baseline"] = cpu_baseline(model, cfg, args.seed, args.offset_mode, args.cpu_layers,
+                                              do_decode, do_prefill, M_pre)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

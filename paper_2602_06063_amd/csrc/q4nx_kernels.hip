@@ -10,7 +10,6 @@
 // the lane's group sits at index 8r + c = 64t + l of the block's tables.
 #include <hip/hip_runtime.h>
 
-#include <mutex>
 #include <string>
 #include <vector>
 
@@ -142,31 +141,36 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict_
 // ---------------------------------------------------------------------------
 // q4nx_gemv / q4nx_gemv_batched: FusedDQP
 // ---------------------------------------------------------------------------
-// A workgroup of 4 waves owns 4 consecutive 32-row strips and one range of
-// blocks along K (a "split").  The split's slice of x is staged once in LDS as
-// float32 together with its group sums S_g = sum_{k in g} x_k, so that each
-// row accumulates
-//     y_n += d_g * (sum_{k in g} q_k x_k) + m_g * S_g          (Eq. 3 in Eq. 15)
-// and the per-weight work is one convert and one FMA.  Each wave streams its
-// strip's blocks (four 1 KiB loads per block), prefetching the next block
-// while it computes the current one.  Lane l accumulates rows 8t + l/8
-// (t = 0..3) for group l%8; a 3-step butterfly adds the 8 groups of a row.
-// With several splits per strip, each wave stores its 32 partial sums, and
-// the last wave to arrive at the strip's counter adds the partials in split
-// order (so the result is deterministic) and resets the counter.
-constexpr int kGemvWaves = 4;
-constexpr int kGemvThreads = 64 * kGemvWaves;
-constexpr int kGemvMaxBpw = 16;  // blocks per split: LDS holds 16 x 256 floats
+// A workgroup owns a row group of R = 8*tq consecutive rows (tq = 4: a whole
+// 32-row strip; 2: half a strip; 1: a quarter) and all of K.  Its W waves
+// split the strip's blocks round-robin (block j goes to wave j % W); each
+// wave accumulates, per lane, the rows 8t + l/8 (t = t0..t0+tq-1) of group
+// l%8 as
+//     acc += d_g * (sum_{k in g} q_k x_k) + m_g * S_g ,  S_g = sum_{k in g} x_k
+// (Eq. 3 folded into Eq. 15), so the per-weight work is one exact code ->
+// float32 convert and one FMA.  x is staged in LDS as float32 with its group
+// sums, a chunk of K at a time; groups are padded to 36 floats so the eight
+// groups a wave reads at once fall in distinct banks.  At the end a 3-step
+// butterfly adds the 8 groups of a row and the W waves' partial sums are added
+// in wave order through LDS.  No workgroup talks to another, so there is no
+// cross-XCD traffic and no device-wide fence; the summation order depends
+// only on K (through W), so a projection gives the same bits alone or batched.
+// Each wave prefetches its next block while computing the current one.
+constexpr int kGemvMaxWaves = 16;
+constexpr int kGemvChunkBlocks = 48;                    // x staged 48 x 256 columns at a time
+constexpr int kGroupPad = 36;                           // floats per staged group of 32
+constexpr int kRedFloats = kGemvMaxWaves * 32;
 
 struct GemvJob {
   const uint8_t* blob;
   const uint16_t* x;
   void* y;
-  float* partial;      // [NS][ksplit][32] if ksplit > 1
-  unsigned* counter;   // [NS] if ksplit > 1, all zero between calls
   int N, K, NS, KB;
-  int ksplit, bpw;
-  int wg_begin;        // first workgroup of this job in the launch
+  int tq;        // row octets per row group (1, 2 or 4)
+  int nrg;       // row groups: NS * 4 / tq
+  int waves;     // waves splitting K (depends on K only)
+  int nwg;       // workgroups of this job (each loops over row groups)
+  int wg_begin;  // first workgroup of this job in the launch
   int pad;
 };
 
@@ -174,6 +178,8 @@ struct GemvArgs {
   GemvJob job[Q4NX_MAX_BATCH];
   int njobs;
   int y_bf16;
+  int chunk_blocks;  // blocks of x staged at once (sizes the dynamic LDS)
+  int pad;
 };
 
 struct GemvBlockRegs {
@@ -181,13 +187,16 @@ struct GemvBlockRegs {
   uint32_t s[4], m[4];
 };
 
-__device__ __forceinline__ void gemv_load_block(const uint8_t* blk, bool ok, int lane, GemvBlockRegs& R) {
+// Loads the tq row octets t0..t0+tq-1 of one block (group `c` of each row).
+__device__ __forceinline__ void gemv_load_block(const uint8_t* blk, bool ok, int t0, int tq, int lane,
+                                                GemvBlockRegs& R) {
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    if (ok) {
-      R.q[t] = load_codes(blk + 1024 * t + 16 * lane);
-      R.s[t] = load_u16(blk + kCodeBytes + 2 * (64 * t + lane));
-      R.m[t] = load_u16(blk + kCodeBytes + kScaleBytes + 2 * (64 * t + lane));
+    if (ok && t < tq) {
+      const int tt = t0 + t;
+      R.q[t] = load_codes(blk + 1024 * tt + 16 * lane);
+      R.s[t] = load_u16(blk + kCodeBytes + 2 * (64 * tt + lane));
+      R.m[t] = load_u16(blk + kCodeBytes + kScaleBytes + 2 * (64 * tt + lane));
     } else {
       R.q[t] = (u32x4){0u, 0u, 0u, 0u};
       R.s[t] = 0u;
@@ -196,8 +205,8 @@ __device__ __forceinline__ void gemv_load_block(const uint8_t* blk, bool ok, int
   }
 }
 
-__device__ __forceinline__ void gemv_compute_block(const GemvBlockRegs& R, const float* __restrict__ xg, float S,
-                                                   float (&acc)[4]) {
+__device__ __forceinline__ void gemv_compute_block(const GemvBlockRegs& R, int tq, const float* __restrict__ xg,
+                                                   float S, float (&acc)[4]) {
   float x[32];
 #pragma unroll
   for (int v = 0; v < 8; ++v) {
@@ -209,15 +218,21 @@ __device__ __forceinline__ void gemv_compute_block(const GemvBlockRegs& R, const
   }
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
-    const float dot = group_dot(R.q[t], x);
-    acc[t] = fmaf(bf16_to_f32(R.s[t]), dot, acc[t]);
-    acc[t] = fmaf(bf16_to_f32(R.m[t]), S, acc[t]);
+    if (t < tq) {
+      const float dot = group_dot(R.q[t], x);
+      acc[t] = fmaf(bf16_to_f32(R.s[t]), dot, acc[t]);
+      acc[t] = fmaf(bf16_to_f32(R.m[t]), S, acc[t]);
+    }
   }
 }
 
-__global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const GemvArgs args) {
-  __shared__ float xs[kGemvMaxBpw * kBlockCols];
-  __shared__ float ssum[kGemvMaxBpw * kGroupsPerRow];
+__global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs args) {
+  // Dynamic LDS: red[16*32] | ssum[chunk*8] | xs[chunk*8*36], chunk = the
+  // launch's largest staged block count (at most kGemvChunkBlocks).
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  float* red = lds;
+  float* ssum = lds + kRedFloats;
+  float* xs = ssum + args.chunk_blocks * kGroupsPerRow;
 
   const int wg = blockIdx.x;
   int jb = 0;
@@ -226,99 +241,96 @@ __global__ __launch_bounds__(kGemvThreads) void gemv_kernel(const GemvArgs args)
     if (t < args.njobs && wg >= args.job[t].wg_begin) jb = t;
   const GemvJob& J = args.job[jb];
 
-  const int local = wg - J.wg_begin;
-  const int sg = local / J.ksplit;
-  const int sp = local - sg * J.ksplit;
-  const int j0 = sp * J.bpw;
-  const int nb = min(J.KB, j0 + J.bpw) - j0;
-
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int c = lane & 7;
-  const int strip = sg * kGemvWaves + w;
-  const bool active = strip < J.NS;  // wave-uniform
-  const bool loads = active && nb > 0;
-  const uint8_t* sblob = J.blob + (size_t)strip * J.KB * kBlockBytes;
+  const int W = J.waves, tq = J.tq;
+  const int nthreads = blockDim.x;
+  const bool wave_on = w < W;  // wave-uniform
+  const int CB = args.chunk_blocks;
+  const int nchunks = (J.KB + CB - 1) / CB;
+  int staged = -1;  // chunk currently held in LDS
 
-  // Issue the first block's loads before staging x so both latencies overlap.
-  GemvBlockRegs A, B;
-  gemv_load_block(sblob + (size_t)j0 * kBlockBytes, loads && (j0 * kBlockCols + kGroup * c < J.K), lane, A);
+  for (int rg = wg - J.wg_begin; rg < J.nrg; rg += J.nwg) {
+    const int row0 = rg * 8 * tq;
+    const int strip = row0 >> 5, t0 = (row0 & 31) >> 3;
+    const uint8_t* sblob = J.blob + (size_t)strip * J.KB * kBlockBytes;
+    float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 
-  // Stage x[j0*256 .. (j0+nb)*256) as float32 (zero beyond K) and the group sums.
-  {
-    const int kbeg = j0 * kBlockCols;
-    const uint32_t* x2 = reinterpret_cast<const uint32_t*>(J.x);
-    for (int e = threadIdx.x; e < nb * (kBlockCols / 2); e += kGemvThreads) {
-      const int k = kbeg + 2 * e;
-      const uint32_t v = (k < J.K) ? x2[k >> 1] : 0u;
-      const float xa = __uint_as_float(v << 16), xb = __uint_as_float(v & 0xFFFF0000u);
-      xs[2 * e] = xa;
-      xs[2 * e + 1] = xb;
-      float s = xa + xb;
-      s += __shfl_xor(s, 1);
-      s += __shfl_xor(s, 2);
-      s += __shfl_xor(s, 4);
-      s += __shfl_xor(s, 8);
-      if ((threadIdx.x & 15) == 0) ssum[e >> 4] = s;
+    for (int ch = 0; ch < nchunks; ++ch) {
+      const int jc0 = ch * CB;
+      const int nb = min(CB, J.KB - jc0);
+      // First block of this wave: issue its loads before the x staging.
+      GemvBlockRegs A, B;
+      {
+        const int j = jc0 + w;
+        const bool ok = wave_on && w < nb && (j * kBlockCols + kGroup * c < J.K);
+        gemv_load_block(sblob + (size_t)j * kBlockBytes, ok, t0, tq, lane, A);
+      }
+      if (staged != ch) {
+        __syncthreads();  // every wave is done with the previous chunk
+        const int kbeg = jc0 * kBlockCols;
+        const uint32_t* x2 = reinterpret_cast<const uint32_t*>(J.x);
+        for (int e = threadIdx.x; e < nb * (kBlockCols / 2); e += nthreads) {
+          const int k = kbeg + 2 * e;
+          const uint32_t v = (k < J.K) ? x2[k >> 1] : 0u;
+          const float xa = __uint_as_float(v << 16), xb = __uint_as_float(v & 0xFFFF0000u);
+          const int g = e >> 4, o = (2 * e) & 31;
+          xs[g * kGroupPad + o] = xa;
+          xs[g * kGroupPad + o + 1] = xb;
+          float sm = xa + xb;
+          sm += __shfl_xor(sm, 1);
+          sm += __shfl_xor(sm, 2);
+          sm += __shfl_xor(sm, 4);
+          sm += __shfl_xor(sm, 8);
+          if ((threadIdx.x & 15) == 0) ssum[g] = sm;
+        }
+        __syncthreads();
+        staged = ch;
+      }
+      if (wave_on) {
+        for (int jj = w; jj < nb; jj += 2 * W) {
+          const int j1 = jj + W, j2 = jj + 2 * W;
+          if (j1 < nb)
+            gemv_load_block(sblob + (size_t)(jc0 + j1) * kBlockBytes,
+                            (jc0 + j1) * kBlockCols + kGroup * c < J.K, t0, tq, lane, B);
+          gemv_compute_block(A, tq, xs + (jj * kGroupsPerRow + c) * kGroupPad, ssum[jj * kGroupsPerRow + c], acc);
+          if (j1 < nb) {
+            if (j2 < nb)
+              gemv_load_block(sblob + (size_t)(jc0 + j2) * kBlockBytes,
+                              (jc0 + j2) * kBlockCols + kGroup * c < J.K, t0, tq, lane, A);
+            gemv_compute_block(B, tq, xs + (j1 * kGroupsPerRow + c) * kGroupPad, ssum[j1 * kGroupsPerRow + c],
+                               acc);
+          }
+        }
+      }
     }
-  }
-  __syncthreads();
 
-  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
-  for (int jj = 0; jj < nb; jj += 2) {
-    const int k1 = (j0 + jj + 1) * kBlockCols + kGroup * c;
-    if (jj + 1 < nb) gemv_load_block(sblob + (size_t)(j0 + jj + 1) * kBlockBytes, active && k1 < J.K, lane, B);
-    gemv_compute_block(A, xs + jj * kBlockCols + kGroup * c, ssum[jj * kGroupsPerRow + c], acc);
-    if (jj + 1 < nb) {
-      const int k2 = (j0 + jj + 2) * kBlockCols + kGroup * c;
-      if (jj + 2 < nb) gemv_load_block(sblob + (size_t)(j0 + jj + 2) * kBlockBytes, active && k2 < J.K, lane, A);
-      gemv_compute_block(B, xs + (jj + 1) * kBlockCols + kGroup * c, ssum[(jj + 1) * kGroupsPerRow + c], acc);
-    }
-  }
-
-  // Add the 8 groups of each row (lanes 8s..8s+7 hold row 8t + s).
+    // Add the 8 groups of each row: lanes 8r'..8r'+7 hold row octet t, row r'.
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    acc[t] += __shfl_xor(acc[t], 1);
-    acc[t] += __shfl_xor(acc[t], 2);
-    acc[t] += __shfl_xor(acc[t], 4);
-  }
-  // Lane with c < 4 owns row 8c + l/8 of the strip.
-  const float v = (c == 0) ? acc[0] : (c == 1) ? acc[1] : (c == 2) ? acc[2] : acc[3];
-  const int row = 8 * c + (lane >> 3);
-  const int64_t n = (int64_t)strip * kBlockRows + row;
-
-  if (J.ksplit == 1) {
-    if (active && c < 4 && n < J.N) {
-      if (args.y_bf16)
-        static_cast<uint16_t*>(J.y)[n] = f32_to_bf16_bits(v);
-      else
-        static_cast<float*>(J.y)[n] = v;
+    for (int t = 0; t < 4; ++t) {
+      acc[t] += __shfl_xor(acc[t], 1);
+      acc[t] += __shfl_xor(acc[t], 2);
+      acc[t] += __shfl_xor(acc[t], 4);
     }
-    return;
-  }
-  if (!active) return;  // wave-uniform
-
-  float* P = J.partial + (size_t)strip * J.ksplit * kBlockRows;
-  if (c < 4) __hip_atomic_store(P + (size_t)sp * kBlockRows + row, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  __threadfence();
-  unsigned old = 0;
-  if (lane == 0) old = atomicAdd(J.counter + strip, 1u);
-  old = __shfl(old, 0);
-  if (old != (unsigned)(J.ksplit - 1)) return;
-  __threadfence();
-  if (lane < kBlockRows) {
-    float s = 0.0f;
-    for (int q = 0; q < J.ksplit; ++q)
-      s += __hip_atomic_load(P + (size_t)q * kBlockRows + lane, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const int64_t nn = (int64_t)strip * kBlockRows + lane;
-    if (nn < J.N) {
-      if (args.y_bf16)
-        static_cast<uint16_t*>(J.y)[nn] = f32_to_bf16_bits(s);
-      else
-        static_cast<float*>(J.y)[nn] = s;
+    // Lane with c == t (t < tq) holds row 8t + l/8 of the row group.
+    if (wave_on && c < tq) {
+      const float v = (c == 0) ? acc[0] : (c == 1) ? acc[1] : (c == 2) ? acc[2] : acc[3];
+      red[w * 32 + 8 * c + (lane >> 3)] = v;
     }
+    __syncthreads();
+    if (threadIdx.x < 8 * tq) {
+      float sum = 0.0f;
+      for (int q = 0; q < W; ++q) sum += red[q * 32 + threadIdx.x];
+      const int64_t n = (int64_t)row0 + threadIdx.x;
+      if (n < J.N) {
+        if (args.y_bf16)
+          static_cast<uint16_t*>(J.y)[n] = f32_to_bf16_bits(sum);
+        else
+          static_cast<float*>(J.y)[n] = sum;
+      }
+    }
+    __syncthreads();  // red[] is rewritten by the next row group
   }
-  if (lane == 0) __hip_atomic_store(J.counter + strip, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ---------------------------------------------------------------------------
@@ -438,67 +450,23 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
     }
 }
 
-// ---------------------------------------------------------------------------
-// per-device scratch for the split-K partial sums
-// ---------------------------------------------------------------------------
-constexpr size_t kPartialCap = size_t(1) << 22;  // floats (16 MiB)
-constexpr size_t kCounterCap = size_t(1) << 20;  // counters (4 MiB)
-
-struct Scratch {
-  float* partial = nullptr;
-  unsigned* counter = nullptr;
-};
-
-static std::mutex g_scratch_mu;
-static std::vector<Scratch> g_scratch;
-
-static q4nx_status get_scratch(Scratch& out) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return fail(Q4NX_ERR_HIP, "hipGetDevice failed");
-  std::lock_guard<std::mutex> lk(g_scratch_mu);
-  if ((int)g_scratch.size() <= dev) g_scratch.resize(dev + 1);
-  Scratch& s = g_scratch[dev];
-  if (!s.partial) {
-    void *p = nullptr, *c = nullptr;
-    if (hipMalloc(&p, kPartialCap * sizeof(float)) != hipSuccess)
-      return fail(Q4NX_ERR_HIP, "scratch allocation failed");
-    if (hipMalloc(&c, kCounterCap * sizeof(unsigned)) != hipSuccess) {
-      (void)hipFree(p);
-      return fail(Q4NX_ERR_HIP, "scratch allocation failed");
-    }
-    if (hipMemset(c, 0, kCounterCap * sizeof(unsigned)) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
-      (void)hipFree(p);
-      (void)hipFree(c);
-      return fail(Q4NX_ERR_HIP, "scratch initialisation failed");
-    }
-    s.partial = static_cast<float*>(p);
-    s.counter = static_cast<unsigned*>(c);
-  }
-  out = s;
-  return Q4NX_OK;
-}
-
 static q4nx_status check_launch(const char* fn) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return fail(Q4NX_ERR_HIP, std::string(fn) + ": " + hipGetErrorString(e));
   return Q4NX_OK;
 }
 
-// Chooses blocks-per-split for one projection so that it alone launches
-// about `target_waves` waves: at least 2 blocks per wave (to amortise the x
-// staging and the reduction), at most kGemvMaxBpw (the LDS slice), balanced
-// across the splits of a strip.  The plan depends only on (N, K), so a
-// projection is summed in the same order whether launched alone or batched.
-// A split plan (ksplit > 1) implies bpw < KB and bpw >= NS*KB/2048, hence
-// NS < 2048: its scratch needs stay far below the scratch capacity.
-static void plan_split(int NS, int KB, int& ksplit, int& bpw) {
-  const int64_t target_waves = 2048;
-  const int64_t total_blocks = (int64_t)NS * KB;
-  int64_t b = (total_blocks + target_waves - 1) / target_waves;
-  b = std::max<int64_t>(2, std::min<int64_t>(kGemvMaxBpw, b));
-  b = std::min<int64_t>(b, KB);
-  ksplit = (int)((KB + b - 1) / b);
-  bpw = (KB + ksplit - 1) / ksplit;
+// Waves that split K: about two blocks per wave, at most 16.  A function of K
+// alone, so a projection is summed in the same order alone or in a batch.
+static int gemv_waves(int KB) { return std::max(1, std::min(kGemvMaxWaves, (KB + 1) / 2)); }
+
+// Row-group size: whole strips when there are enough of them to keep at least
+// ~160 CUs streaming (one CU sustains ~55 GB/s of the ~7 TB/s), else halves or
+// quarters of strips.  `strips` is the number of strips of the whole launch.
+static int gemv_tq(int64_t strips) {
+  if (strips >= 160) return 4;
+  if (strips * 2 >= 160) return 2;
+  return 1;
 }
 
 static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtype y_dtype, hipStream_t stream,
@@ -508,19 +476,21 @@ static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtyp
     return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": need 1..8 descriptors");
   if (y_dtype != Q4NX_F32 && y_dtype != Q4NX_BF16)
     return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": unknown y_dtype");
-  bool need_split = false;
+  int64_t strips = 0;
   for (int i = 0; i < count; ++i) {
     const q4nx_gemv_desc& d = descs[i];
     if (q4nx_status st = check_shape(d.N, d.K, fn)) return st;
     if (!d.blob || !d.x || !d.y) return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
     if (!aligned(d.blob, 16) || !aligned(d.x, 16) || !aligned(d.y, 4))
       return fail(Q4NX_ERR_ALIGNMENT, std::string(fn) + ": blob/x need 16-byte, y 4-byte alignment");
+    strips += ceil_div(d.N, kBlockRows);
   }
+  const int tq = gemv_tq(strips);
   GemvArgs args = {};
   args.njobs = count;
   args.y_bf16 = (y_dtype == Q4NX_BF16);
   int64_t wg = 0;
-  size_t part_off = 0, ctr_off = 0;
+  int max_waves = 1;
   for (int i = 0; i < count; ++i) {
     const q4nx_gemv_desc& d = descs[i];
     GemvJob& J = args.job[i];
@@ -531,32 +501,19 @@ static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtyp
     J.K = (int)d.K;
     J.NS = (int)ceil_div(d.N, kBlockRows);
     J.KB = (int)ceil_div(d.K, kBlockCols);
-    plan_split(J.NS, J.KB, J.ksplit, J.bpw);
-    if (J.ksplit > 1) {
-      if (part_off + (size_t)J.NS * J.ksplit * kBlockRows > kPartialCap || ctr_off + (size_t)J.NS > kCounterCap)
-        return fail(Q4NX_ERR_SHAPE, std::string(fn) + ": problem exceeds the split-K scratch");
-      need_split = true;
-      J.partial = reinterpret_cast<float*>(part_off);   // rebased below
-      J.counter = reinterpret_cast<unsigned*>(ctr_off);
-      part_off += (size_t)J.NS * J.ksplit * kBlockRows;
-      ctr_off += (size_t)J.NS;
-    }
+    J.tq = tq;
+    J.nrg = J.NS * (4 / tq);
+    J.waves = gemv_waves(J.KB);
+    // Up to 2048 workgroups per job; beyond that a workgroup loops over row
+    // groups and reuses the x it staged.
+    J.nwg = std::min(J.nrg, 2048);
     J.wg_begin = (int)wg;
-    wg += ceil_div(J.NS, kGemvWaves) * (int64_t)J.ksplit;
-    if (wg > 0x7FFFFFFF) return fail(Q4NX_ERR_SHAPE, std::string(fn) + ": grid too large");
+    wg += J.nwg;
+    max_waves = std::max(max_waves, J.waves);
+    args.chunk_blocks = std::max(args.chunk_blocks, std::min(J.KB, kGemvChunkBlocks));
   }
-  if (need_split) {
-    Scratch s;
-    if (q4nx_status st = get_scratch(s)) return st;
-    for (int i = 0; i < count; ++i) {
-      GemvJob& J = args.job[i];
-      if (J.ksplit > 1) {
-        J.partial = s.partial + reinterpret_cast<size_t>(J.partial);
-        J.counter = s.counter + reinterpret_cast<size_t>(J.counter);
-      }
-    }
-  }
-  hipLaunchKernelGGL(gemv_kernel, dim3((unsigned)wg), dim3(kGemvThreads), 0, stream, args);
+  const size_t lds = sizeof(float) * ((size_t)kRedFloats + (size_t)args.chunk_blocks * kGroupsPerRow * (1 + kGroupPad));
+  hipLaunchKernelGGL(gemv_kernel, dim3((unsigned)wg), dim3(64 * max_waves), lds, stream, args);
   return check_launch(fn);
 }
 

@@ -152,3 +152,18 @@ def gen_edge_weights(N: int, K: int, seed: int = 0):
     scales = choices_s[rng.integers(0, len(choices_s), size=(N, G))]
     offsets = choices_m[rng.integers(0, len(choices_m), size=(N, G))]
     return codes, scales, offsets
+
+
+def device_act_seed(seed: int, layer: int, proj: int) -> int:
+    """64-bit seed of the on-device activation stream of (seed, layer, proj)."""
+    st = np.random.SeedSequence([seed, layer, proj, 2]).generate_state(2, dtype=np.uint32)
+    return int(st[0]) | (int(st[1]) << 32)
+
+
+def gen_activations_device(shape, seed: int = 0, layer: int = 0, proj: int = 0, device="cuda"):
+    """bf16 standard-normal activations drawn directly on the GPU with torch's
+    seeded generator (for large prefill inputs of the benchmark)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(device_act_seed(seed, layer, proj) & ((1 << 63) - 1))
+    return torch.randn(shape, generator=g, device=device, dtype=torch.float32).to(torch.bfloat16)
