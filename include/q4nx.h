@@ -37,11 +37,10 @@
  *     any HIP call, then only enqueue work on `stream` (NULL = the default
  *     stream) and return; they never synchronize the device.  A launch failure
  *     is reported as Q4NX_ERR_HIP (details in q4nx_last_error()).
- *   - The library keeps one small scratch area per device (split-K partial
- *     sums and arrival counters of q4nx_gemv / q4nx_gemv_batched), allocated
- *     and zeroed on the first call that needs it on that device; make that
- *     first call outside HIP graph capture.  Calls that use it must not run
- *     concurrently on one device (e.g. on two streams at once).
+ *   - The library allocates no device memory of its own: every kernel works
+ *     in the caller's buffers plus on-chip memory, so calls may be captured
+ *     in HIP graphs and may run concurrently on different streams (as long as
+ *     their output buffers do not overlap).
  *   - No C++ exception crosses this interface.
  */
 #ifndef Q4NX_H
@@ -125,6 +124,7 @@ q4nx_status q4nx_dequant(const void* d_blob, int64_t N, int64_t K,
  *   d_x    : device, K bf16 values, 16-byte aligned
  *   d_y    : device, N values of y_dtype, 4-byte aligned; fully overwritten
  *            (no zeroing needed); nothing beyond N is written
+ * Deterministic: the same call gives the same bits every time.
  * Errors: Q4NX_ERR_INVALID_ARG, Q4NX_ERR_SHAPE, Q4NX_ERR_ALIGNMENT, Q4NX_ERR_HIP.
  */
 q4nx_status q4nx_gemv(const void* d_blob, const uint16_t* d_x, void* d_y, q4nx_dtype y_dtype,
@@ -146,8 +146,10 @@ typedef struct q4nx_gemv_desc {
 /*
  * Device.  Runs 1..Q4NX_MAX_BATCH independent FusedDQP projections in one
  * launch -- e.g. the q/k/v projections of a layer, or gate/up, which read the
- * same activation.  Each result equals what q4nx_gemv gives for that
- * descriptor (bit for bit).  Outputs must not overlap inputs or each other.
+ * same activation.  Each result meets the same error bound as q4nx_gemv (the
+ * work split, hence the float32 summation order, is chosen for the launch as
+ * a whole); repeating a call with the same descriptors reproduces it bit for
+ * bit.  Outputs must not overlap inputs or each other.
  * Errors: as q4nx_gemv, for any descriptor; Q4NX_ERR_INVALID_ARG for a
  * count outside 1..Q4NX_MAX_BATCH.
  */

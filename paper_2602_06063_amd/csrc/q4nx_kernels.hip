@@ -10,6 +10,7 @@
 // the lane's group sits at index 8r + c = 64t + l of the block's tables.
 #include <hip/hip_runtime.h>
 
+#include <cstdlib>
 #include <string>
 #include <vector>
 
@@ -18,6 +19,7 @@
 namespace q4nx {
 
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -47,49 +49,75 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float a) {
 }
 
 // Streaming loads of the packed weights (read once per call).
+#ifndef Q4NX_PLAIN_LOADS
 __device__ __forceinline__ u32x4 load_codes(const uint8_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
 __device__ __forceinline__ uint32_t load_u16(const uint8_t* p) {
   return (uint32_t)__builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(p));
 }
+#else
+__device__ __forceinline__ u32x4 load_codes(const uint8_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ uint32_t load_u16(const uint8_t* p) { return *reinterpret_cast<const uint16_t*>(p); }
+#endif
 
-// The 32 codes of one group as float32 (exact), in column order.
-__device__ __forceinline__ void codes_to_f32(u32x4 q, float (&f)[32]) {
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const uint32_t lo = opaque(q[u] & 0x0F0F0F0Fu);   // even columns
-    const uint32_t hi = opaque((q[u] >> 4) & 0x0F0F0F0Fu);  // odd columns
-    f[8 * u + 0] = (float)(lo & 0xFFu);
-    f[8 * u + 1] = (float)(hi & 0xFFu);
-    f[8 * u + 2] = (float)((lo >> 8) & 0xFFu);
-    f[8 * u + 3] = (float)((hi >> 8) & 0xFFu);
-    f[8 * u + 4] = (float)((lo >> 16) & 0xFFu);
-    f[8 * u + 5] = (float)((hi >> 16) & 0xFFu);
-    f[8 * u + 6] = (float)(lo >> 24);
-    f[8 * u + 7] = (float)(hi >> 24);
-  }
+// A byte holding a 4-bit code q, read as an FP8 E4M3 value, is exactly
+// q * 2^-9 (codes 0..7 are the subnormals m * 2^-9, codes 8..15 the first
+// normal binade (8 + m) * 2^-9), so one gfx950 conversion turns two code bytes
+// into two exact bf16 values; the conversion's scale operand 2^9 makes them q.
+template <bool HI_WORD>
+__device__ __forceinline__ bf16x2 codes2_bf16(uint32_t bytes) {
+  return __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(bytes, 512.0f, HI_WORD);
 }
 
-// sum_i q_i * x_i over one group: even columns from the low nibbles, odd
-// columns from the high nibbles kept in place (16 q), rescaled by 2^-4 once
-// (exact), two independent accumulation chains.
-__device__ __forceinline__ float group_dot(u32x4 q, const float (&x)[32]) {
+// sum_i q_i * x_i over one group of 32 codes (one 16-byte word), with x given
+// as 16 bf16 pairs in the order the nibble split produces: for each 8-column
+// run u, (x0,x2), (x4,x6), (x1,x3), (x5,x7).  Products of two bf16 values are
+// exact; v_dot2 adds two of them to the float32 accumulator.
+__device__ __forceinline__ float group_dot_bf16(u32x4 q, const uint32_t (&xp)[16]) {
   float a = 0.0f, b = 0.0f;
 #pragma unroll
   for (int u = 0; u < 4; ++u) {
-    const uint32_t lo = opaque(q[u] & 0x0F0F0F0Fu);
-    const uint32_t hi = opaque(q[u] & 0xF0F0F0F0u);
-    a = fmaf((float)(lo & 0xFFu), x[8 * u + 0], a);
-    b = fmaf((float)(hi & 0xFFu), x[8 * u + 1], b);
-    a = fmaf((float)((lo >> 8) & 0xFFu), x[8 * u + 2], a);
-    b = fmaf((float)((hi >> 8) & 0xFFu), x[8 * u + 3], b);
-    a = fmaf((float)((lo >> 16) & 0xFFu), x[8 * u + 4], a);
-    b = fmaf((float)((hi >> 16) & 0xFFu), x[8 * u + 5], b);
-    a = fmaf((float)(lo >> 24), x[8 * u + 6], a);
-    b = fmaf((float)(hi >> 24), x[8 * u + 7], b);
+    const uint32_t lo = opaque(q[u] & 0x0F0F0F0Fu);          // columns 8u + 0, 2, 4, 6
+    const uint32_t hi = opaque((q[u] >> 4) & 0x0F0F0F0Fu);   // columns 8u + 1, 3, 5, 7
+    a = __builtin_amdgcn_fdot2_f32_bf16(codes2_bf16<false>(lo), __builtin_bit_cast(bf16x2, xp[4 * u + 0]), a, false);
+    a = __builtin_amdgcn_fdot2_f32_bf16(codes2_bf16<true>(lo), __builtin_bit_cast(bf16x2, xp[4 * u + 1]), a, false);
+    b = __builtin_amdgcn_fdot2_f32_bf16(codes2_bf16<false>(hi), __builtin_bit_cast(bf16x2, xp[4 * u + 2]), b, false);
+    b = __builtin_amdgcn_fdot2_f32_bf16(codes2_bf16<true>(hi), __builtin_bit_cast(bf16x2, xp[4 * u + 3]), b, false);
   }
-  return fmaf(b, 0.0625f, a);
+  return a + b;
+}
+
+// The 32 codes of one group as float32 values q * 2^-9 (exact), in column
+// order: one conversion turns two code bytes into two float32 values.
+template <bool HI_WORD>
+__device__ __forceinline__ f32x2 codes2_f32(uint32_t bytes) {
+  return __builtin_amdgcn_cvt_pk_f32_fp8(bytes, HI_WORD);
+}
+
+__device__ __forceinline__ void codes_to_f32_scaled(u32x4 q, float (&f)[32]) {
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const uint32_t lo = opaque(q[u] & 0x0F0F0F0Fu);          // columns 8u + 0, 2, 4, 6
+    const uint32_t hi = opaque((q[u] >> 4) & 0x0F0F0F0Fu);   // columns 8u + 1, 3, 5, 7
+    const f32x2 a = codes2_f32<false>(lo), b = codes2_f32<true>(lo);
+    const f32x2 e = codes2_f32<false>(hi), g = codes2_f32<true>(hi);
+    f[8 * u + 0] = a[0];
+    f[8 * u + 2] = a[1];
+    f[8 * u + 4] = b[0];
+    f[8 * u + 6] = b[1];
+    f[8 * u + 1] = e[0];
+    f[8 * u + 3] = e[1];
+    f[8 * u + 5] = g[0];
+    f[8 * u + 7] = g[1];
+  }
+}
+
+// Eq. 3 from a scaled code: (q 2^-9) * (d 2^9) is the exact product d*q (both
+// scalings are exact powers of two inside the value domain), so one FMA gives
+// RN(d*q + m) -- the same bits as the plain definition.
+__device__ __forceinline__ float eq3(float q_scaled, float d_times_512, float m) {
+  return fmaf(q_scaled, d_times_512, m);
 }
 
 // ---------------------------------------------------------------------------
@@ -97,7 +125,7 @@ __device__ __forceinline__ float group_dot(u32x4 q, const float (&x)[32]) {
 // ---------------------------------------------------------------------------
 // One workgroup of 256 threads per block; thread (t, l) handles the group at
 // row 8t + l/8, columns 32(l%8)..+31.  Eight lanes write one row's 256
-// contiguous outputs.  d*q is exact, so fmaf(q, d, m) == RN(d*q + m).
+// contiguous outputs.
 __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict__ blob, int64_t N, int64_t K,
                                                       int64_t KB, int64_t nblocks, void* __restrict__ W,
                                                       int w_bf16) {
@@ -113,9 +141,10 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict_
     const float d = bf16_to_f32(load_u16(blk + kCodeBytes + 2 * (64 * t + lane)));
     const float m = bf16_to_f32(load_u16(blk + kCodeBytes + kScaleBytes + 2 * (64 * t + lane)));
     float f[32];
-    codes_to_f32(q, f);
+    codes_to_f32_scaled(q, f);
+    const float d512 = d * 512.0f;
 #pragma unroll
-    for (int e = 0; e < 32; ++e) f[e] = fmaf(f[e], d, m);
+    for (int e = 0; e < 32; ++e) f[e] = eq3(f[e], d512, m);
     if (w_bf16) {
       u32x4* out = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(W) + n * K + k0);
 #pragma unroll
@@ -153,13 +182,19 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict_
 // groups a wave reads at once fall in distinct banks.  At the end a 3-step
 // butterfly adds the 8 groups of a row and the W waves' partial sums are added
 // in wave order through LDS.  No workgroup talks to another, so there is no
-// cross-XCD traffic and no device-wide fence; the summation order depends
-// only on K (through W), so a projection gives the same bits alone or batched.
+// cross-XCD traffic and no device-wide fence.  The summation order is fixed
+// for a given launch (results are reproducible call to call); it depends on
+// the wave count W, which is chosen for the launch as a whole.
 // Each wave prefetches its next block while computing the current one.
 constexpr int kGemvMaxWaves = 16;
 constexpr int kGemvChunkBlocks = 48;                    // x staged 48 x 256 columns at a time
-constexpr int kGroupPad = 36;                           // floats per staged group of 32
+constexpr int kGroupPadDw = 20;  // dwords per staged group (16 bf16 pairs + 4 pad: conflict-free reads)
 constexpr int kRedFloats = kGemvMaxWaves * 32;
+// Blocks in flight per wave (register slots), by row octets per wave.
+#ifndef Q4NX_GEMV_D4
+#define Q4NX_GEMV_D4 1
+#endif
+constexpr int kGemvDepth4 = Q4NX_GEMV_D4, kGemvDepth2 = 3, kGemvDepth1 = 4;
 
 struct GemvJob {
   const uint8_t* blob;
@@ -182,57 +217,68 @@ struct GemvArgs {
   int pad;
 };
 
-struct GemvBlockRegs {
-  u32x4 q[4];
-  uint32_t s[4], m[4];
+// Registers of one in-flight block: TQ row octets of codes, scales, offsets.
+template <int TQ>
+struct GemvSlot {
+  u32x4 q[TQ];
+  uint32_t s[TQ], m[TQ];
 };
 
-// Loads the tq row octets t0..t0+tq-1 of one block (group `c` of each row).
-__device__ __forceinline__ void gemv_load_block(const uint8_t* blk, bool ok, int t0, int tq, int lane,
-                                                GemvBlockRegs& R) {
+// Buffer descriptor over one chunk of one strip (at most 48 blocks = 240 KiB,
+// so every offset fits the 32-bit descriptor range); raw, stride 0.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t chunk_rsrc(const uint8_t* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), (short)0, bytes, 0x00020000);
+}
+
+// Cache policy of the weight loads: non-temporal (read once per call).
+constexpr int kNtLoad = 2;
+
+// Loads row octets t0..t0+TQ-1 of block `jj` of the chunk.  Every lane loads
+// (all addresses lie inside the chunk); the caller skips blocks past the end
+// with a wave-uniform branch.
+template <int TQ>
+__device__ __forceinline__ void gemv_load(__amdgpu_buffer_rsrc_t rs, int jj, int t0, int lane, GemvSlot<TQ>& R) {
+  const int boff = jj * kBlockBytes;
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    if (ok && t < tq) {
-      const int tt = t0 + t;
-      R.q[t] = load_codes(blk + 1024 * tt + 16 * lane);
-      R.s[t] = load_u16(blk + kCodeBytes + 2 * (64 * tt + lane));
-      R.m[t] = load_u16(blk + kCodeBytes + kScaleBytes + 2 * (64 * tt + lane));
-    } else {
-      R.q[t] = (u32x4){0u, 0u, 0u, 0u};
-      R.s[t] = 0u;
-      R.m[t] = 0u;
-    }
+  for (int t = 0; t < TQ; ++t) {
+    const int tt = t0 + t;
+    R.q[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, 16 * lane, boff + 1024 * tt, kNtLoad));
+    R.s[t] = __builtin_amdgcn_raw_buffer_load_b16(rs, 2 * lane, boff + kCodeBytes + 128 * tt, kNtLoad);
+    R.m[t] = __builtin_amdgcn_raw_buffer_load_b16(rs, 2 * lane, boff + kCodeBytes + kScaleBytes + 128 * tt, kNtLoad);
   }
 }
 
-__device__ __forceinline__ void gemv_compute_block(const GemvBlockRegs& R, int tq, const float* __restrict__ xg,
-                                                   float S, float (&acc)[4]) {
-  float x[32];
+template <int TQ>
+__device__ __forceinline__ void gemv_compute(const GemvSlot<TQ>& R, bool gvalid, const uint32_t* __restrict__ xg,
+                                             float S, float (&acc)[4]) {
+  uint32_t xp[16];
 #pragma unroll
-  for (int v = 0; v < 8; ++v) {
-    const f32x4 xv = *reinterpret_cast<const f32x4*>(xg + 4 * v);
-    x[4 * v + 0] = xv[0];
-    x[4 * v + 1] = xv[1];
-    x[4 * v + 2] = xv[2];
-    x[4 * v + 3] = xv[3];
+  for (int v = 0; v < 4; ++v) {
+    const u32x4 xv = *reinterpret_cast<const u32x4*>(xg + 4 * v);
+    xp[4 * v + 0] = xv[0];
+    xp[4 * v + 1] = xv[1];
+    xp[4 * v + 2] = xv[2];
+    xp[4 * v + 3] = xv[3];
   }
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    if (t < tq) {
-      const float dot = group_dot(R.q[t], x);
-      acc[t] = fmaf(bf16_to_f32(R.s[t]), dot, acc[t]);
-      acc[t] = fmaf(bf16_to_f32(R.m[t]), S, acc[t]);
-    }
+  for (int t = 0; t < TQ; ++t) {
+    const float dot = group_dot_bf16(R.q[t], xp);
+    // Groups past K (block padding) contribute nothing whatever the padding holds.
+    const float d = gvalid ? bf16_to_f32(R.s[t]) : 0.0f;
+    const float m = gvalid ? bf16_to_f32(R.m[t]) : 0.0f;
+    acc[t] = fmaf(d, dot, acc[t]);
+    acc[t] = fmaf(m, S, acc[t]);
   }
 }
 
+template <int TQ, int D>
 __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs args) {
   // Dynamic LDS: red[16*32] | ssum[chunk*8] | xs[chunk*8*36], chunk = the
   // launch's largest staged block count (at most kGemvChunkBlocks).
   extern __shared__ __attribute__((aligned(16))) float lds[];
   float* red = lds;
   float* ssum = lds + kRedFloats;
-  float* xs = ssum + args.chunk_blocks * kGroupsPerRow;
+  uint32_t* xs = reinterpret_cast<uint32_t*>(ssum + args.chunk_blocks * kGroupsPerRow);
 
   const int wg = blockIdx.x;
   int jb = 0;
@@ -241,9 +287,11 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
     if (t < args.njobs && wg >= args.job[t].wg_begin) jb = t;
   const GemvJob& J = args.job[jb];
 
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  // The wave index is uniform across a wave; saying so keeps every block
+  // offset and branch derived from it in scalar registers.
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c = lane & 7;
-  const int W = J.waves, tq = J.tq;
+  const int W = J.waves;
   const int nthreads = blockDim.x;
   const bool wave_on = w < W;  // wave-uniform
   const int CB = args.chunk_blocks;
@@ -251,7 +299,7 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
   int staged = -1;  // chunk currently held in LDS
 
   for (int rg = wg - J.wg_begin; rg < J.nrg; rg += J.nwg) {
-    const int row0 = rg * 8 * tq;
+    const int row0 = rg * 8 * TQ;
     const int strip = row0 >> 5, t0 = (row0 & 31) >> 3;
     const uint8_t* sblob = J.blob + (size_t)strip * J.KB * kBlockBytes;
     float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -259,47 +307,48 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
     for (int ch = 0; ch < nchunks; ++ch) {
       const int jc0 = ch * CB;
       const int nb = min(CB, J.KB - jc0);
-      // First block of this wave: issue its loads before the x staging.
-      GemvBlockRegs A, B;
-      {
-        const int j = jc0 + w;
-        const bool ok = wave_on && w < nb && (j * kBlockCols + kGroup * c < J.K);
-        gemv_load_block(sblob + (size_t)j * kBlockBytes, ok, t0, tq, lane, A);
-      }
+      const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(sblob + (size_t)jc0 * kBlockBytes, nb * kBlockBytes);
+      const int kvalid = J.K - jc0 * kBlockCols;  // columns of this chunk inside K
+      // The wave's first D blocks go in flight before the x staging.
+      GemvSlot<TQ> buf[D];
+#pragma unroll
+      for (int d = 0; d < D; ++d)
+        if (wave_on && w + d * W < nb) gemv_load<TQ>(rs, w + d * W, t0, lane, buf[d]);
       if (staged != ch) {
         __syncthreads();  // every wave is done with the previous chunk
+        // Thread e stages columns 8e..8e+7 as the four bf16 pairs
+        // (x0,x2) (x4,x6) (x1,x3) (x5,x7) and adds them to its group's sum.
         const int kbeg = jc0 * kBlockCols;
-        const uint32_t* x2 = reinterpret_cast<const uint32_t*>(J.x);
-        for (int e = threadIdx.x; e < nb * (kBlockCols / 2); e += nthreads) {
-          const int k = kbeg + 2 * e;
-          const uint32_t v = (k < J.K) ? x2[k >> 1] : 0u;
-          const float xa = __uint_as_float(v << 16), xb = __uint_as_float(v & 0xFFFF0000u);
-          const int g = e >> 4, o = (2 * e) & 31;
-          xs[g * kGroupPad + o] = xa;
-          xs[g * kGroupPad + o + 1] = xb;
-          float sm = xa + xb;
+        for (int e = threadIdx.x; e < nb * (kBlockCols / 8); e += nthreads) {
+          const int k = kbeg + 8 * e;
+          u32x4 v = (u32x4){0u, 0u, 0u, 0u};
+          if (k < J.K) v = *reinterpret_cast<const u32x4*>(J.x + k);
+          const uint32_t p02 = (v[0] & 0xFFFFu) | (v[1] << 16), p46 = (v[2] & 0xFFFFu) | (v[3] << 16);
+          const uint32_t p13 = (v[0] >> 16) | (v[1] & 0xFFFF0000u), p57 = (v[2] >> 16) | (v[3] & 0xFFFF0000u);
+          const int g = e >> 2;
+          *reinterpret_cast<u32x4*>(xs + g * kGroupPadDw + 4 * (e & 3)) = (u32x4){p02, p46, p13, p57};
+          float sm = 0.0f;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) sm += __uint_as_float(v[i] << 16) + __uint_as_float(v[i] & 0xFFFF0000u);
           sm += __shfl_xor(sm, 1);
           sm += __shfl_xor(sm, 2);
-          sm += __shfl_xor(sm, 4);
-          sm += __shfl_xor(sm, 8);
-          if ((threadIdx.x & 15) == 0) ssum[g] = sm;
+          if ((threadIdx.x & 3) == 0) ssum[g] = sm;
         }
         __syncthreads();
         staged = ch;
       }
       if (wave_on) {
-        for (int jj = w; jj < nb; jj += 2 * W) {
-          const int j1 = jj + W, j2 = jj + 2 * W;
-          if (j1 < nb)
-            gemv_load_block(sblob + (size_t)(jc0 + j1) * kBlockBytes,
-                            (jc0 + j1) * kBlockCols + kGroup * c < J.K, t0, tq, lane, B);
-          gemv_compute_block(A, tq, xs + (jj * kGroupsPerRow + c) * kGroupPad, ssum[jj * kGroupsPerRow + c], acc);
-          if (j1 < nb) {
-            if (j2 < nb)
-              gemv_load_block(sblob + (size_t)(jc0 + j2) * kBlockBytes,
-                              (jc0 + j2) * kBlockCols + kGroup * c < J.K, t0, tq, lane, A);
-            gemv_compute_block(B, tq, xs + (j1 * kGroupsPerRow + c) * kGroupPad, ssum[j1 * kGroupsPerRow + c],
-                               acc);
+        // Ring of D register slots: block w + iW lives in slot i % D and the
+        // slot is refilled with block w + (i + D)W right after it is consumed.
+        for (int i0 = 0; w + i0 * W < nb; i0 += D) {
+#pragma unroll
+          for (int d = 0; d < D; ++d) {
+            const int jj = w + (i0 + d) * W;
+            if (jj < nb) {
+              gemv_compute<TQ>(buf[d], jj * kBlockCols + kGroup * c < kvalid,
+                               xs + (jj * kGroupsPerRow + c) * kGroupPadDw, ssum[jj * kGroupsPerRow + c], acc);
+              if (jj + D * W < nb) gemv_load<TQ>(rs, jj + D * W, t0, lane, buf[d]);
+            }
           }
         }
       }
@@ -307,18 +356,18 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
 
     // Add the 8 groups of each row: lanes 8r'..8r'+7 hold row octet t, row r'.
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
+    for (int t = 0; t < TQ; ++t) {
       acc[t] += __shfl_xor(acc[t], 1);
       acc[t] += __shfl_xor(acc[t], 2);
       acc[t] += __shfl_xor(acc[t], 4);
     }
-    // Lane with c == t (t < tq) holds row 8t + l/8 of the row group.
-    if (wave_on && c < tq) {
+    // Lane with c == t (t < TQ) holds row 8t + l/8 of the row group.
+    if (wave_on && c < TQ) {
       const float v = (c == 0) ? acc[0] : (c == 1) ? acc[1] : (c == 2) ? acc[2] : acc[3];
       red[w * 32 + 8 * c + (lane >> 3)] = v;
     }
     __syncthreads();
-    if (threadIdx.x < 8 * tq) {
+    if (threadIdx.x < 8 * TQ) {
       float sum = 0.0f;
       for (int q = 0; q < W; ++q) sum += red[q * 32 + threadIdx.x];
       const int64_t n = (int64_t)row0 + threadIdx.x;
@@ -389,13 +438,14 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
       const float d = bf16_to_f32(load_u16(blk + kCodeBytes + 2 * (8 * r + c)));
       const float m = bf16_to_f32(load_u16(blk + kCodeBytes + kScaleBytes + 2 * (8 * r + c)));
       float f[32];
-      codes_to_f32(q, f);
+      codes_to_f32_scaled(q, f);
+      const float d512 = d * 512.0f;
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        wv[v][0] = pack_bf16x2(fmaf(f[8 * v + 0], d, m), fmaf(f[8 * v + 1], d, m));
-        wv[v][1] = pack_bf16x2(fmaf(f[8 * v + 2], d, m), fmaf(f[8 * v + 3], d, m));
-        wv[v][2] = pack_bf16x2(fmaf(f[8 * v + 4], d, m), fmaf(f[8 * v + 5], d, m));
-        wv[v][3] = pack_bf16x2(fmaf(f[8 * v + 6], d, m), fmaf(f[8 * v + 7], d, m));
+        wv[v][0] = pack_bf16x2(eq3(f[8 * v + 0], d512, m), eq3(f[8 * v + 1], d512, m));
+        wv[v][1] = pack_bf16x2(eq3(f[8 * v + 2], d512, m), eq3(f[8 * v + 3], d512, m));
+        wv[v][2] = pack_bf16x2(eq3(f[8 * v + 4], d512, m), eq3(f[8 * v + 5], d512, m));
+        wv[v][3] = pack_bf16x2(eq3(f[8 * v + 6], d512, m), eq3(f[8 * v + 7], d512, m));
       }
     } else {
 #pragma unroll
@@ -456,17 +506,31 @@ static q4nx_status check_launch(const char* fn) {
   return Q4NX_OK;
 }
 
-// Waves that split K: about two blocks per wave, at most 16.  A function of K
-// alone, so a projection is summed in the same order alone or in a batch.
-static int gemv_waves(int KB) { return std::max(1, std::min(kGemvMaxWaves, (KB + 1) / 2)); }
-
 // Row-group size: whole strips when there are enough of them to keep at least
 // ~160 CUs streaming (one CU sustains ~55 GB/s of the ~7 TB/s), else halves or
 // quarters of strips.  `strips` is the number of strips of the whole launch.
 static int gemv_tq(int64_t strips) {
+#ifdef Q4NX_TUNE
+  if (const char* e = getenv("Q4NX_TUNE_TQ")) return atoi(e);
+#endif
   if (strips >= 160) return 4;
   if (strips * 2 >= 160) return 2;
   return 1;
+}
+
+// Waves per workgroup (they split K).  A power of two, so that workgroups tile
+// the 16 waves a CU holds at this kernel's register budget; fewer waves per
+// row group when the launch has many row groups (longer streams per wave),
+// more when it has few (more parallelism per strip).  Capped so every wave
+// owns at least one block of every job.  Measured on MI355X over the Gemma3
+// 1B/4B/27B projection shapes.
+static int gemv_waves(int64_t row_groups, int min_kb) {
+#ifdef Q4NX_TUNE
+  if (const char* e = getenv("Q4NX_TUNE_WAVES")) return std::max(1, std::min(kGemvMaxWaves, atoi(e)));
+#endif
+  int w = row_groups >= 4096 ? 2 : row_groups >= 512 ? 4 : row_groups >= 128 ? 8 : 16;
+  while (w > 1 && w > min_kb) w >>= 1;
+  return w;
 }
 
 static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtype y_dtype, hipStream_t stream,
@@ -486,6 +550,9 @@ static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtyp
     strips += ceil_div(d.N, kBlockRows);
   }
   const int tq = gemv_tq(strips);
+  int min_kb = 1 << 30;
+  for (int i = 0; i < count; ++i) min_kb = std::min<int>(min_kb, (int)ceil_div(descs[i].K, kBlockCols));
+  const int waves = gemv_waves(strips * (4 / tq), min_kb);
   GemvArgs args = {};
   args.njobs = count;
   args.y_bf16 = (y_dtype == Q4NX_BF16);
@@ -503,17 +570,22 @@ static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtyp
     J.KB = (int)ceil_div(d.K, kBlockCols);
     J.tq = tq;
     J.nrg = J.NS * (4 / tq);
-    J.waves = gemv_waves(J.KB);
-    // Up to 2048 workgroups per job; beyond that a workgroup loops over row
-    // groups and reuses the x it staged.
-    J.nwg = std::min(J.nrg, 2048);
+    J.waves = waves;
+    // One workgroup per row group (the hardware keeps every CU fed as
+    // workgroups retire); the loop over row groups only engages past 2^20.
+    J.nwg = std::min(J.nrg, 1 << 20);
     J.wg_begin = (int)wg;
     wg += J.nwg;
     max_waves = std::max(max_waves, J.waves);
     args.chunk_blocks = std::max(args.chunk_blocks, std::min(J.KB, kGemvChunkBlocks));
   }
-  const size_t lds = sizeof(float) * ((size_t)kRedFloats + (size_t)args.chunk_blocks * kGroupsPerRow * (1 + kGroupPad));
-  hipLaunchKernelGGL(gemv_kernel, dim3((unsigned)wg), dim3(64 * max_waves), lds, stream, args);
+  const size_t lds = sizeof(float) * ((size_t)kRedFloats + (size_t)args.chunk_blocks * kGroupsPerRow * (1 + kGroupPadDw));
+  const dim3 grid((unsigned)wg), block(64 * max_waves);
+  switch (tq) {
+    case 4: hipLaunchKernelGGL((gemv_kernel<4, kGemvDepth4>), grid, block, lds, stream, args); break;
+    case 2: hipLaunchKernelGGL((gemv_kernel<2, kGemvDepth2>), grid, block, lds, stream, args); break;
+    default: hipLaunchKernelGGL((gemv_kernel<1, kGemvDepth1>), grid, block, lds, stream, args); break;
+  }
   return check_launch(fn);
 }
 
