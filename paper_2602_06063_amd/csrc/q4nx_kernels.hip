@@ -385,111 +385,233 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
 // ---------------------------------------------------------------------------
 // q4nx_gemm: fused dequant + bf16 MFMA matrix product
 // ---------------------------------------------------------------------------
-// Workgroup tile 128 (tokens) x 128 (outputs), K step 64 (two groups), four
-// waves in a 2 x 2 arrangement, each owning 64 x 64 outputs as 2 x 2 tiles of
-// v_mfma_f32_32x32x16_bf16.  Per K step every thread stages 32 bf16 of X and
-// dequantizes one group (32 weights) of W -- Eq. 3 in float32, rounded to bf16
-// -- into LDS.  Rows are padded to 72 bf16 (144 B) so the 16-byte fragment
-// reads of 8 consecutive rows fall in distinct banks.
-constexpr int kBM = 128, kBN = 128, kBK = 64;
+// Workgroup tile BM (tokens) x BN (outputs), K step 64 (two quantization
+// groups).  WAVES_M x WAVES_N waves; each owns a (BM/WAVES_M) x (BN/WAVES_N)
+// sub-tile as 32 x 32 tiles of v_mfma_f32_32x32x16_bf16 (float32
+// accumulators).  LDS holds two stages of the X tile and of the dequantized W
+// tile (bf16, rows padded to 72 elements = 144 B so the 16-byte fragment
+// reads of 8 consecutive rows hit distinct banks).  In the steady state a
+// K step runs the MFMAs of step k from one LDS stage while the same waves
+// dequantize step k+1 -- Eq. 3 in float32, rounded to bf16 (the paper's
+// prefill dequantizes to bf16 before the MM) -- into the other stage, with
+// the instruction streams interleaved; the raw global data of step k+1 was
+// loaded into registers two steps earlier, so neither waits on memory.  One
+// workgroup barrier per K step.
+constexpr int kBK = 64;
 constexpr int kLdsStride = kBK + 8;  // bf16 elements per LDS row
 
-__global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ X, const uint8_t* __restrict__ blob,
-                                                   void* __restrict__ Y, int M, int N, int K, int KB, int NS,
-                                                   int tiles_n, int y_bf16) {
-  __shared__ __attribute__((aligned(16))) uint16_t xs[kBM * kLdsStride];
-  __shared__ __attribute__((aligned(16))) uint16_t ws[kBN * kLdsStride];
+// Tile order.  Workgroups are dispatched round-robin over the 8 XCDs, each
+// with its own L2.  Workgroup w runs on XCD w % 8, so XCD x is given the
+// contiguous range of logical tiles [x*T/8, (x+1)*T/8); logical tiles are
+// ordered in groups of kGroupM tile rows, column by column, so the tiles an
+// XCD runs at the same time share a few X row blocks and W column blocks in
+// its L2 instead of streaming the whole operands from the memory-side cache.
+constexpr int kXcds = 8;
+constexpr int kGroupM = 4;
 
-  const int tile = blockIdx.x;
-  const int bn = tile % tiles_n, bm = tile / tiles_n;
-  const int m0 = bm * kBM, n0 = bn * kBN;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+__device__ __forceinline__ void gemm_tile_of(int wg, int ntiles, int tiles_n, int& bm, int& bn) {
+  const int x = wg % kXcds, l = wg / kXcds;
+  const int base = ntiles / kXcds, rem = ntiles % kXcds;
+  const int t = x * base + min(x, rem) + l;
+  const int tiles_m = ntiles / tiles_n;
+  const int group = t / (kGroupM * tiles_n);
+  const int rows = min(kGroupM, tiles_m - group * kGroupM);  // tile rows in this (last) group
+  const int r = t - group * kGroupM * tiles_n;
+  bm = group * kGroupM + r % rows;
+  bn = r / rows;
+}
 
-  // staging role: row lr of the tile, half h (columns 32h..32h+31 of the K step)
-  const int lr = tid >> 1, h = tid & 1;
-  const int gm = m0 + lr, gn = n0 + lr;
-  const int strip = gn >> 5, r = gn & 31;
+template <int BM, int BN, int WAVES_M, int WAVES_N>
+struct GemmCfg {
+  static constexpr int kThreads = 64 * WAVES_M * WAVES_N;
+  static constexpr int kWTM = BM / WAVES_M, kWTN = BN / WAVES_N;
+  static constexpr int kTI = kWTM / 32, kTJ = kWTN / 32;
+  static constexpr int kXChunks = BM * (kBK / 8) / kThreads;   // 16-byte X chunks per thread per step
+  // Weight groups per step and per thread (threads past the step's groups --
+  // whole waves, since BN * 2 is a multiple of 64 -- dequantize none).
+  static constexpr int kStepGroups = BN * (kBK / kGroup);
+  static constexpr int kWGroups = (kStepGroups + kThreads - 1) / kThreads;
+  static constexpr int kLdsElems = 2 * (BM + BN) * kLdsStride;
+  static_assert(kXChunks >= 1 && kWGroups >= 1, "tile too small for the thread count");
+  static_assert(kTI >= 1 && kTJ >= 1, "wave tile below 32 x 32");
+};
 
-  f32x16 acc[2][2];
+// Raw global data of one K step held by one thread: its X chunks and the
+// codes / scale / offset of its weight groups.
+template <int XC, int WG>
+struct GemmRegs {
+  u32x4 x[XC];
+  u32x4 q[WG];
+  uint32_t s[WG], m[WG];
+};
+
+// Scheduling hint: interleave the MFMAs of a K step with the VALU and LDS
+// work of the next step's dequantization (masks: 0x008 MFMA, 0x002 VALU,
+// 0x100 LDS read, 0x200 LDS write).
+#ifndef Q4NX_GEMM_VALU_PER_MFMA
+#define Q4NX_GEMM_VALU_PER_MFMA 3
+#endif
+
+template <int BM, int BN, int WAVES_M, int WAVES_N>
+__global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
+    const uint16_t* __restrict__ X, const uint8_t* __restrict__ blob, void* __restrict__ Y, int M, int N, int K,
+    int KB, int NS, int tiles_n, int y_bf16) {
+  using C = GemmCfg<BM, BN, WAVES_M, WAVES_N>;
+  using Regs = GemmRegs<C::kXChunks, C::kWGroups>;
+  extern __shared__ __attribute__((aligned(16))) uint16_t gl[];
+  uint16_t* xs0 = gl;                              // [2][BM][72]
+  uint16_t* ws0 = gl + 2 * BM * kLdsStride;        // [2][BN][72]
+
+  int bm, bn;
+  gemm_tile_of(blockIdx.x, gridDim.x, tiles_n, bm, bn);
+  const int m0 = bm * BM, n0 = bn * BN;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave / WAVES_N, wn = wave % WAVES_N;
+
+  f32x16 acc[C::kTI][C::kTJ];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < C::kTI; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b)
+    for (int b = 0; b < C::kTJ; ++b)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
 
-  for (int k0 = 0; k0 < K; k0 += kBK) {
-    const int gk = k0 + 32 * h;
-    u32x4 xv[4];
-    if (gm < M && gk < K) {
-      const u32x4* src = reinterpret_cast<const u32x4*>(X + (size_t)gm * K + gk);
+  // Global loads of step k0 into registers.  Row and column indices are
+  // clamped so every address is inside the operands; the values that belong
+  // outside the matrices are zeroed only when the step is stored, so nothing
+  // here waits for the loads to return.
+  auto load_step = [&](Regs& R, int k0) {
 #pragma unroll
-      for (int v = 0; v < 4; ++v) xv[v] = src[v];
-    } else {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) xv[v] = (u32x4){0u, 0u, 0u, 0u};
+    for (int i = 0; i < C::kXChunks; ++i) {
+      const int ch = tid + i * C::kThreads;       // chunk: row ch/8, columns 8(ch%8)..+7
+      const int r = ch >> 3, kk = k0 + 8 * (ch & 7);
+      R.x[i] = *reinterpret_cast<const u32x4*>(X + (size_t)min(m0 + r, M - 1) * K + min(kk, K - 8));
     }
-    u32x4 wv[4];
-    if (strip < NS && gk < K) {
+#pragma unroll
+    for (int i = 0; i < C::kWGroups; ++i) {
+      const int gi = tid + i * C::kThreads;       // group: row gi/2, half gi%2 of the K step
+      if (C::kStepGroups % C::kThreads != 0 && gi >= C::kStepGroups) break;  // wave-uniform
+      const int r = gi >> 1, gk = min(k0 + kGroup * (gi & 1), K - kGroup);
+      const int gn = n0 + r, rr = gn & 31;
       const int j = gk >> 8, c = (gk & 255) >> 5;
-      const uint8_t* blk = blob + ((size_t)strip * KB + j) * kBlockBytes;
-      const u32x4 q = load_codes(blk + 128 * r + 16 * c);
-      const float d = bf16_to_f32(load_u16(blk + kCodeBytes + 2 * (8 * r + c)));
-      const float m = bf16_to_f32(load_u16(blk + kCodeBytes + kScaleBytes + 2 * (8 * r + c)));
+      const uint8_t* blk = blob + ((size_t)min(gn >> 5, NS - 1) * KB + j) * kBlockBytes;
+      R.q[i] = load_codes(blk + 128 * rr + 16 * c);
+      R.s[i] = load_u16(blk + kCodeBytes + 2 * (8 * rr + c));
+      R.m[i] = load_u16(blk + kCodeBytes + kScaleBytes + 2 * (8 * rr + c));
+    }
+  };
+
+  // Zero what lies outside the matrices, dequantize the weight groups (Eq. 3
+  // in float32, rounded to bf16) and write X and W of step k0 to LDS stage st.
+  auto store_step = [&](const Regs& R, int st, int k0) {
+    uint16_t* xs = xs0 + st * BM * kLdsStride;
+    uint16_t* ws = ws0 + st * BN * kLdsStride;
+#pragma unroll
+    for (int i = 0; i < C::kXChunks; ++i) {
+      const int ch = tid + i * C::kThreads;
+      const bool ok = m0 + (ch >> 3) < M && k0 + 8 * (ch & 7) < K;
+      *reinterpret_cast<u32x4*>(xs + (ch >> 3) * kLdsStride + 8 * (ch & 7)) = ok ? R.x[i] : (u32x4){0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int i = 0; i < C::kWGroups; ++i) {
+      const int gi = tid + i * C::kThreads;
+      if (C::kStepGroups % C::kThreads != 0 && gi >= C::kStepGroups) break;  // wave-uniform
+      const bool ok = ((n0 + (gi >> 1)) >> 5) < NS && k0 + kGroup * (gi & 1) < K;
       float f[32];
-      codes_to_f32_scaled(q, f);
-      const float d512 = d * 512.0f;
+      codes_to_f32_scaled(ok ? R.q[i] : (u32x4){0u, 0u, 0u, 0u}, f);
+      const float d512 = ok ? bf16_to_f32(R.s[i]) * 512.0f : 0.0f, m = ok ? bf16_to_f32(R.m[i]) : 0.0f;
+      u32x4* wd = reinterpret_cast<u32x4*>(ws + (gi >> 1) * kLdsStride + kGroup * (gi & 1));
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
-        wv[v][0] = pack_bf16x2(eq3(f[8 * v + 0], d512, m), eq3(f[8 * v + 1], d512, m));
-        wv[v][1] = pack_bf16x2(eq3(f[8 * v + 2], d512, m), eq3(f[8 * v + 3], d512, m));
-        wv[v][2] = pack_bf16x2(eq3(f[8 * v + 4], d512, m), eq3(f[8 * v + 5], d512, m));
-        wv[v][3] = pack_bf16x2(eq3(f[8 * v + 6], d512, m), eq3(f[8 * v + 7], d512, m));
-      }
-    } else {
-#pragma unroll
-      for (int v = 0; v < 4; ++v) wv[v] = (u32x4){0u, 0u, 0u, 0u};
-    }
-    __syncthreads();
-    {
-      u32x4* xd = reinterpret_cast<u32x4*>(xs + lr * kLdsStride + 32 * h);
-      u32x4* wd = reinterpret_cast<u32x4*>(ws + lr * kLdsStride + 32 * h);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        xd[v] = xv[v];
-        wd[v] = wv[v];
+        u32x4 o;
+        o[0] = pack_bf16x2(eq3(f[8 * v + 0], d512, m), eq3(f[8 * v + 1], d512, m));
+        o[1] = pack_bf16x2(eq3(f[8 * v + 2], d512, m), eq3(f[8 * v + 3], d512, m));
+        o[2] = pack_bf16x2(eq3(f[8 * v + 4], d512, m), eq3(f[8 * v + 5], d512, m));
+        o[3] = pack_bf16x2(eq3(f[8 * v + 6], d512, m), eq3(f[8 * v + 7], d512, m));
+        wd[v] = o;
       }
     }
-    __syncthreads();
+  };
+
+  // The MFMAs of one K step from LDS stage st.
+  auto mma_step = [&](int st) {
+    const uint16_t* xs = xs0 + st * BM * kLdsStride;
+    const uint16_t* ws = ws0 + st * BN * kLdsStride;
 #pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
-      const int kk = ks * 16 + 8 * (lane >> 5);
-      bf16x8 af[2], bfr[2];
+    for (int kq = 0; kq < kBK / 16; ++kq) {
+      const int kk = kq * 16 + 8 * (lane >> 5);
+      bf16x8 af[C::kTI], bfr[C::kTJ];
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
-        af[a] = *reinterpret_cast<const bf16x8*>(xs + (64 * wm + 32 * a + (lane & 31)) * kLdsStride + kk);
+      for (int a = 0; a < C::kTI; ++a)
+        af[a] = *reinterpret_cast<const bf16x8*>(xs + (C::kWTM * wm + 32 * a + (lane & 31)) * kLdsStride + kk);
 #pragma unroll
-      for (int b = 0; b < 2; ++b)
-        bfr[b] = *reinterpret_cast<const bf16x8*>(ws + (64 * wn + 32 * b + (lane & 31)) * kLdsStride + kk);
+      for (int b = 0; b < C::kTJ; ++b)
+        bfr[b] = *reinterpret_cast<const bf16x8*>(ws + (C::kWTN * wn + 32 * b + (lane & 31)) * kLdsStride + kk);
 #pragma unroll
-      for (int a = 0; a < 2; ++a)
+      for (int a = 0; a < C::kTI; ++a)
 #pragma unroll
-        for (int b = 0; b < 2; ++b)
+        for (int b = 0; b < C::kTJ; ++b)
           acc[a][b] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[a], bfr[b], acc[a][b], 0, 0, 0);
     }
+  };
+
+  // One steady-state iteration: MFMAs of step ks (stage ks&1) interleaved
+  // with the dequantization of step ks+1 (held in Rn) into the other stage;
+  // then the loads of step ks+3 into Rn (two steps of register prefetch).
+  auto interleave = [&]() {
+#if Q4NX_GEMM_VALU_PER_MFMA > 0
+#pragma unroll
+    for (int i = 0; i < C::kTI * C::kTJ * (kBK / 16); ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, Q4NX_GEMM_VALU_PER_MFMA, 0);
+    }
+#endif
+  };
+
+  const int nsteps = (K + kBK - 1) / kBK;
+  Regs R0, R1;
+  load_step(R0, 0);
+  store_step(R0, 0, 0);
+  load_step(R0, kBK);
+  load_step(R1, 2 * kBK);
+  __syncthreads();
+  int ks = 0;
+  // Steady state, two steps per trip so the register sets stay static.
+  for (; ks + 2 < nsteps; ks += 2) {
+    mma_step(0);
+    store_step(R0, 1, (ks + 1) * kBK);
+    interleave();
+    // Unconditional (addresses are clamped; data past the last step is never
+    // stored), so the wait-count bookkeeping sees the same load order on every
+    // trip and waits only for the register set being consumed.
+    load_step(R0, (ks + 3) * kBK);
+    __syncthreads();
+    mma_step(1);
+    store_step(R1, 0, (ks + 2) * kBK);
+    interleave();
+    load_step(R1, (ks + 4) * kBK);
+    __syncthreads();
   }
+  // Tail: one or two steps left; step ks+1 (if any) is in R0.
+  if (ks + 1 < nsteps) {
+    mma_step(ks & 1);
+    store_step(R0, (ks + 1) & 1, (ks + 1) * kBK);
+    __syncthreads();
+    ++ks;
+  }
+  mma_step(ks & 1);
 
   // Accumulator element e of lane l: column l%32, row 8(e/4) + 4(l/32) + e%4.
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < C::kTI; ++a)
 #pragma unroll
-    for (int b = 0; b < 2; ++b) {
-      const int col = n0 + 64 * wn + 32 * b + (lane & 31);
+    for (int b = 0; b < C::kTJ; ++b) {
+      const int col = n0 + C::kWTN * wn + 32 * b + (lane & 31);
       if (col >= N) continue;
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int row = m0 + 64 * wm + 32 * a + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int row = m0 + C::kWTM * wm + 32 * a + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         if (row < M) {
           if (y_bf16)
             static_cast<uint16_t*>(Y)[(size_t)row * N + col] = f32_to_bf16_bits(acc[a][b][e]);
@@ -498,6 +620,27 @@ __global__ __launch_bounds__(256) void gemm_kernel(const uint16_t* __restrict__ 
         }
       }
     }
+}
+
+template <int BM, int BN, int WAVES_M, int WAVES_N>
+static q4nx_status launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* X, const void* blob, void* Y,
+                               int y_bf16, hipStream_t stream) {
+  using Cfg = GemmCfg<BM, BN, WAVES_M, WAVES_N>;
+  const int64_t tiles_n = ceil_div(N, BN), tiles_m = ceil_div(M, BM);
+  if (tiles_n * tiles_m > 0x7FFFFFFF) return fail(Q4NX_ERR_SHAPE, "q4nx_gemm: problem too large for one launch");
+  const size_t lds = sizeof(uint16_t) * Cfg::kLdsElems;
+  auto kern = gemm_kernel<BM, BN, WAVES_M, WAVES_N>;
+  static bool attr_set = false;  // LDS above 64 KiB must be requested once per kernel
+  if (!attr_set) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)lds) != hipSuccess)
+      return fail(Q4NX_ERR_HIP, "q4nx_gemm: cannot reserve LDS");
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_n * tiles_m)), dim3(Cfg::kThreads), lds, stream, X,
+                     static_cast<const uint8_t*>(blob), Y, (int)M, (int)N, (int)K, (int)ceil_div(K, kBlockCols),
+                     (int)ceil_div(N, kBlockRows), (int)tiles_n, y_bf16);
+  return Q4NX_OK;
 }
 
 static q4nx_status check_launch(const char* fn) {
@@ -633,13 +776,20 @@ q4nx_status q4nx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, cons
     return fail(Q4NX_ERR_INVALID_ARG, "q4nx_gemm: unknown y_dtype");
   if (!aligned(d_X, 16) || !aligned(d_blob, 16) || !aligned(d_Y, 16))
     return fail(Q4NX_ERR_ALIGNMENT, "q4nx_gemm: X, blob and Y need 16-byte alignment");
-  const int64_t tiles_n = ceil_div(N, kBN), tiles_m = ceil_div(M, kBM);
-  if (tiles_n * tiles_m > 0x7FFFFFFF || M * N > (int64_t(1) << 40))
-    return fail(Q4NX_ERR_SHAPE, "q4nx_gemm: problem too large for one launch");
-  hipLaunchKernelGGL(gemm_kernel, dim3((unsigned)(tiles_n * tiles_m)), dim3(256), 0, stream, d_X,
-                     static_cast<const uint8_t*>(d_blob), d_Y, (int)M, (int)N, (int)K,
-                     (int)ceil_div(K, kBlockCols), (int)ceil_div(N, kBlockRows), (int)tiles_n,
-                     (int)(y_dtype == Q4NX_BF16));
+  if (M * N > (int64_t(1) << 40)) return fail(Q4NX_ERR_SHAPE, "q4nx_gemm: problem too large for one launch");
+  // Largest tile that still gives about one workgroup per CU.
+  const int yb = (y_dtype == Q4NX_BF16);
+  const auto tiles = [&](int bm, int bn) { return ceil_div(M, bm) * ceil_div(N, bn); };
+  q4nx_status st;
+  if (tiles(256, 256) >= 240)
+    st = launch_gemm<256, 256, 2, 4>(M, N, K, d_X, d_blob, d_Y, yb, stream);
+  else if (tiles(256, 128) >= 240)
+    st = launch_gemm<256, 128, 4, 2>(M, N, K, d_X, d_blob, d_Y, yb, stream);
+  else if (tiles(128, 128) >= 200)
+    st = launch_gemm<128, 128, 2, 4>(M, N, K, d_X, d_blob, d_Y, yb, stream);
+  else
+    st = launch_gemm<128, 64, 2, 2>(M, N, K, d_X, d_blob, d_Y, yb, stream);
+  if (st != Q4NX_OK) return st;
   return check_launch("q4nx_gemm");
 }
 
