@@ -330,7 +330,7 @@ def main():
             result["value_gemm"] = round(pre_tflops, 2)
     # Dominant kernel by time: the GEMM when the step has a prefill chunk.
     if do_prefill:
-        result["roofline"] = {"kernel": "gemm_kernel", "bound": "mfma", "achieved": round(pre_tflops, 2),
+        result["roofline"] = {"kernel": "q4nx_gemm launches (gemm256_kernel, gemm_kernel)", "bound": "mfma", "achieved": round(pre_tflops, 2),
                               "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                               "frac": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None}
     if do_decode:

@@ -385,18 +385,14 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
 // ---------------------------------------------------------------------------
 // q4nx_gemm: fused dequant + bf16 MFMA matrix product
 // ---------------------------------------------------------------------------
-// Workgroup tile BM (tokens) x BN (outputs), K step 64 (two quantization
-// groups).  WAVES_M x WAVES_N waves; each owns a (BM/WAVES_M) x (BN/WAVES_N)
-// sub-tile as 32 x 32 tiles of v_mfma_f32_32x32x16_bf16 (float32
-// accumulators).  LDS holds two stages of the X tile and of the dequantized W
-// tile (bf16, rows padded to 72 elements = 144 B so the 16-byte fragment
-// reads of 8 consecutive rows hit distinct banks).  In the steady state a
-// K step runs the MFMAs of step k from one LDS stage while the same waves
-// dequantize step k+1 -- Eq. 3 in float32, rounded to bf16 (the paper's
-// prefill dequantizes to bf16 before the MM) -- into the other stage, with
-// the instruction streams interleaved; the raw global data of step k+1 was
-// loaded into registers two steps earlier, so neither waits on memory.  One
-// workgroup barrier per K step.
+// Every kernel below walks K in steps of 64 (two quantization groups) and
+// feeds v_mfma_f32_32x32x16_bf16 from LDS: the X tile as loaded (bf16) and
+// the W tile dequantized with Eq. 3 in float32 and rounded to bf16 (the
+// paper's prefill dequantizes to bf16 before the MM).  LDS rows are padded to
+// 72 elements (144 B) so that the 16-byte fragment reads of 8 consecutive
+// rows, and the 16-byte tile writes, hit distinct banks.  Each output is the
+// float32 sum of its MFMA chain over K in increasing order, so every kernel
+// and every tile shape gives the same bits.
 constexpr int kBK = 64;
 constexpr int kLdsStride = kBK + 8;  // bf16 elements per LDS row
 
@@ -421,6 +417,266 @@ __device__ __forceinline__ void gemm_tile_of(int wg, int ntiles, int tiles_n, in
   bn = r / rows;
 }
 
+// Dequantizes 8 consecutive weights (one 32-bit word of codes) of a group to
+// bf16 pairs in column order; d512 = d * 2^9 (see eq3).
+__device__ __forceinline__ u32x4 dequant8_bf16(uint32_t codes, float d512, float m) {
+  const uint32_t lo = opaque(codes & 0x0F0F0F0Fu);          // columns 0, 2, 4, 6
+  const uint32_t hi = opaque((codes >> 4) & 0x0F0F0F0Fu);   // columns 1, 3, 5, 7
+  const f32x2 a = codes2_f32<false>(lo), b = codes2_f32<true>(lo);
+  const f32x2 e = codes2_f32<false>(hi), g = codes2_f32<true>(hi);
+  u32x4 o;
+  o[0] = pack_bf16x2(eq3(a[0], d512, m), eq3(e[0], d512, m));
+  o[1] = pack_bf16x2(eq3(a[1], d512, m), eq3(e[1], d512, m));
+  o[2] = pack_bf16x2(eq3(b[0], d512, m), eq3(g[0], d512, m));
+  o[3] = pack_bf16x2(eq3(b[1], d512, m), eq3(g[1], d512, m));
+  return o;
+}
+
+// ---- 256 x 256 tile, one wave per SIMD ------------------------------------
+// Four waves in a 2 x 2 grid, each owning a 128 x 128 sub-tile: 16 MFMA
+// accumulators (256 accumulation registers, which live in the AGPR half of the
+// register file), so each 16-deep K slice costs 16 MFMAs against 8 fragment
+// reads -- half the LDS read traffic per MFMA of a 128 x 64 wave tile.  With
+// a single wave per SIMD nothing hides a stall, so the instruction order is
+// fixed by hand: a K step is four blocks of 16 MFMA slots, each slot one MFMA
+// plus a fixed share of the other work, fenced so the compiler keeps it there:
+//   slots  0-15  MFMAs of K slice 0 | fragment reads of slice 1 | X tile of
+//                the next step into the other LDS stage | weight group 0 of
+//                the next step dequantized (a quarter of 8 columns per slot)
+//   slots 16-31  slice 1 | reads of slice 2 | weight group 1 dequantized
+//   slots 32-47  slice 2 | reads of slice 3 | global loads of step + 3
+//   barrier      (the other stage is complete; this stage's reads are done)
+//   slots 48-63  slice 3 | reads of slice 0 of the next step
+// The raw operands of a step are loaded into registers two steps ahead.  X and
+// W are read through buffer descriptors limited to the tile's rows and strips;
+// in the last step of a K that is not a multiple of 64 the columns past K are
+// given an offset past the descriptor's end, which reads as zero -- code 0,
+// scale 0 and offset 0 give w = +0 -- so no mask is needed anywhere else.  X
+// rows past M and W strips past the matrix are clamped to the last valid one;
+// their outputs are never stored.
+constexpr int kWideThreads = 256;
+constexpr int kWideLdsBytes = 2 * 2 * 256 * kLdsStride * 2;  // two stages of X and W
+constexpr int64_t kWideMaxK = int64_t(1) << 22;               // 256 rows x K x 2 B < 2^31
+
+struct WideRegs {
+  u32x4 x[8];      // X: rows tid/8 + 32i, columns 8(tid%8)..+7 of the step
+  u32x4 q[2];      // W: codes of group (row tid/2 + 128g, half tid%2 of the step)
+  uint32_t s[2], m[2];
+};
+
+template <bool KTAIL>
+__global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* __restrict__ X,
+                                                               const uint8_t* __restrict__ blob,
+                                                               void* __restrict__ Y, int M, int N, int K, int ldy,
+                                                               int KB, int NS, int tiles_n, int y_bf16) {
+  constexpr int TI = 4, TJ = 4;
+  extern __shared__ __attribute__((aligned(16))) uint16_t gl[];
+  uint16_t* const xs0 = gl;                          // [2][256][72]
+  uint16_t* const ws0 = gl + 2 * 256 * kLdsStride;   // [2][256][72]
+
+  int bm, bn;
+  gemm_tile_of(blockIdx.x, gridDim.x, tiles_n, bm, bn);
+  const int m0 = bm * 256, n0 = bn * 256;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  const int rows_x = min(256, M - m0);
+  const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(X + (size_t)m0 * K), (short)0, rows_x * K * 2, 0x00020000);
+  const int s0 = n0 >> 5, nst = min(8, NS - s0);
+  const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(blob + (size_t)s0 * KB * kBlockBytes), (short)0, nst * KB * kBlockBytes, 0x00020000);
+  constexpr int kPastEnd = 0x7FFFFFF0;  // beyond every descriptor: loads return 0
+
+  const int c8 = tid & 7, half = tid & 1;
+  int vx[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) vx[i] = (min((tid >> 3) + 32 * i, rows_x - 1) * K + 8 * c8) * 2;
+  int vq[2], vs[2];
+#pragma unroll
+  for (int g = 0; g < 2; ++g) {
+    const int r = (tid >> 1) + 128 * g;
+    const int st = min(r >> 5, nst - 1), rr = r & 31;
+    vq[g] = st * KB * kBlockBytes + 128 * rr + 16 * half;
+    vs[g] = st * KB * kBlockBytes + kCodeBytes + 2 * (8 * rr + half);
+  }
+  const int nsteps = (K + kBK - 1) / kBK;
+
+  f32x16 acc[TI][TJ];
+#pragma unroll
+  for (int a = 0; a < TI; ++a)
+#pragma unroll
+    for (int b = 0; b < TJ; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
+
+  // Global loads of step t (clamped to the last step) into R, one of the 14
+  // loads per call (i = 0..13), so that they can be spread over MFMA slots.
+  auto load1 = [&](WideRegs& R, int t, int i) {
+    const int k0 = min(t, nsteps - 1) * kBK;
+    const int sq = (k0 >> 8) * kBlockBytes + 16 * ((k0 & 255) >> 5);
+    const int ss = (k0 >> 8) * kBlockBytes + 2 * ((k0 & 255) >> 5);
+    const bool okx = !KTAIL || k0 + 8 * c8 < K;
+    const bool okw = !KTAIL || k0 + kGroup * half < K;
+    if (i < 8) {
+      if (!KTAIL)
+        R.x[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsx, vx[i], 2 * k0, 0));
+      else
+        R.x[i] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsx, okx ? vx[i] + 2 * k0 : kPastEnd, 0, 0));
+    } else if (i < 10) {
+      const int g = i - 8;
+      R.q[g] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsw, okw ? vq[g] + sq : kPastEnd, 0, kNtLoad));
+    } else if (i < 12) {
+      const int g = i - 10;
+      R.s[g] = __builtin_amdgcn_raw_buffer_load_b16(rsw, okw ? vs[g] + ss : kPastEnd, 0, kNtLoad);
+    } else {
+      const int g = i - 12;
+      R.m[g] = __builtin_amdgcn_raw_buffer_load_b16(rsw, okw ? vs[g] + ss + kScaleBytes : kPastEnd, 0, kNtLoad);
+    }
+  };
+  auto xs_row = [&](int st) { return xs0 + st * 256 * kLdsStride + (tid >> 3) * kLdsStride + 8 * c8; };
+  auto ws_row = [&](int st, int g) {
+    return ws0 + st * 256 * kLdsStride + ((tid >> 1) + 128 * g) * kLdsStride + kGroup * half;
+  };
+  // Fragment i of K slice kq, in first-use order A0, B0, B1, B2, B3, A1, A2, A3.
+  const int fa = (128 * wm + (lane & 31)) * kLdsStride + 8 * (lane >> 5);
+  const int fb = (128 * wn + (lane & 31)) * kLdsStride + 8 * (lane >> 5);
+  auto read1 = [&](int st, int kq, bf16x8 (&A)[TI], bf16x8 (&B)[TJ], int i) {
+    const uint16_t* xs = xs0 + st * 256 * kLdsStride + fa + 16 * kq;
+    const uint16_t* ws = ws0 + st * 256 * kLdsStride + fb + 16 * kq;
+    if (i == 0) A[0] = *reinterpret_cast<const bf16x8*>(xs);
+    else if (i <= 4) B[i - 1] = *reinterpret_cast<const bf16x8*>(ws + 32 * (i - 1) * kLdsStride);
+    else A[i - 4] = *reinterpret_cast<const bf16x8*>(xs + 32 * (i - 4) * kLdsStride);
+  };
+  auto mma1 = [&](const bf16x8 (&A)[TI], const bf16x8 (&B)[TJ], int i) {
+    acc[i >> 2][i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[i >> 2], B[i & 3], acc[i >> 2][i & 3], 0, 0, 0);
+  };
+  // Dequantization of weight group g in 16 pieces: piece p handles a quarter
+  // of the 8 columns 8(p/4)..+7 (Eq. 3, as in dequant8_bf16).
+  uint32_t wlo = 0, whi = 0;
+  float wd = 0.0f, wmo = 0.0f;
+  f32x2 wa, we, wb, wg;
+  u32x4 wo;
+  auto wpiece = [&](const WideRegs& R, int st, int g, int p) {
+    const int u = p >> 2, qt = p & 3;
+    if (qt == 0) {
+      if (u == 0) {
+        wd = bf16_to_f32(R.s[g]) * 512.0f;
+        wmo = bf16_to_f32(R.m[g]);
+      }
+      wlo = opaque(R.q[g][u] & 0x0F0F0F0Fu);
+      whi = opaque((R.q[g][u] >> 4) & 0x0F0F0F0Fu);
+      wa = codes2_f32<false>(wlo);
+    } else if (qt == 1) {
+      we = codes2_f32<false>(whi);
+      wo[0] = pack_bf16x2(eq3(wa[0], wd, wmo), eq3(we[0], wd, wmo));
+      wo[1] = pack_bf16x2(eq3(wa[1], wd, wmo), eq3(we[1], wd, wmo));
+    } else if (qt == 2) {
+      wb = codes2_f32<true>(wlo);
+      wg = codes2_f32<true>(whi);
+      wo[2] = pack_bf16x2(eq3(wb[0], wd, wmo), eq3(wg[0], wd, wmo));
+    } else {
+      wo[3] = pack_bf16x2(eq3(wb[1], wd, wmo), eq3(wg[1], wd, wmo));
+      *reinterpret_cast<u32x4*>(ws_row(st, g) + 8 * u) = wo;
+    }
+  };
+
+  // One K step: MFMAs of step s from stage s&1 while step s+1 (held in Rs) is
+  // written to the other stage and step s+3 is loaded into Rs.
+  bf16x8 A0[TI], B0[TJ], A1[TI], B1[TJ];
+  auto step = [&](int s, WideRegs& Rs) {
+    const int cur = s & 1, nxt = cur ^ 1;
+    uint16_t* xsn = xs_row(nxt);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      mma1(A0, B0, i);
+      if (i < 8) read1(cur, 1, A1, B1, i);
+      else *reinterpret_cast<u32x4*>(xsn + 32 * (i - 8) * kLdsStride) = Rs.x[i - 8];
+      wpiece(Rs, nxt, 0, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      mma1(A1, B1, i);
+      if (i < 8) read1(cur, 2, A0, B0, i);
+      wpiece(Rs, nxt, 1, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      mma1(A0, B0, i);
+      if (i < 8) read1(cur, 3, A1, B1, i);
+      if (i < 14) load1(Rs, s + 3, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      mma1(A1, B1, i);
+      if (i < 8) read1(nxt, 0, A0, B0, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  WideRegs R0, R1;
+#pragma unroll
+  for (int i = 0; i < 14; ++i) load1(R0, 0, i);
+#pragma unroll
+  for (int i = 0; i < 14; ++i) load1(R1, 1, i);
+  {
+    uint16_t* xs = xs_row(0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(xs + 32 * i * kLdsStride) = R0.x[i];
+#pragma unroll
+    for (int g = 0; g < 2; ++g) {
+      const float d512 = bf16_to_f32(R0.s[g]) * 512.0f, m = bf16_to_f32(R0.m[g]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) *reinterpret_cast<u32x4*>(ws_row(0, g) + 8 * u) = dequant8_bf16(R0.q[g][u], d512, m);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 14; ++i) load1(R0, 2, i);
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 8; ++i) read1(0, 0, A0, B0, i);
+  int s = 0;
+  for (; s + 1 < nsteps; s += 2) {  // two steps per trip, so the register sets stay static
+    step(s, R1);
+    step(s + 1, R0);
+  }
+  if (s < nsteps) step(s, R1);
+
+  // Accumulator element e of lane l: column l%32, row 8(e/4) + 4(l/32) + e%4.
+  const bool full = m0 + 256 <= M && n0 + 256 <= N;
+#pragma unroll
+  for (int a = 0; a < TI; ++a)
+#pragma unroll
+    for (int b = 0; b < TJ; ++b) {
+      const int col = n0 + 128 * wn + 32 * b + (lane & 31);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = m0 + 128 * wm + 32 * a + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        if (full || (row < M && col < N)) {
+          if (y_bf16)
+            static_cast<uint16_t*>(Y)[(size_t)row * ldy + col] = f32_to_bf16_bits(acc[a][b][e]);
+          else
+            static_cast<float*>(Y)[(size_t)row * ldy + col] = acc[a][b][e];
+        }
+      }
+    }
+}
+
+// ---- general tiles, two waves per SIMD --------------------------------------
+// Workgroup tile BM (tokens) x BN (outputs) for the shapes the 256 x 256 tile
+// does not fill.  WAVES_M x WAVES_N waves; each owns a (BM/WAVES_M) x
+// (BN/WAVES_N) sub-tile.  LDS holds two stages of the X tile and of the
+// dequantized W tile; a K step runs the MFMAs of step k from one stage while
+// the same waves dequantize step k+1 into the other, with the raw global data
+// of step k+1 loaded into registers two steps earlier.  One workgroup barrier
+// per K step.
 template <int BM, int BN, int WAVES_M, int WAVES_N>
 struct GemmCfg {
   static constexpr int kThreads = 64 * WAVES_M * WAVES_N;
@@ -445,17 +701,10 @@ struct GemmRegs {
   uint32_t s[WG], m[WG];
 };
 
-// Scheduling hint: interleave the MFMAs of a K step with the VALU and LDS
-// work of the next step's dequantization (masks: 0x008 MFMA, 0x002 VALU,
-// 0x100 LDS read, 0x200 LDS write).
-#ifndef Q4NX_GEMM_VALU_PER_MFMA
-#define Q4NX_GEMM_VALU_PER_MFMA 3
-#endif
-
 template <int BM, int BN, int WAVES_M, int WAVES_N>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ blob, void* __restrict__ Y, int M, int N, int K,
-    int KB, int NS, int tiles_n, int y_bf16) {
+    int ldy, int KB, int NS, int tiles_n, int y_bf16) {
   using C = GemmCfg<BM, BN, WAVES_M, WAVES_N>;
   using Regs = GemmRegs<C::kXChunks, C::kWGroups>;
   extern __shared__ __attribute__((aligned(16))) uint16_t gl[];
@@ -518,19 +767,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
       const int gi = tid + i * C::kThreads;
       if (C::kStepGroups % C::kThreads != 0 && gi >= C::kStepGroups) break;  // wave-uniform
       const bool ok = ((n0 + (gi >> 1)) >> 5) < NS && k0 + kGroup * (gi & 1) < K;
-      float f[32];
-      codes_to_f32_scaled(ok ? R.q[i] : (u32x4){0u, 0u, 0u, 0u}, f);
+      const u32x4 q = ok ? R.q[i] : (u32x4){0u, 0u, 0u, 0u};
       const float d512 = ok ? bf16_to_f32(R.s[i]) * 512.0f : 0.0f, m = ok ? bf16_to_f32(R.m[i]) : 0.0f;
       u32x4* wd = reinterpret_cast<u32x4*>(ws + (gi >> 1) * kLdsStride + kGroup * (gi & 1));
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        u32x4 o;
-        o[0] = pack_bf16x2(eq3(f[8 * v + 0], d512, m), eq3(f[8 * v + 1], d512, m));
-        o[1] = pack_bf16x2(eq3(f[8 * v + 2], d512, m), eq3(f[8 * v + 3], d512, m));
-        o[2] = pack_bf16x2(eq3(f[8 * v + 4], d512, m), eq3(f[8 * v + 5], d512, m));
-        o[3] = pack_bf16x2(eq3(f[8 * v + 6], d512, m), eq3(f[8 * v + 7], d512, m));
-        wd[v] = o;
-      }
+      for (int v = 0; v < 4; ++v) wd[v] = dequant8_bf16(q[v], d512, m);
     }
   };
 
@@ -556,19 +797,6 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
     }
   };
 
-  // One steady-state iteration: MFMAs of step ks (stage ks&1) interleaved
-  // with the dequantization of step ks+1 (held in Rn) into the other stage;
-  // then the loads of step ks+3 into Rn (two steps of register prefetch).
-  auto interleave = [&]() {
-#if Q4NX_GEMM_VALU_PER_MFMA > 0
-#pragma unroll
-    for (int i = 0; i < C::kTI * C::kTJ * (kBK / 16); ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, Q4NX_GEMM_VALU_PER_MFMA, 0);
-    }
-#endif
-  };
-
   const int nsteps = (K + kBK - 1) / kBK;
   Regs R0, R1;
   load_step(R0, 0);
@@ -581,7 +809,6 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
   for (; ks + 2 < nsteps; ks += 2) {
     mma_step(0);
     store_step(R0, 1, (ks + 1) * kBK);
-    interleave();
     // Unconditional (addresses are clamped; data past the last step is never
     // stored), so the wait-count bookkeeping sees the same load order on every
     // trip and waits only for the register set being consumed.
@@ -589,7 +816,6 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
     __syncthreads();
     mma_step(1);
     store_step(R1, 0, (ks + 2) * kBK);
-    interleave();
     load_step(R1, (ks + 4) * kBK);
     __syncthreads();
   }
@@ -614,20 +840,90 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
         const int row = m0 + C::kWTM * wm + 32 * a + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         if (row < M) {
           if (y_bf16)
-            static_cast<uint16_t*>(Y)[(size_t)row * N + col] = f32_to_bf16_bits(acc[a][b][e]);
+            static_cast<uint16_t*>(Y)[(size_t)row * ldy + col] = f32_to_bf16_bits(acc[a][b][e]);
           else
-            static_cast<float*>(Y)[(size_t)row * N + col] = acc[a][b][e];
+            static_cast<float*>(Y)[(size_t)row * ldy + col] = acc[a][b][e];
         }
       }
     }
 }
 
+// ---- launch planning ----------------------------------------------------------
+// Tile shapes: 0 = 256 x 256 (gemm256_kernel; the general kernel past
+// kWideMaxK), 1 = 256 x 128, 2 = 128 x 128, 3 = 128 x 64.
+struct GemmTile {
+  int bm, bn;
+  float round_cost;  // time of one full round (a tile on every CU), relative to shape 0
+};
+// Round costs measured on MI355X for the Gemma3 prefill projections (K = 5376).
+constexpr GemmTile kGemmTiles[4] = {{256, 256, 1.0f}, {256, 128, 0.68f}, {128, 128, 0.52f}, {128, 64, 0.38f}};
+
+// A rectangle of the output computed by one launch.
+struct GemmRegion {
+  int tile;
+  int64_t m0, n0, M, N;
+};
+
+static int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    cus[dev] = (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) ? n : 256;
+  }
+  return cus[dev];
+}
+
+// Chooses one launch, or two launches over a split of the rows or columns,
+// minimising the estimated time: sum over launches of (rounds of tiles on the
+// CUs) x (round cost of the tile shape), plus a small cost per extra launch.
+// A launch whose last round is only partly filled still pays a whole round,
+// so a shape with 336 256x256 tiles on 256 CUs is better done as one full
+// round of 256 x 256 tiles and the rest in smaller tiles.
+static int gemm_plan(int64_t M, int64_t N, int cus, GemmRegion (&plan)[2]) {
+  const auto rounds = [&](int t, int64_t m, int64_t n) {
+    return (double)ceil_div(ceil_div(m, kGemmTiles[t].bm) * ceil_div(n, kGemmTiles[t].bn), cus);
+  };
+  double best = 1e300;
+  int count = 0;
+  for (int a = 0; a < 4; ++a) {
+    const double c1 = rounds(a, M, N) * kGemmTiles[a].round_cost;
+    if (c1 < best) {
+      best = c1;
+      plan[0] = {a, 0, 0, M, N};
+      count = 1;
+    }
+    const int64_t tm = ceil_div(M, kGemmTiles[a].bm), tn = ceil_div(N, kGemmTiles[a].bn);
+    const int64_t full = (tm * tn) / cus;  // whole rounds of shape a
+    if (full < 1) continue;
+    for (int dir = 0; dir < 2; ++dir) {
+      // Largest leading block of rows (dir 0) or columns (dir 1) whose tiles
+      // fit in the whole rounds; the rest goes to a smaller shape.
+      const int64_t split = dir == 0 ? (full * cus / tn) * kGemmTiles[a].bm : (full * cus / tm) * kGemmTiles[a].bn;
+      if (split <= 0 || split >= (dir == 0 ? M : N)) continue;
+      const int64_t ma = dir == 0 ? split : M, na = dir == 0 ? N : split;
+      const int64_t mb = dir == 0 ? M - split : M, nb = dir == 0 ? N : N - split;
+      for (int b = a + 1; b < 4; ++b) {
+        const double c2 = rounds(a, ma, na) * kGemmTiles[a].round_cost +
+                          rounds(b, mb, nb) * kGemmTiles[b].round_cost + 0.02 + 0.001 * dir;
+        if (c2 < best) {
+          best = c2;
+          plan[0] = {a, 0, 0, ma, na};
+          plan[1] = {b, dir == 0 ? split : 0, dir == 0 ? 0 : split, mb, nb};
+          count = 2;
+        }
+      }
+    }
+  }
+  return count;
+}
+
 template <int BM, int BN, int WAVES_M, int WAVES_N>
 static q4nx_status launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* X, const void* blob, void* Y,
-                               int y_bf16, hipStream_t stream) {
+                               int64_t ldy, int y_bf16, hipStream_t stream) {
   using Cfg = GemmCfg<BM, BN, WAVES_M, WAVES_N>;
   const int64_t tiles_n = ceil_div(N, BN), tiles_m = ceil_div(M, BM);
-  if (tiles_n * tiles_m > 0x7FFFFFFF) return fail(Q4NX_ERR_SHAPE, "q4nx_gemm: problem too large for one launch");
   const size_t lds = sizeof(uint16_t) * Cfg::kLdsElems;
   auto kern = gemm_kernel<BM, BN, WAVES_M, WAVES_N>;
   static bool attr_set = false;  // LDS above 64 KiB must be requested once per kernel
@@ -638,9 +934,45 @@ static q4nx_status launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* 
     attr_set = true;
   }
   hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_n * tiles_m)), dim3(Cfg::kThreads), lds, stream, X,
-                     static_cast<const uint8_t*>(blob), Y, (int)M, (int)N, (int)K, (int)ceil_div(K, kBlockCols),
-                     (int)ceil_div(N, kBlockRows), (int)tiles_n, y_bf16);
+                     static_cast<const uint8_t*>(blob), Y, (int)M, (int)N, (int)K, (int)ldy,
+                     (int)ceil_div(K, kBlockCols), (int)ceil_div(N, kBlockRows), (int)tiles_n, y_bf16);
   return Q4NX_OK;
+}
+
+template <bool KTAIL>
+static q4nx_status launch_gemm256(int64_t M, int64_t N, int64_t K, const uint16_t* X, const void* blob, void* Y,
+                                  int64_t ldy, int y_bf16, hipStream_t stream) {
+  auto kern = gemm256_kernel<KTAIL>;
+  static bool attr_set = false;
+  if (!attr_set) {
+    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                            kWideLdsBytes) != hipSuccess)
+      return fail(Q4NX_ERR_HIP, "q4nx_gemm: cannot reserve LDS");
+    attr_set = true;
+  }
+  const int64_t tiles_n = ceil_div(N, 256), tiles_m = ceil_div(M, 256);
+  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_n * tiles_m)), dim3(kWideThreads), kWideLdsBytes, stream, X,
+                     static_cast<const uint8_t*>(blob), Y, (int)M, (int)N, (int)K, (int)ldy,
+                     (int)ceil_div(K, kBlockCols), (int)ceil_div(N, kBlockRows), (int)tiles_n, y_bf16);
+  return Q4NX_OK;
+}
+
+// One region of the output: X rows m0.., W strips n0/32.. and Y at (m0, n0)
+// with row stride N, so each launch sees an ordinary smaller problem.
+static q4nx_status launch_region(const GemmRegion& r, int64_t N, int64_t K, const uint16_t* X, const void* blob,
+                                 void* Y, int y_bf16, hipStream_t stream) {
+  const uint16_t* Xr = X + r.m0 * K;
+  const void* Br = static_cast<const uint8_t*>(blob) + (r.n0 / kBlockRows) * ceil_div(K, kBlockCols) * kBlockBytes;
+  void* Yr = static_cast<uint8_t*>(Y) + (r.m0 * N + r.n0) * (y_bf16 ? 2 : 4);
+  switch (r.tile) {
+    case 0:
+      if (K >= kWideMaxK) return launch_gemm<256, 256, 2, 4>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
+      if (K % kBK != 0) return launch_gemm256<true>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
+      return launch_gemm256<false>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
+    case 1: return launch_gemm<256, 128, 4, 2>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
+    case 2: return launch_gemm<128, 128, 2, 4>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
+    default: return launch_gemm<128, 64, 2, 2>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
+  }
 }
 
 static q4nx_status check_launch(const char* fn) {
@@ -777,18 +1109,11 @@ q4nx_status q4nx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, cons
   if (!aligned(d_X, 16) || !aligned(d_blob, 16) || !aligned(d_Y, 16))
     return fail(Q4NX_ERR_ALIGNMENT, "q4nx_gemm: X, blob and Y need 16-byte alignment");
   if (M * N > (int64_t(1) << 40)) return fail(Q4NX_ERR_SHAPE, "q4nx_gemm: problem too large for one launch");
-  // Largest tile that still gives about one workgroup per CU.
   const int yb = (y_dtype == Q4NX_BF16);
-  const auto tiles = [&](int bm, int bn) { return ceil_div(M, bm) * ceil_div(N, bn); };
-  q4nx_status st;
-  if (tiles(256, 256) >= 240)
-    st = launch_gemm<256, 256, 2, 4>(M, N, K, d_X, d_blob, d_Y, yb, stream);
-  else if (tiles(256, 128) >= 240)
-    st = launch_gemm<256, 128, 4, 2>(M, N, K, d_X, d_blob, d_Y, yb, stream);
-  else if (tiles(128, 128) >= 200)
-    st = launch_gemm<128, 128, 2, 4>(M, N, K, d_X, d_blob, d_Y, yb, stream);
-  else
-    st = launch_gemm<128, 64, 2, 2>(M, N, K, d_X, d_blob, d_Y, yb, stream);
+  GemmRegion plan[2];
+  const int count = gemm_plan(M, N, device_cus(), plan);
+  q4nx_status st = Q4NX_OK;
+  for (int i = 0; i < count && st == Q4NX_OK; ++i) st = launch_region(plan[i], N, K, d_X, d_blob, d_Y, yb, stream);
   if (st != Q4NX_OK) return st;
   return check_launch("q4nx_gemm");
 }

@@ -266,3 +266,28 @@ def test_gemm_full_size_sampled_rows(q4, model, p):
     ok, worst, tight = _gemm_case(q4, M, N, K, seed=0, rows=rows, layer=0, proj=p)
     assert ok, (name, worst)
     assert tight, name
+
+
+# Shapes that take each launch plan of q4nx_gemm on a 256-CU device, with
+# ragged M and N and a K that is not a multiple of the 64-column step:
+#   3996 x 4080 x 5344  one launch of 256 x 256 tiles (the K-tail variant)
+#   4000 x 5344 x 2080  rows 0..3071 in 256 x 256 tiles, the rest in 256 x 128
+#   4096 x 21472 x 96   columns 0..20479 in 256 x 256 tiles, the rest in 128 x 128
+#   1024 x 16384 x 128  one launch of 256 x 256 tiles, K a multiple of 64
+PLAN_SHAPES = [(3996, 4080, 5344), (4000, 5344, 2080), (4096, 21472, 96), (1024, 16384, 128)]
+
+
+@pytest.mark.parametrize("M,N,K", PLAN_SHAPES)
+@pytest.mark.parametrize("bf16_out", [False, True])
+def test_gemm_launch_plans_sampled_rows(q4, M, N, K, bf16_out):
+    """The oracle checks the first and last 32 rows, the 32 rows on each side
+    of a row split at 3072, and 32 random rows, all N outputs each."""
+    rng = np.random.default_rng(2)
+    rows = np.concatenate([np.arange(32), M - 32 + np.arange(32), rng.integers(0, M, 32)])
+    if M > 3072 + 32:
+        rows = np.concatenate([rows, 3072 - 32 + np.arange(64)])
+    rows = np.unique(rows)
+    _say("gemm plan", M, N, K, "bf16" if bf16_out else "f32")
+    ok, worst, tight = _gemm_case(q4, M, N, K, seed=M + N, rows=rows, bf16_out=bf16_out)
+    assert ok, worst
+    assert tight
