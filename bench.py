@@ -50,6 +50,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=1, help="layers of the oracle CPU sample")
     ap.add_argument("--decode-graph", type=int, default=1, help="replay the decode step as a HIP graph")
+    ap.add_argument("--pmc-pass", action="store_true",
+                    help="run one eager decode step, one prefill step and a 1 GiB device copy (for rocprofv3 "
+                         "counter passes), then exit")
+    ap.add_argument("--pmc-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "MFMA_DIR"),
+                    help="summarise three rocprofv3 --pmc output folders of a --pmc-pass run as markdown")
     return ap.parse_args()
 
 
@@ -160,8 +165,132 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
     return out
 
 
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2602_06063_amd", "csrc", "q4nx_kernels.hip")
+PROFILES = os.path.join(ROOT, "profiles")
+CALIB_BYTES = 1 << 30  # the calibration copy reads and writes this many bytes
+
+
+def kernel_source_sha256():
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def traffic_file(config):
+    return os.path.join(PROFILES, f"hbm-traffic_config{config}.md")
+
+
+def kernel_family(name):
+    if "gemm256_kernel" in name or "gemm_kernel" in name:
+        return "gemm"
+    if "gemv_kernel" in name:
+        return "gemv"
+    return None
+
+
+def read_pmc(folder):
+    """Per-dispatch counter values of a rocprofv3 --pmc csv folder:
+    {dispatch_id: (kernel_name, {counter: value})}."""
+    import csv
+    import glob
+    out = {}
+    for path in glob.glob(os.path.join(folder, "**", "*counter_collection.csv"), recursive=True):
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                d = int(r["Dispatch_Id"])
+                name, ctr = out.setdefault(d, (r["Kernel_Name"], {}))
+                ctr[r["Counter_Name"]] = ctr.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+    return out
+
+
+def pmc_summary(config, fetch_dir, write_dir, mfma_dir):
+    """Markdown summary of the counter passes, with a JSON block that bench.py
+    reads back (only while the kernel source is unchanged).  FETCH_SIZE and
+    WRITE_SIZE are KiB per dispatch; each is scaled by bytes / counter of the
+    calibration copy (the last dispatch of the pass)."""
+    fetch, write, mfma = read_pmc(fetch_dir), read_pmc(write_dir), read_pmc(mfma_dir)
+
+    def calib(pass_, counter):
+        # Copy dispatches after the last kernel of the path: the calibration copy.
+        last = max(d for d, (n, _) in pass_.items() if kernel_family(n))
+        return sum(c[counter] for d, (n, c) in pass_.items() if d > last and "copy" in n.lower())
+    calib_f, calib_w = calib(fetch, "FETCH_SIZE"), calib(write, "WRITE_SIZE")
+    cf = CALIB_BYTES / (calib_f * 1024.0)
+    cw = CALIB_BYTES / (calib_w * 1024.0)
+    fam = {}
+    for d, (name, c) in fetch.items():
+        k = kernel_family(name)
+        if k:
+            fam.setdefault(k, {"dispatches": 0, "fetch_kib": 0.0, "write_kib": 0.0, "mfma_busy": 0.0, "gui_active": 0.0})
+            fam[k]["dispatches"] += 1
+            fam[k]["fetch_kib"] += c["FETCH_SIZE"]
+    for d, (name, c) in write.items():
+        k = kernel_family(name)
+        if k:
+            fam[k]["write_kib"] += c["WRITE_SIZE"]
+    for d, (name, c) in mfma.items():
+        k = kernel_family(name)
+        if k:
+            fam[k]["mfma_busy"] += c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+            fam[k]["gui_active"] += c.get("GRBM_GUI_ACTIVE", 0.0)
+    data = {"config": config, "kernel_source_sha256": kernel_source_sha256(),
+            "calibration": {"bytes": CALIB_BYTES, "fetch_kib": calib_f, "write_kib": calib_w,
+                            "fetch_scale": cf, "write_scale": cw},
+            "families": {}}
+    for k, v in fam.items():
+        fb, wb = v["fetch_kib"] * 1024.0 * cf, v["write_kib"] * 1024.0 * cw
+        e = {"dispatches_per_step": v["dispatches"], "fetch_bytes_per_step": fb, "write_bytes_per_step": wb,
+             "hbm_bytes_per_step": fb + wb}
+        if v["mfma_busy"] > 0:
+            # SQ_VALU_MFMA_BUSY_CYCLES is summed over all SIMDs; GRBM_GUI_ACTIVE over the 8 XCDs.
+            e["mfma_busy_fraction"] = v["mfma_busy"] / (1024.0 * v["gui_active"] / 8.0)
+        data["families"][k] = e
+    lines = [f"# HBM traffic and MFMA busy counters, bench configuration {config}", "",
+             "Three rocprofv3 counter passes over `python3 bench.py --config %d --pmc-pass` (one eager decode "
+             "step, one prefill step, then a 1 GiB device-to-device copy used as the calibration):" % config, "",
+             "```", "cd /tmp && export TMPDIR=/tmp; cd $GRAFT_REPO_ROOT",
+             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py --config %d --pmc-pass" % config,
+             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py --config %d --pmc-pass" % config,
+             "rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE --output-format csv -d gpurun_out/pmc_mfma -o run -- python3 bench.py --config %d --pmc-pass" % config,
+             "python3 bench.py --config %d --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write gpurun_out/pmc_mfma" % config,
+             "```", "",
+             "Calibration copy: FETCH_SIZE %.0f KiB and WRITE_SIZE %.0f KiB for %d bytes each way, so counter bytes are "
+             "scaled by %.4f (fetch) and %.4f (write)." % (data["calibration"]["fetch_kib"], data["calibration"]["write_kib"],
+                                                        CALIB_BYTES, cf, cw), "",
+             "| kernels | dispatches per step | HBM read (GB/step) | HBM write (GB/step) | MFMA busy |",
+             "|---|---:|---:|---:|---:|"]
+    for k, e in data["families"].items():
+        mb = "%.1f%%" % (100 * e["mfma_busy_fraction"]) if "mfma_busy_fraction" in e else "-"
+        lines.append(f"| {k} | {e['dispatches_per_step']} | {e['fetch_bytes_per_step'] / 1e9:.3f} | "
+                     f"{e['write_bytes_per_step'] / 1e9:.3f} | {mb} |")
+    lines += ["", "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES (summed over the 1024 SIMDs) / (1024 x GRBM_GUI_ACTIVE / 8), "
+              "i.e. the fraction of the kernels' busy cycles in which a SIMD's matrix core is working.", "",
+              "bench.py reads the block below while the kernel source still has this SHA-256:", "",
+              "```json", json.dumps(data, indent=1), "```", ""]
+    return "\n".join(lines)
+
+
+def stored_traffic(config):
+    """The counter summary for this configuration, if taken on the current kernels."""
+    path = traffic_file(config)
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    try:
+        block = text.split("```json", 1)[1].split("```", 1)[0]
+        data = json.loads(block)
+    except (IndexError, ValueError):
+        return None
+    if data.get("config") != config or data.get("kernel_source_sha256") != kernel_source_sha256():
+        return None
+    return data
+
+
 def main():
     args = parse()
+    if args.pmc_summary:
+        print(pmc_summary(args.config, *args.pmc_summary))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: this build measures the single-GPU path "
@@ -228,6 +357,19 @@ def main():
     torch.cuda.synchronize()
     log(f"inputs resident: {sum(t.numel() for t in weights.values()) / 1e9:.2f} GB of packed weights")
 
+    if args.pmc_pass:
+        # Exactly one step of each kind, then the calibration copy as the last dispatch.
+        dec.run()
+        pre.run()
+        torch.cuda.synchronize()
+        src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("pmc pass done")
+        return
+
     # ---------------------------------------------------------------- timing
     for _ in range(args.warmup):
         dec.run()
@@ -286,6 +428,12 @@ def main():
     if do_decode and decode_fn is not dec.run:
         eager_dec_ms, _, _ = timed(dec.run, lambda: None, args.steps)
 
+    # Bytes the launches must move at least once (operands in, results out).
+    alg_dec = sum(N * K * WEIGHT_BYTES + 2 * K + 4 * N for _, N, K in model["proj"]) * L if do_decode else 0
+    if do_decode and cfg.get("lm_head"):
+        _, N, K = model["lm_head"]
+        alg_dec += N * K * WEIGHT_BYTES + 2 * K + 4 * N
+    alg_pre = sum(2 * M_pre * K + N * K * WEIGHT_BYTES + 4 * M_pre * N for _, N, K in model["proj"]) * L if do_prefill else 0
     dec_gbs = dec_bytes / (mean(dec_ms) * 1e-3) / 1e9 if do_decode else None
     pre_tflops = pre_flops / (mean(pre_ms) * 1e-3) / 1e12 if do_prefill else None
 
@@ -332,11 +480,24 @@ def main():
     if do_prefill:
         result["roofline"] = {"kernel": "q4nx_gemm launches (gemm256_kernel, gemm_kernel)", "bound": "mfma", "achieved": round(pre_tflops, 2),
                               "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                              "frac": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None}
+                              "frac": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
+                              "algorithmic_bytes": round(alg_pre)}
     if do_decode:
         r = {"kernel": "gemv_kernel", "bound": "hbm", "achieved": round(dec_gbs, 2), "peak": HBM_PEAK_GBS,
-             "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None}
+             "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+             "algorithmic_bytes": round(alg_dec)}
         result["roofline" if not do_prefill else "roofline_gemv"] = r
+
+    stored = stored_traffic(args.config)
+    for key, fam in (("roofline", "gemm" if do_prefill else "gemv"), ("roofline_gemv", "gemv")):
+        if key in result and stored and fam in stored["families"]:
+            e = stored["families"][fam]
+            result[key]["traffic"] = round(e["hbm_bytes_per_step"])
+            result[key]["traffic_note"] = ("HBM bytes per step (read + write) of these launches, from rocprofv3 "
+                                           "FETCH_SIZE/WRITE_SIZE scaled by a copy-kernel calibration: "
+                                           + os.path.relpath(traffic_file(args.config), ROOT))
+            if "mfma_busy_fraction" in e:
+                result[key]["mfma_busy_counter"] = round(e["mfma_busy_fraction"], 4)
 
     if not args.no_cpu_baseline:
         log("timing the CPU oracle sample")
