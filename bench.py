@@ -50,6 +50,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-layers", type=int, default=1, help="layers of the oracle CPU sample")
     ap.add_argument("--decode-graph", type=int, default=1, help="replay the decode step as a HIP graph")
+    ap.add_argument("--two-phase", type=int, default=1,
+                    help="also time the two-phase prefill (q4nx_dequant to bf16, then q4nx_gemm_bf16)")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="run one eager decode step, one prefill step and a 1 GiB device copy (for rocprofv3 "
                          "counter passes), then exit")
@@ -106,6 +108,17 @@ class Step:
         self.q4._need(X, 2 * M * K, "X")
         self.q4._need(Y, M * N * Y.element_size(), "Y")
         self.calls.append((self.q4.lib.q4nx_gemm, (M, N, K, X.data_ptr(), blob.data_ptr(), Y.data_ptr(), ydt, self.s)))
+
+    def dequant_bf16(self, blob, N, K, W):
+        self.q4._need(blob, self.q4.q4nx_packed_size(N, K), "blob")
+        self.q4._need(W, 2 * N * K, "W")
+        self.calls.append((self.q4.lib.q4nx_dequant, (blob.data_ptr(), N, K, W.data_ptr(), self.q4.Q4NX_BF16, self.s)))
+
+    def gemm_bf16(self, M, N, K, X, W, Y, ydt):
+        self.q4._need(W, 2 * N * K, "W")
+        self.q4._need(X, 2 * M * K, "X")
+        self.q4._need(Y, M * N * Y.element_size(), "Y")
+        self.calls.append((self.q4.lib.q4nx_gemm_bf16, (M, N, K, X.data_ptr(), W.data_ptr(), Y.data_ptr(), ydt, self.s)))
 
     def run(self):
         for fn, args in self.calls:
@@ -343,16 +356,20 @@ def main():
 
     # ---------------------------------------------------------------- prefill
     pre = Step(q4, stream.cuda_stream)
+    two = Step(q4, stream.cuda_stream)   # two-phase: dequant to bf16 W, then the plain bf16 GEMM
     pre_flops = 0.0
     if do_prefill:
         Xs = {}
         Ys = {}
         for p, (_, N, K) in enumerate(model["proj"]):
             Ys[p] = torch.empty((M_pre, N), dtype=torch.float32, device="cuda")
+        Wtmp = torch.empty(max(N * K for _, N, K in model["proj"]), dtype=torch.bfloat16, device="cuda")
         for l in range(L):
             for p, (_, N, K) in enumerate(model["proj"]):
                 Xs[(l, p)] = gen_activations_device((M_pre, K), seed=args.seed, layer=l, proj=p)
                 pre.gemm(M_pre, N, K, Xs[(l, p)], weights[(l, p)], Ys[p], F32)
+                two.dequant_bf16(weights[(l, p)], N, K, Wtmp)
+                two.gemm_bf16(M_pre, N, K, Xs[(l, p)], Wtmp, Ys[p], F32)
                 pre_flops += 2.0 * M_pre * N * K
     torch.cuda.synchronize()
     log(f"inputs resident: {sum(t.numel() for t in weights.values()) / 1e9:.2f} GB of packed weights")
@@ -427,6 +444,11 @@ def main():
     eager_dec_ms = None
     if do_decode and decode_fn is not dec.run:
         eager_dec_ms, _, _ = timed(dec.run, lambda: None, args.steps)
+    two_ms = None
+    if do_prefill and args.two_phase:
+        for _ in range(args.warmup):
+            two.run()
+        _, two_ms, _ = timed(lambda: None, two.run, args.steps)
 
     # Bytes the launches must move at least once (operands in, results out).
     alg_dec = sum(N * K * WEIGHT_BYTES + 2 * K + 4 * N for _, N, K in model["proj"]) * L if do_decode else 0
@@ -474,6 +496,13 @@ def main():
                              "TFLOP": round(pre_flops / 1e12, 4), "TFLOP_per_s": round(pre_tflops, 2),
                              "frac_mfma": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4),
                              "launches": len(pre.calls), "dtype": "bf16 MFMA, f32 accumulate"}
+        if two_ms:
+            t = mean(two_ms)
+            result["prefill"]["two_phase"] = {
+                "ms": round(t, 4), "ms_min": round(min(two_ms), 4),
+                "TFLOP_per_s": round(pre_flops / (t * 1e-3) / 1e12, 2),
+                "launches": len(two.calls),
+                "what": "per projection: q4nx_dequant to a bf16 W buffer, then q4nx_gemm_bf16 (same bits as q4nx_gemm)"}
         if do_decode:
             result["value_gemm"] = round(pre_tflops, 2)
     # Dominant kernel by time: the GEMM when the step has a prefill chunk.

@@ -171,6 +171,24 @@ q4nx_status q4nx_gemv_batched(const q4nx_gemv_desc* descs, int32_t count, q4nx_d
 q4nx_status q4nx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_blob,
                       void* d_Y, q4nx_dtype y_dtype, hipStream_t stream);
 
+/*
+ * Device.  Plain bf16 matrix product Y[m][n] = sum_k X[m][k] * W[n][k] with W
+ * given in bf16 -- the second phase of the paper's two-phase prefill, where
+ * the dequantization engine writes the bf16 weights that the MM then consumes
+ * (Sec. 3.1.1 and 3.1.2): q4nx_dequant(blob, Q4NX_BF16) followed by this call.
+ * The arithmetic is that of q4nx_gemm (bf16 x bf16 products on the matrix
+ * cores, float32 sums over K in increasing order), so with W from
+ * q4nx_dequant the result equals q4nx_gemm on the packed matrix bit for bit.
+ *   d_X : device, row-major [M][K] bf16, 16-byte aligned
+ *   d_W : device, row-major [N][K] bf16, 16-byte aligned (the caller owns it)
+ *   d_Y : device, row-major [M][N] of y_dtype, 16-byte aligned; fully
+ *         overwritten, nothing outside [M][N] is written
+ * K must be a multiple of 32, as for q4nx_gemm.
+ * Errors: Q4NX_ERR_INVALID_ARG, Q4NX_ERR_SHAPE, Q4NX_ERR_ALIGNMENT, Q4NX_ERR_HIP.
+ */
+q4nx_status q4nx_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const uint16_t* d_W,
+                           void* d_Y, q4nx_dtype y_dtype, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* q4nx_status_str(q4nx_status status);
 

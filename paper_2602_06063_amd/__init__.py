@@ -30,7 +30,7 @@ Q4NX_BF16 = 1
 Q4NX_MAX_BATCH = 8
 
 EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_dequant", "q4nx_gemv",
-            "q4nx_gemv_batched", "q4nx_gemm", "q4nx_status_str", "q4nx_last_error"]
+            "q4nx_gemv_batched", "q4nx_gemm", "q4nx_gemm_bf16", "q4nx_status_str", "q4nx_last_error"]
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2602_06063_amd.build`")
@@ -67,6 +67,8 @@ lib.q4nx_gemv_batched.argtypes = [ctypes.POINTER(q4nx_gemv_desc), _i32, ctypes.c
 lib.q4nx_gemv_batched.restype = ctypes.c_int
 lib.q4nx_gemm.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp]
 lib.q4nx_gemm.restype = ctypes.c_int
+lib.q4nx_gemm_bf16.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp]
+lib.q4nx_gemm_bf16.restype = ctypes.c_int
 lib.q4nx_status_str.argtypes = [ctypes.c_int]
 lib.q4nx_status_str.restype = ctypes.c_char_p
 lib.q4nx_last_error.argtypes = []
@@ -190,3 +192,13 @@ def q4nx_gemm(M: int, N: int, K: int, X, blob, Y, stream=None):
     _need(Y, M * N * Y.element_size(), "Y")
     _check(lib.q4nx_gemm(M, N, K, _dptr(X), _dptr(blob), _dptr(Y), _dtype_code(Y), _stream(stream)),
            "q4nx_gemm")
+
+
+def q4nx_gemm_bf16(M: int, N: int, K: int, X, W, Y, stream=None):
+    """Y[M][N] <- X[M][K] W^T with W already bf16 [N][K] (the second phase of
+    the two-phase prefill: W from q4nx_dequant with a bf16 output)."""
+    _need(W, 2 * N * K, "W")
+    _need(X, 2 * M * K, "X")
+    _need(Y, M * N * Y.element_size(), "Y")
+    _check(lib.q4nx_gemm_bf16(M, N, K, _dptr(X), _dptr(W), _dptr(Y), _dtype_code(Y), _stream(stream)),
+           "q4nx_gemm_bf16")

@@ -458,15 +458,26 @@ constexpr int kWideThreads = 256;
 constexpr int kWideLdsBytes = 2 * 2 * 256 * kLdsStride * 2;  // two stages of X and W
 constexpr int64_t kWideMaxK = int64_t(1) << 22;               // 256 rows x K x 2 B < 2^31
 
+// Raw operands of one K step held by one thread.  X (and bf16 W): rows
+// tid/8 + 32i, columns 8(tid%8)..+7 of the step.  Packed W: codes, scale and
+// offset of group (row tid/2 + 128g, half tid%2 of the step).
+template <bool WQ4>
 struct WideRegs {
-  u32x4 x[8];      // X: rows tid/8 + 32i, columns 8(tid%8)..+7 of the step
-  u32x4 q[2];      // W: codes of group (row tid/2 + 128g, half tid%2 of the step)
+  u32x4 x[8];
+  u32x4 q[2];
   uint32_t s[2], m[2];
 };
+template <>
+struct WideRegs<false> {
+  u32x4 x[8];
+  u32x4 w[8];
+};
 
-template <bool KTAIL>
+// WQ4: W is a packed Q4NX matrix (dequantized on the fly); otherwise W is
+// bf16 [N][K] and its tile is staged exactly like the X tile.
+template <bool KTAIL, bool WQ4>
 __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* __restrict__ X,
-                                                               const uint8_t* __restrict__ blob,
+                                                               const uint8_t* __restrict__ wsrc,
                                                                void* __restrict__ Y, int M, int N, int K, int ldy,
                                                                int KB, int NS, int tiles_n, int y_bf16) {
   constexpr int TI = 4, TJ = 4;
@@ -484,22 +495,31 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
   const int rows_x = min(256, M - m0);
   const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(X + (size_t)m0 * K), (short)0, rows_x * K * 2, 0x00020000);
-  const int s0 = n0 >> 5, nst = min(8, NS - s0);
-  const __amdgpu_buffer_rsrc_t rsw = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint8_t*>(blob + (size_t)s0 * KB * kBlockBytes), (short)0, nst * KB * kBlockBytes, 0x00020000);
+  const int s0 = n0 >> 5, nst = min(8, NS - s0), rows_w = min(256, N - n0);
+  const __amdgpu_buffer_rsrc_t rsw =
+      WQ4 ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wsrc + (size_t)s0 * KB * kBlockBytes), (short)0,
+                                              nst * KB * kBlockBytes, 0x00020000)
+          : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wsrc + (size_t)n0 * K * 2), (short)0,
+                                              rows_w * K * 2, 0x00020000);
   constexpr int kPastEnd = 0x7FFFFFF0;  // beyond every descriptor: loads return 0
+  constexpr int kLoads = WQ4 ? 14 : 16;  // global loads per thread and K step
 
   const int c8 = tid & 7, half = tid & 1;
   int vx[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) vx[i] = (min((tid >> 3) + 32 * i, rows_x - 1) * K + 8 * c8) * 2;
-  int vq[2], vs[2];
+  int vq[2], vs[2], vw[8];
+  if constexpr (WQ4) {
 #pragma unroll
-  for (int g = 0; g < 2; ++g) {
-    const int r = (tid >> 1) + 128 * g;
-    const int st = min(r >> 5, nst - 1), rr = r & 31;
-    vq[g] = st * KB * kBlockBytes + 128 * rr + 16 * half;
-    vs[g] = st * KB * kBlockBytes + kCodeBytes + 2 * (8 * rr + half);
+    for (int g = 0; g < 2; ++g) {
+      const int r = (tid >> 1) + 128 * g;
+      const int st = min(r >> 5, nst - 1), rr = r & 31;
+      vq[g] = st * KB * kBlockBytes + 128 * rr + 16 * half;
+      vs[g] = st * KB * kBlockBytes + kCodeBytes + 2 * (8 * rr + half);
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) vw[i] = (min((tid >> 3) + 32 * i, rows_w - 1) * K + 8 * c8) * 2;
   }
   const int nsteps = (K + kBK - 1) / kBK;
 
@@ -511,9 +531,9 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
 
-  // Global loads of step t (clamped to the last step) into R, one of the 14
-  // loads per call (i = 0..13), so that they can be spread over MFMA slots.
-  auto load1 = [&](WideRegs& R, int t, int i) {
+  // Global loads of step t (clamped to the last step) into R, one of the
+  // kLoads loads per call, so that they can be spread over MFMA slots.
+  auto load1 = [&](WideRegs<WQ4>& R, int t, int i) {
     const int k0 = min(t, nsteps - 1) * kBK;
     const int sq = (k0 >> 8) * kBlockBytes + 16 * ((k0 & 255) >> 5);
     const int ss = (k0 >> 8) * kBlockBytes + 2 * ((k0 & 255) >> 5);
@@ -525,6 +545,14 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
       else
         R.x[i] = __builtin_bit_cast(
             u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsx, okx ? vx[i] + 2 * k0 : kPastEnd, 0, 0));
+      return;
+    }
+    if constexpr (!WQ4) {
+      if (!KTAIL)
+        R.w[i - 8] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsw, vw[i - 8], 2 * k0, 0));
+      else
+        R.w[i - 8] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsw, okx ? vw[i - 8] + 2 * k0 : kPastEnd, 0, 0));
     } else if (i < 10) {
       const int g = i - 8;
       R.q[g] = __builtin_bit_cast(
@@ -560,7 +588,8 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
   float wd = 0.0f, wmo = 0.0f;
   f32x2 wa, we, wb, wg;
   u32x4 wo;
-  auto wpiece = [&](const WideRegs& R, int st, int g, int p) {
+  auto wpiece = [&](const WideRegs<WQ4>& R, int st, int g, int p) {
+    if constexpr (WQ4) {
     const int u = p >> 2, qt = p & 3;
     if (qt == 0) {
       if (u == 0) {
@@ -582,12 +611,18 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
       wo[3] = pack_bf16x2(eq3(wb[1], wd, wmo), eq3(wg[1], wd, wmo));
       *reinterpret_cast<u32x4*>(ws_row(st, g) + 8 * u) = wo;
     }
+    }
+  };
+  // bf16 W: chunk i of the thread's W rows, staged like X.
+  auto wchunk = [&](const WideRegs<WQ4>& R, int st, int i) {
+    if constexpr (!WQ4)
+      *reinterpret_cast<u32x4*>(xs_row(st) + 2 * 256 * kLdsStride + 32 * i * kLdsStride) = R.w[i];
   };
 
   // One K step: MFMAs of step s from stage s&1 while step s+1 (held in Rs) is
   // written to the other stage and step s+3 is loaded into Rs.
   bf16x8 A0[TI], B0[TJ], A1[TI], B1[TJ];
-  auto step = [&](int s, WideRegs& Rs) {
+  auto step = [&](int s, WideRegs<WQ4>& Rs) {
     const int cur = s & 1, nxt = cur ^ 1;
     uint16_t* xsn = xs_row(nxt);
 #pragma unroll
@@ -602,6 +637,7 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
     for (int i = 0; i < 16; ++i) {
       mma1(A1, B1, i);
       if (i < 8) read1(cur, 2, A0, B0, i);
+      else if (!WQ4) wchunk(Rs, nxt, i - 8);
       wpiece(Rs, nxt, 1, i);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -609,7 +645,7 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
     for (int i = 0; i < 16; ++i) {
       mma1(A0, B0, i);
       if (i < 8) read1(cur, 3, A1, B1, i);
-      if (i < 14) load1(Rs, s + 3, i);
+      if (i < kLoads) load1(Rs, s + 3, i);
       __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
@@ -621,24 +657,30 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
     }
   };
 
-  WideRegs R0, R1;
+  WideRegs<WQ4> R0, R1;
 #pragma unroll
-  for (int i = 0; i < 14; ++i) load1(R0, 0, i);
+  for (int i = 0; i < kLoads; ++i) load1(R0, 0, i);
 #pragma unroll
-  for (int i = 0; i < 14; ++i) load1(R1, 1, i);
+  for (int i = 0; i < kLoads; ++i) load1(R1, 1, i);
   {
     uint16_t* xs = xs_row(0);
 #pragma unroll
     for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(xs + 32 * i * kLdsStride) = R0.x[i];
+    if constexpr (WQ4) {
 #pragma unroll
-    for (int g = 0; g < 2; ++g) {
-      const float d512 = bf16_to_f32(R0.s[g]) * 512.0f, m = bf16_to_f32(R0.m[g]);
+      for (int g = 0; g < 2; ++g) {
+        const float d512 = bf16_to_f32(R0.s[g]) * 512.0f, m = bf16_to_f32(R0.m[g]);
 #pragma unroll
-      for (int u = 0; u < 4; ++u) *reinterpret_cast<u32x4*>(ws_row(0, g) + 8 * u) = dequant8_bf16(R0.q[g][u], d512, m);
+        for (int u = 0; u < 4; ++u)
+          *reinterpret_cast<u32x4*>(ws_row(0, g) + 8 * u) = dequant8_bf16(R0.q[g][u], d512, m);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) wchunk(R0, 0, i);
     }
   }
 #pragma unroll
-  for (int i = 0; i < 14; ++i) load1(R0, 2, i);
+  for (int i = 0; i < kLoads; ++i) load1(R0, 2, i);
   __syncthreads();
 #pragma unroll
   for (int i = 0; i < 8; ++i) read1(0, 0, A0, B0, i);
@@ -687,26 +729,30 @@ struct GemmCfg {
   // whole waves, since BN * 2 is a multiple of 64 -- dequantize none).
   static constexpr int kStepGroups = BN * (kBK / kGroup);
   static constexpr int kWGroups = (kStepGroups + kThreads - 1) / kThreads;
+  static constexpr int kWChunks = BN * (kBK / 8) / kThreads;   // 16-byte chunks of a bf16 W tile
   static constexpr int kLdsElems = 2 * (BM + BN) * kLdsStride;
   static_assert(kXChunks >= 1 && kWGroups >= 1, "tile too small for the thread count");
   static_assert(kTI >= 1 && kTJ >= 1, "wave tile below 32 x 32");
 };
 
-// Raw global data of one K step held by one thread: its X chunks and the
-// codes / scale / offset of its weight groups.
-template <int XC, int WG>
+// Raw global data of one K step held by one thread: its X chunks and either
+// the codes / scale / offset of its weight groups or its bf16 W chunks.
+template <int XC, int WG, int WC>
 struct GemmRegs {
   u32x4 x[XC];
   u32x4 q[WG];
   uint32_t s[WG], m[WG];
+  u32x4 w[WC];
 };
 
-template <int BM, int BN, int WAVES_M, int WAVES_N>
+// WQ4: W is a packed Q4NX matrix (blob); otherwise W is bf16 [N][K].
+template <int BM, int BN, int WAVES_M, int WAVES_N, bool WQ4>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ blob, void* __restrict__ Y, int M, int N, int K,
     int ldy, int KB, int NS, int tiles_n, int y_bf16) {
   using C = GemmCfg<BM, BN, WAVES_M, WAVES_N>;
-  using Regs = GemmRegs<C::kXChunks, C::kWGroups>;
+  using Regs = GemmRegs<C::kXChunks, WQ4 ? C::kWGroups : 1, WQ4 ? 1 : C::kWChunks>;
+  const uint16_t* const Wb = reinterpret_cast<const uint16_t*>(blob);
   extern __shared__ __attribute__((aligned(16))) uint16_t gl[];
   uint16_t* xs0 = gl;                              // [2][BM][72]
   uint16_t* ws0 = gl + 2 * BM * kLdsStride;        // [2][BN][72]
@@ -737,6 +783,15 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
       const int r = ch >> 3, kk = k0 + 8 * (ch & 7);
       R.x[i] = *reinterpret_cast<const u32x4*>(X + (size_t)min(m0 + r, M - 1) * K + min(kk, K - 8));
     }
+    if constexpr (!WQ4) {
+#pragma unroll
+      for (int i = 0; i < C::kWChunks; ++i) {
+        const int ch = tid + i * C::kThreads;     // chunk: W row ch/8, columns 8(ch%8)..+7
+        const int r = ch >> 3, kk = k0 + 8 * (ch & 7);
+        R.w[i] = *reinterpret_cast<const u32x4*>(Wb + (size_t)min(n0 + r, N - 1) * K + min(kk, K - 8));
+      }
+      return;
+    }
 #pragma unroll
     for (int i = 0; i < C::kWGroups; ++i) {
       const int gi = tid + i * C::kThreads;       // group: row gi/2, half gi%2 of the K step
@@ -761,6 +816,15 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
       const int ch = tid + i * C::kThreads;
       const bool ok = m0 + (ch >> 3) < M && k0 + 8 * (ch & 7) < K;
       *reinterpret_cast<u32x4*>(xs + (ch >> 3) * kLdsStride + 8 * (ch & 7)) = ok ? R.x[i] : (u32x4){0u, 0u, 0u, 0u};
+    }
+    if constexpr (!WQ4) {
+#pragma unroll
+      for (int i = 0; i < C::kWChunks; ++i) {
+        const int ch = tid + i * C::kThreads;
+        const bool ok = n0 + (ch >> 3) < N && k0 + 8 * (ch & 7) < K;
+        *reinterpret_cast<u32x4*>(ws + (ch >> 3) * kLdsStride + 8 * (ch & 7)) = ok ? R.w[i] : (u32x4){0u, 0u, 0u, 0u};
+      }
+      return;
     }
 #pragma unroll
     for (int i = 0; i < C::kWGroups; ++i) {
@@ -919,13 +983,13 @@ static int gemm_plan(int64_t M, int64_t N, int cus, GemmRegion (&plan)[2]) {
   return count;
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N>
+template <int BM, int BN, int WAVES_M, int WAVES_N, bool WQ4>
 static q4nx_status launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* X, const void* blob, void* Y,
                                int64_t ldy, int y_bf16, hipStream_t stream) {
   using Cfg = GemmCfg<BM, BN, WAVES_M, WAVES_N>;
   const int64_t tiles_n = ceil_div(N, BN), tiles_m = ceil_div(M, BM);
   const size_t lds = sizeof(uint16_t) * Cfg::kLdsElems;
-  auto kern = gemm_kernel<BM, BN, WAVES_M, WAVES_N>;
+  auto kern = gemm_kernel<BM, BN, WAVES_M, WAVES_N, WQ4>;
   static bool attr_set = false;  // LDS above 64 KiB must be requested once per kernel
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -939,10 +1003,10 @@ static q4nx_status launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* 
   return Q4NX_OK;
 }
 
-template <bool KTAIL>
+template <bool KTAIL, bool WQ4>
 static q4nx_status launch_gemm256(int64_t M, int64_t N, int64_t K, const uint16_t* X, const void* blob, void* Y,
                                   int64_t ldy, int y_bf16, hipStream_t stream) {
-  auto kern = gemm256_kernel<KTAIL>;
+  auto kern = gemm256_kernel<KTAIL, WQ4>;
   static bool attr_set = false;
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -957,22 +1021,51 @@ static q4nx_status launch_gemm256(int64_t M, int64_t N, int64_t K, const uint16_
   return Q4NX_OK;
 }
 
-// One region of the output: X rows m0.., W strips n0/32.. and Y at (m0, n0)
-// with row stride N, so each launch sees an ordinary smaller problem.
-static q4nx_status launch_region(const GemmRegion& r, int64_t N, int64_t K, const uint16_t* X, const void* blob,
+// One region of the output: X rows m0.., W rows n0.. (strips n0/32.. of a
+// packed matrix) and Y at (m0, n0) with row stride N, so each launch sees an
+// ordinary smaller problem.
+template <bool WQ4>
+static q4nx_status launch_region(const GemmRegion& r, int64_t N, int64_t K, const uint16_t* X, const void* w,
                                  void* Y, int y_bf16, hipStream_t stream) {
   const uint16_t* Xr = X + r.m0 * K;
-  const void* Br = static_cast<const uint8_t*>(blob) + (r.n0 / kBlockRows) * ceil_div(K, kBlockCols) * kBlockBytes;
+  const void* Wr = WQ4 ? static_cast<const void*>(static_cast<const uint8_t*>(w) +
+                                                  (r.n0 / kBlockRows) * ceil_div(K, kBlockCols) * kBlockBytes)
+                       : static_cast<const void*>(static_cast<const uint16_t*>(w) + r.n0 * K);
   void* Yr = static_cast<uint8_t*>(Y) + (r.m0 * N + r.n0) * (y_bf16 ? 2 : 4);
   switch (r.tile) {
     case 0:
-      if (K >= kWideMaxK) return launch_gemm<256, 256, 2, 4>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
-      if (K % kBK != 0) return launch_gemm256<true>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
-      return launch_gemm256<false>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
-    case 1: return launch_gemm<256, 128, 4, 2>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
-    case 2: return launch_gemm<128, 128, 2, 4>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
-    default: return launch_gemm<128, 64, 2, 2>(r.M, r.N, K, Xr, Br, Yr, N, y_bf16, stream);
+      if (K >= kWideMaxK) return launch_gemm<256, 256, 2, 4, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+      if (K % kBK != 0) return launch_gemm256<true, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+      return launch_gemm256<false, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+    case 1: return launch_gemm<256, 128, 4, 2, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+    case 2: return launch_gemm<128, 128, 2, 4, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+    default: return launch_gemm<128, 64, 2, 2, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
   }
+}
+
+static q4nx_status check_launch(const char* fn);
+
+// Validation shared by q4nx_gemm and q4nx_gemm_bf16, then the planned launches.
+template <bool WQ4>
+static q4nx_status gemm_entry(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_W, void* d_Y,
+                              q4nx_dtype y_dtype, hipStream_t stream, const char* fn) {
+  clear_error();
+  if (q4nx_status st = check_shape(N, K, fn)) return st;
+  if (M <= 0 || M > Q4NX_MAX_DIM) return fail(Q4NX_ERR_SHAPE, std::string(fn) + ": M must lie in 1..2^30");
+  if (!d_X || !d_W || !d_Y) return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
+  if (y_dtype != Q4NX_F32 && y_dtype != Q4NX_BF16)
+    return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": unknown y_dtype");
+  if (!aligned(d_X, 16) || !aligned(d_W, 16) || !aligned(d_Y, 16))
+    return fail(Q4NX_ERR_ALIGNMENT, std::string(fn) + (WQ4 ? ": X, blob and Y need 16-byte alignment"
+                                                           : ": X, W and Y need 16-byte alignment"));
+  if (M * N > (int64_t(1) << 40)) return fail(Q4NX_ERR_SHAPE, std::string(fn) + ": problem too large for one launch");
+  GemmRegion plan[2];
+  const int count = gemm_plan(M, N, device_cus(), plan);
+  q4nx_status st = Q4NX_OK;
+  for (int i = 0; i < count && st == Q4NX_OK; ++i)
+    st = launch_region<WQ4>(plan[i], N, K, d_X, d_W, d_Y, y_dtype == Q4NX_BF16, stream);
+  if (st != Q4NX_OK) return st;
+  return check_launch(fn);
 }
 
 static q4nx_status check_launch(const char* fn) {
@@ -1100,22 +1193,12 @@ q4nx_status q4nx_gemv_batched(const q4nx_gemv_desc* descs, int32_t count, q4nx_d
 
 q4nx_status q4nx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_blob, void* d_Y,
                       q4nx_dtype y_dtype, hipStream_t stream) {
-  clear_error();
-  if (q4nx_status st = check_shape(N, K, "q4nx_gemm")) return st;
-  if (M <= 0 || M > Q4NX_MAX_DIM) return fail(Q4NX_ERR_SHAPE, "q4nx_gemm: M must lie in 1..2^30");
-  if (!d_X || !d_blob || !d_Y) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_gemm: NULL pointer");
-  if (y_dtype != Q4NX_F32 && y_dtype != Q4NX_BF16)
-    return fail(Q4NX_ERR_INVALID_ARG, "q4nx_gemm: unknown y_dtype");
-  if (!aligned(d_X, 16) || !aligned(d_blob, 16) || !aligned(d_Y, 16))
-    return fail(Q4NX_ERR_ALIGNMENT, "q4nx_gemm: X, blob and Y need 16-byte alignment");
-  if (M * N > (int64_t(1) << 40)) return fail(Q4NX_ERR_SHAPE, "q4nx_gemm: problem too large for one launch");
-  const int yb = (y_dtype == Q4NX_BF16);
-  GemmRegion plan[2];
-  const int count = gemm_plan(M, N, device_cus(), plan);
-  q4nx_status st = Q4NX_OK;
-  for (int i = 0; i < count && st == Q4NX_OK; ++i) st = launch_region(plan[i], N, K, d_X, d_blob, d_Y, yb, stream);
-  if (st != Q4NX_OK) return st;
-  return check_launch("q4nx_gemm");
+  return gemm_entry<true>(M, N, K, d_X, d_blob, d_Y, y_dtype, stream, "q4nx_gemm");
+}
+
+q4nx_status q4nx_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const uint16_t* d_W, void* d_Y,
+                           q4nx_dtype y_dtype, hipStream_t stream) {
+  return gemm_entry<false>(M, N, K, d_X, d_W, d_Y, y_dtype, stream, "q4nx_gemm_bf16");
 }
 
 }  // extern "C"

@@ -291,3 +291,49 @@ def test_gemm_launch_plans_sampled_rows(q4, M, N, K, bf16_out):
     ok, worst, tight = _gemm_case(q4, M, N, K, seed=M + N, rows=rows, bf16_out=bf16_out)
     assert ok, worst
     assert tight
+
+
+# ----------------------------------------------------------------- two-phase prefill
+# q4nx_dequant (bf16) then q4nx_gemm_bf16: the paper's dequantize-then-MM
+# structure.  Same bf16 weights and the same MFMA chain over K as the fused
+# q4nx_gemm, hence the same bits.
+TWO_PHASE_SHAPES = [(5, 33, 288), (130, 200, 1152), (300, 96, 5376), (4096, 2048, 256), (3996, 4080, 544),
+                    (4000, 5344, 224), (4096, 21472, 96)]
+
+
+@pytest.mark.parametrize("M,N,K", TWO_PHASE_SHAPES)
+@pytest.mark.parametrize("bf16_out", [False, True])
+def test_two_phase_prefill_equals_fused_bitwise(q4, M, N, K, bf16_out):
+    _say("two-phase", M, N, K, "bf16" if bf16_out else "f32")
+    codes, s, o = make(N, K, seed=M + K, mode="zp")
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    X = dev_bf16(gen_activations((M, K), seed=M + K))
+    ydt = torch.bfloat16 if bf16_out else torch.float32
+    W = torch.empty((N, K), dtype=torch.bfloat16, device="cuda")
+    Y1 = torch.full((M, N), float("nan"), dtype=ydt, device="cuda")
+    Y2 = torch.full((M, N), float("nan"), dtype=ydt, device="cuda")
+    q4.q4nx_gemm(M, N, K, X, blob, Y1)
+    q4.q4nx_dequant(blob, N, K, W)
+    q4.q4nx_gemm_bf16(M, N, K, X, W, Y2)
+    torch.cuda.synchronize()
+    it = torch.int16 if bf16_out else torch.int32
+    assert torch.equal(Y1.view(it), Y2.view(it))
+
+
+@pytest.mark.parametrize("M,N,K", [(7, 40, 96), (129, 257, 1184), (512, 640, 2048)])
+def test_gemm_bf16_arbitrary_weights_vs_float64(q4, M, N, K):
+    """Any bf16 W (not only dequantized ones): the float64 product of the bf16
+    values, with the GEMM tolerance and the tight diagnostic bound."""
+    _say("gemm_bf16", M, N, K)
+    rng = np.random.default_rng(M * N)
+    w32 = rng.standard_normal((N, K), dtype=np.float32) * np.float32(0.05)
+    wbits = oracle.f32_to_bf16(w32)
+    w16 = oracle.bf16_to_f32(wbits)
+    X = gen_activations((M, K), seed=N)
+    Y = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    q4.q4nx_gemm_bf16(M, N, K, dev_bf16(X), dev_bf16(wbits), Y)
+    Yh = host_f32(Y)
+    ref = oracle.gemm_f64(X, w16)
+    ok, worst = oracle.check_close(Yh, ref, oracle.abs_bound(X, w16))
+    assert ok, worst
+    assert (np.abs(Yh.astype(np.float64) - ref) <= 1e-5 * oracle.abs_bound(X, w16) + 1e-6).all()
