@@ -24,3 +24,4 @@ from .q4nx import (  # noqa: F401
     dequant_f32, dequant_bf16, dequant_blob_f32, gemv_f64, gemm_f64, abs_bound,
     tolerance, check_close,
 )
+from .quantize import quantize, clamp_weights, group_scale_offset  # noqa: F401,E402

@@ -129,3 +129,64 @@ def project_exact(blob, N: int, K: int, X_rows):
             xv.append(-mag if s else mag)
         Y.append([sum((xv[k] * Wf[n][k] for k in range(K)), Fraction(0)) for n in range(N)])
     return Y
+
+
+# ----------------------------------------------------------------------------
+# quantizer (the reading of oracle.quantize, in exact rational arithmetic)
+# ----------------------------------------------------------------------------
+def round_sig(v: Fraction, bits: int) -> Fraction:
+    """Round a nonzero rational of magnitude >= 2^-126 to `bits` significant
+    bits, ties to even (the normal range of binary32 and bf16)."""
+    neg = v < 0
+    a = -v if neg else v
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    while Fraction(2) ** (e + 1) <= a:
+        e += 1
+    quantum = Fraction(2) ** (e - (bits - 1))
+    n = a / quantum
+    fl = n.numerator // n.denominator
+    rem = n - fl
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and fl % 2 == 1):
+        fl += 1
+    r = fl * quantum
+    return -r if neg else r
+
+
+def bf16_bits_of(v: Fraction) -> int:
+    """bf16 bit pattern of RNE_bf16(v) with magnitudes below 2^-100 flushed
+    to a zero of the same sign (v a binary32 value)."""
+    if v == 0 or abs(v) < Fraction(2) ** -101:
+        return 0x8000 if v < 0 else 0
+    r = round_sig(v, 8)
+    if abs(r) < Fraction(2) ** -100:
+        return 0x8000 if r < 0 else 0
+    sign = 1 if r < 0 else 0
+    a = abs(r)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    man = int(a / Fraction(2) ** e * 128) - 128
+    return (sign << 15) | ((e + 127) << 7) | man
+
+
+def quantize_group_exact(ws):
+    """One group of float32 values (Python floats, already clamped) ->
+    (codes, scale bits, offset bits), by exact arithmetic."""
+    vals = [Fraction(w) for w in ws]
+    lo, hi = min(vals), max(vals)
+    diff = hi - lo
+    d32 = round_to_f32(round_to_f32(diff) / 15) if diff != 0 else Fraction(0)
+    s_bits = bf16_bits_of(d32)
+    m_bits = bf16_bits_of(lo)  # a zero minimum is +0
+    levels = [f32_from_bits(eq3_bits(q, s_bits, m_bits)) for q in range(16)]
+    codes = []
+    for v in vals:
+        best, bq = None, 0
+        for q in range(16):
+            dist = abs(levels[q] - v)
+            if best is None or dist < best:
+                best, bq = dist, q
+        codes.append(bq)
+    return codes, s_bits, m_bits
