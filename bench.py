@@ -52,6 +52,8 @@ def parse():
     ap.add_argument("--decode-graph", type=int, default=1, help="replay the decode step as a HIP graph")
     ap.add_argument("--two-phase", type=int, default=1,
                     help="also time the two-phase prefill (q4nx_dequant to bf16, then q4nx_gemm_bf16)")
+    ap.add_argument("--quantize", type=int, default=1,
+                    help="also time q4nx_quantize on the model's largest projection (float32 -> Q4NX)")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="run one eager decode step, one prefill step and a 1 GiB device copy (for rocprofv3 "
                          "counter passes), then exit")
@@ -456,6 +458,29 @@ def main():
         _, N, K = model["lm_head"]
         alg_dec += N * K * WEIGHT_BYTES + 2 * K + 4 * N
     alg_pre = sum(2 * M_pre * K + N * K * WEIGHT_BYTES + 4 * M_pre * N for _, N, K in model["proj"]) * L if do_prefill else 0
+    quant = None
+    if args.quantize:
+        # The offline conversion on the GPU: one float32 matrix of the largest
+        # projection shape (N(0, 0.02) values), timed like the steps.
+        _, Nq, Kq = max(model["proj"] + ([model["lm_head"]] if cfg.get("lm_head") else []), key=lambda p: p[1] * p[2])
+        gq = torch.Generator(device="cuda")
+        gq.manual_seed(args.seed)
+        Wq = torch.randn((Nq, Kq), generator=gq, device="cuda", dtype=torch.float32) * 0.02
+        Bq = torch.empty(q4.q4nx_packed_size(Nq, Kq), dtype=torch.uint8, device="cuda")
+        sq = Step(q4, stream.cuda_stream)
+        sq.calls.append((q4.lib.q4nx_quantize, (Wq.data_ptr(), Nq, Kq, Bq.data_ptr(), sq.s)))
+        for _ in range(args.warmup):
+            sq.run()
+        _, q_ms, _ = timed(lambda: None, sq.run, args.steps)
+        tq = mean(q_ms)
+        qbytes = Nq * Kq * (4 + WEIGHT_BYTES)
+        quant = {"shape": [Nq, Kq], "ms": round(tq, 4), "ms_min": round(min(q_ms), 4),
+                 "Gweights_per_s": round(Nq * Kq / (tq * 1e-3) / 1e9, 2),
+                 "GB_per_s": round(qbytes / (tq * 1e-3) / 1e9, 2),
+                 "frac_hbm": round(qbytes / (tq * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                 "bytes": "4 B read + 0.625 B written per weight"}
+        del Wq, Bq
+
     dec_gbs = dec_bytes / (mean(dec_ms) * 1e-3) / 1e9 if do_decode else None
     pre_tflops = pre_flops / (mean(pre_ms) * 1e-3) / 1e12 if do_prefill else None
 
@@ -517,6 +542,8 @@ def main():
              "algorithmic_bytes": round(alg_dec)}
         result["roofline" if not do_prefill else "roofline_gemv"] = r
 
+    if quant:
+        result["quantize"] = quant
     stored = stored_traffic(args.config)
     for key, fam in (("roofline", "gemm" if do_prefill else "gemv"), ("roofline_gemv", "gemv")):
         if key in result and stored and fam in stored["families"]:

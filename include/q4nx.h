@@ -117,6 +117,26 @@ q4nx_status q4nx_dequant(const void* d_blob, int64_t N, int64_t K,
                          void* d_W, q4nx_dtype w_dtype, hipStream_t stream);
 
 /*
+ * Device.  Quantizer into Q4NX: the offline conversion of float32 weights into
+ * the packed format that the paper performs before inference (Sec. 3.1.1:
+ * per-group scale and minimal-value offset, groups of 32 as in Q4_1), written
+ * straight into a blob.  Per group of 32 consecutive input columns:
+ *   w -> 0 if NaN, else clamped to [-2^100, 2^100];
+ *   lo, hi = min and max of the group (a zero minimum is +0);
+ *   d = RNE_bf16(RN_fp32(RN_fp32(hi - lo) / 15)), m = RNE_bf16(lo), each
+ *   flushed to a signed zero if its magnitude is below 2^-100;
+ *   q = the code 0..15 whose Eq. 3 value RN_fp32(d*q + m) is nearest to w
+ *   (differences taken in float64), the smaller code on a tie.
+ *   d_W    : device, row-major [N][K] float32, 16-byte aligned
+ *   d_blob : device, q4nx_packed_size(N, K) bytes, 16-byte aligned; fully
+ *            written, padding included (code 0, scale +0, offset +0)
+ * Every input value is accepted (the clamp above), so no device-side error
+ * exists.  Errors: Q4NX_ERR_INVALID_ARG, Q4NX_ERR_SHAPE, Q4NX_ERR_ALIGNMENT,
+ * Q4NX_ERR_HIP.
+ */
+q4nx_status q4nx_quantize(const float* d_W, int64_t N, int64_t K, void* d_blob, hipStream_t stream);
+
+/*
  * Device.  FusedDQP (Sec. 3.2.1, Eq. 14/15): y[n] = sum_k w[n][k] * x[k] with
  * w from Eq. 3, dequantized in registers and never written to memory; float32
  * accumulation.

@@ -29,11 +29,11 @@ Q4NX_F32 = 0
 Q4NX_BF16 = 1
 Q4NX_MAX_BATCH = 8
 
-EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_dequant", "q4nx_gemv",
+EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_quantize", "q4nx_dequant", "q4nx_gemv",
             "q4nx_gemv_batched", "q4nx_gemm", "q4nx_gemm_bf16", "q4nx_status_str", "q4nx_last_error"]
 
 if not os.path.exists(LIB_PATH):
-    raise ImportError(f"{LIB_PATH} is missing: build it with `python -m paper_2602_06063_amd.build`")
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2602_06063_amd/build.py`")
 
 # torch ships its own HIP runtime under the same soname (libamdhip64.so.7).
 # Loading torch first makes the dynamic loader satisfy libq4nx's dependency
@@ -59,6 +59,8 @@ lib.q4nx_pack.argtypes = [_vp, _vp, _vp, _i64, _i64, _vp, _sz]
 lib.q4nx_pack.restype = ctypes.c_int
 lib.q4nx_unpack.argtypes = [_vp, _sz, _i64, _i64, _vp, _vp, _vp]
 lib.q4nx_unpack.restype = ctypes.c_int
+lib.q4nx_quantize.argtypes = [_vp, _i64, _i64, _vp, _vp]
+lib.q4nx_quantize.restype = ctypes.c_int
 lib.q4nx_dequant.argtypes = [_vp, _i64, _i64, _vp, ctypes.c_int, _vp]
 lib.q4nx_dequant.restype = ctypes.c_int
 lib.q4nx_gemv.argtypes = [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _vp]
@@ -153,6 +155,13 @@ def _dtype_code(t) -> int:
     if t.dtype == torch.bfloat16:
         return Q4NX_BF16
     raise ValueError("outputs must be float32 or bfloat16")
+
+
+def q4nx_quantize(W, N: int, K: int, blob, stream=None):
+    """blob <- Q4NX quantization of the float32 weights W[N][K] (device)."""
+    _need(W, 4 * N * K, "W")
+    _need(blob, q4nx_packed_size(N, K), "blob")
+    _check(lib.q4nx_quantize(_dptr(W), N, K, _dptr(blob), _stream(stream)), "q4nx_quantize")
 
 
 def q4nx_dequant(blob, N: int, K: int, W, stream=None):

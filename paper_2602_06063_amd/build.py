@@ -1,6 +1,6 @@
 """Builds libq4nx.so in-tree with hipcc for gfx950.
 
-    python -m paper_2602_06063_amd.build
+    python paper_2602_06063_amd/build.py
 
 Every HIP source is compiled with packed-fp32 instructions disabled (the
 compiler otherwise forms v_pk_*_f32 from plain float code).

@@ -168,6 +168,99 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict_
 }
 
 // ---------------------------------------------------------------------------
+// q4nx_quantize: float32 weights -> packed blob (the offline conversion)
+// ---------------------------------------------------------------------------
+// Per group of 32 consecutive input columns (Q4_1-style, Sec. 3.1.1):
+//   w -> 0 if NaN, else clamped to [-2^100, 2^100] (keeps d and m in the
+//   format's value domain); lo, hi = min, max (a zero minimum is +0);
+//   d = RNE_bf16(RN(RN(hi - lo) / 15)), m = RNE_bf16(lo), magnitudes below
+//   2^-100 flushed to a zero of the same sign;
+//   q = the code whose Eq. 3 value is nearest to w (float64 differences),
+//   the smaller code on a tie.
+// The Eq. 3 levels L_q = fma(q, d, m) are non-decreasing in q, so the
+// nearest level is found with two binary searches instead of a scan: c = the
+// number of levels below w; the candidates are level c (the first >= w) and
+// the first code whose level equals level c-1.
+constexpr float kQuantClamp = 1.2676506002282294e30f;  // 2^100
+
+__device__ __forceinline__ uint32_t bf16_rne_flushed(float v) {
+  uint32_t b = pack_bf16x2(v, 0.0f) & 0xFFFFu;
+  if ((b & 0x7FFFu) < (27u << 7)) b &= 0x8000u;  // |v| < 2^-100 -> signed zero
+  return b;
+}
+
+// Number of codes q in 0..15 whose level fma(q, d, m) is below v.
+__device__ __forceinline__ int levels_below(float v, float d, float m) {
+  int c = 0;
+#pragma unroll
+  for (int s = 8; s >= 1; s >>= 1)
+    if (fmaf((float)(c + s - 1), d, m) < v) c += s;
+  if (c == 15 && fmaf(15.0f, d, m) < v) c = 16;
+  return c;
+}
+
+__global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__ W, int64_t N, int64_t K, int64_t KB,
+                                                       int64_t nblocks, uint8_t* __restrict__ blob) {
+  const int t = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = 8 * t + (lane >> 3), c = lane & 7;
+  for (int64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
+    const int64_t i = b / KB, j = b - i * KB;
+    const int64_t n = i * kBlockRows + r;
+    const int64_t k0 = j * kBlockCols + kGroup * c;
+    uint8_t* blk = blob + b * kBlockBytes;
+    u32x4 codes = (u32x4){0u, 0u, 0u, 0u};
+    uint32_t sb = 0, mb = 0;
+    if (n < N && k0 < K) {
+      float w[32];
+      const f32x4* src = reinterpret_cast<const f32x4*>(W + n * K + k0);
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        const f32x4 x = src[v];
+        w[4 * v + 0] = x[0];
+        w[4 * v + 1] = x[1];
+        w[4 * v + 2] = x[2];
+        w[4 * v + 3] = x[3];
+      }
+      float lo = kQuantClamp, hi = -kQuantClamp;
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        const float x = w[e] != w[e] ? 0.0f : fminf(fmaxf(w[e], -kQuantClamp), kQuantClamp);
+        w[e] = x;
+        lo = fminf(lo, x);
+        hi = fmaxf(hi, x);
+      }
+      lo = lo + 0.0f;  // a zero minimum is +0
+      sb = bf16_rne_flushed((hi - lo) / 15.0f);
+      mb = bf16_rne_flushed(lo);
+      const float d = bf16_to_f32(sb), m = bf16_to_f32(mb);
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        const int cnt = levels_below(w[e], d, m);
+        int q;
+        if (cnt == 0) {
+          q = 0;
+        } else {
+          const float l_lo = fmaf((float)(cnt - 1), d, m);
+          const int q_lo = levels_below(l_lo, d, m);  // first code with that level
+          if (cnt == 16) {
+            q = q_lo;
+          } else {
+            const float l_hi = fmaf((float)cnt, d, m);
+            const double dist_hi = (double)l_hi - (double)w[e];
+            const double dist_lo = (double)w[e] - (double)l_lo;
+            q = dist_hi < dist_lo ? cnt : q_lo;
+          }
+        }
+        codes[e >> 3] |= (uint32_t)q << (4 * (e & 7));
+      }
+    }
+    *reinterpret_cast<u32x4*>(blk + 1024 * t + 16 * lane) = codes;
+    *reinterpret_cast<uint16_t*>(blk + kCodeBytes + 2 * (64 * t + lane)) = (uint16_t)sb;
+    *reinterpret_cast<uint16_t*>(blk + kCodeBytes + kScaleBytes + 2 * (64 * t + lane)) = (uint16_t)mb;
+  }
+}
+
+// ---------------------------------------------------------------------------
 // q4nx_gemv / q4nx_gemv_batched: FusedDQP
 // ---------------------------------------------------------------------------
 // A workgroup owns a row group of R = 8*tq consecutive rows (tq = 4: a whole
@@ -1178,6 +1271,20 @@ q4nx_status q4nx_dequant(const void* d_blob, int64_t N, int64_t K, void* d_W, q4
   hipLaunchKernelGGL(dequant_kernel, dim3((unsigned)grid), dim3(256), 0, stream,
                      static_cast<const uint8_t*>(d_blob), N, K, KB, nblocks, d_W, (int)(w_dtype == Q4NX_BF16));
   return check_launch("q4nx_dequant");
+}
+
+q4nx_status q4nx_quantize(const float* d_W, int64_t N, int64_t K, void* d_blob, hipStream_t stream) {
+  clear_error();
+  if (q4nx_status st = check_shape(N, K, "q4nx_quantize")) return st;
+  if (!d_W || !d_blob) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_quantize: NULL pointer");
+  if (!aligned(d_W, 16) || !aligned(d_blob, 16))
+    return fail(Q4NX_ERR_ALIGNMENT, "q4nx_quantize: W and blob need 16-byte alignment");
+  const int64_t KB = ceil_div(K, kBlockCols);
+  const int64_t nblocks = ceil_div(N, kBlockRows) * KB;
+  const int64_t grid = std::min<int64_t>(nblocks, int64_t(1) << 20);
+  hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)grid), dim3(256), 0, stream, d_W, N, K, KB, nblocks,
+                     static_cast<uint8_t*>(d_blob));
+  return check_launch("q4nx_quantize");
 }
 
 q4nx_status q4nx_gemv(const void* d_blob, const uint16_t* d_x, void* d_y, q4nx_dtype y_dtype, int64_t N,

@@ -170,6 +170,12 @@ def test_device_calls_validate_before_hip():
     assert L.q4nx_gemm(4, 32, 256, A16, MIS, A16, 0, None) == q4.Q4NX_ERR_ALIGNMENT
     assert L.q4nx_gemm(4, 32, 256, A16, A16, MIS, 0, None) == q4.Q4NX_ERR_ALIGNMENT
     assert L.q4nx_gemm(4, 32, 256, A16, A16, A16, 3, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_quantize(A16, 32, 80, A16, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_quantize(A16, 0, 256, A16, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_quantize(None, 32, 256, A16, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_quantize(A16, 32, 256, None, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_quantize(MIS, 32, 256, A16, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_quantize(A16, 32, 256, MIS, None) == q4.Q4NX_ERR_ALIGNMENT
     assert L.q4nx_gemm_bf16(0, 32, 256, A16, A16, A16, 0, None) == q4.Q4NX_ERR_SHAPE
     assert L.q4nx_gemm_bf16(4, 32, 80, A16, A16, A16, 0, None) == q4.Q4NX_ERR_SHAPE
     assert L.q4nx_gemm_bf16(4, 32, 256, None, A16, A16, 0, None) == q4.Q4NX_ERR_INVALID_ARG

@@ -337,3 +337,47 @@ def test_gemm_bf16_arbitrary_weights_vs_float64(q4, M, N, K):
     ok, worst = oracle.check_close(Yh, ref, oracle.abs_bound(X, w16))
     assert ok, worst
     assert (np.abs(Yh.astype(np.float64) - ref) <= 1e-5 * oracle.abs_bound(X, w16) + 1e-6).all()
+
+
+# ----------------------------------------------------------------- quantizer
+def _edge_weights(N, K, seed):
+    rng = np.random.default_rng(seed)
+    W = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    G = K // 32
+    kinds = rng.integers(0, 8, size=(N, G))
+    for n in range(N):
+        for g in range(G):
+            sl = W[n, 32 * g:32 * g + 32]
+            k = kinds[n, g]
+            if k == 1:
+                sl[:] = np.float32(0.125)                                  # constant
+            elif k == 2:
+                sl[:] = rng.integers(-4, 5, 32).astype(np.float32)         # ties on an integer grid
+                sl[0], sl[1] = -4.0, 11.0
+            elif k == 3:
+                sl[:] = (rng.standard_normal(32) * 2.0 ** -110).astype(np.float32)  # d, m flushed
+            elif k == 4:
+                sl[:] = (rng.standard_normal(32) * 1e31).astype(np.float32)        # clamped
+                sl[3], sl[4], sl[5] = np.inf, -np.inf, np.nan
+            elif k == 5:
+                sl[:] = 0.0
+                sl[7] = -0.0
+            elif k == 6:
+                sl[:] = -np.abs(sl) - np.float32(3.0)                       # offset far from zero
+    return W
+
+
+@pytest.mark.parametrize("N,K,kind", [(1, 32, "normal"), (33, 288, "edge"), (64, 1152, "edge"),
+                                      (1024, 1152, "normal"), (2048, 5376, "normal"), (100, 21504, "edge")])
+def test_quantize_bit_exact(q4, N, K, kind):
+    _say("quantize", N, K, kind)
+    if kind == "edge":
+        W = _edge_weights(N, K, seed=N + K)
+    else:
+        W = (np.random.default_rng(N).standard_normal((N, K)) * 0.02).astype(np.float32)
+    want = oracle.pack(*oracle.quantize(W))
+    blob = torch.full((q4.q4nx_packed_size(N, K),), 0xAB, dtype=torch.uint8, device="cuda")
+    q4.q4nx_quantize(torch.from_numpy(W).cuda(), N, K, blob)
+    torch.cuda.synchronize()
+    got = blob.cpu().numpy()
+    assert np.array_equal(got, want)
