@@ -1,4 +1,5 @@
-"""CPU oracle for the Q4NX projection path -- TEST INFRASTRUCTURE ONLY.
+"""CPU oracle for the Q4NX projection path and its next steps (the quantizer
+into Q4NX, FlowKV decode attention) -- TEST INFRASTRUCTURE ONLY.
 
 A plain, slow, obviously correct NumPy implementation of what the GPU path
 computes: the Q4NX block format, the block-wise asymmetric dequantization
@@ -25,3 +26,4 @@ from .q4nx import (  # noqa: F401
     tolerance, check_close,
 )
 from .quantize import quantize, clamp_weights, group_scale_offset  # noqa: F401,E402
+from .attention import attended_range, decode_attention, decode_attention_chunked  # noqa: F401,E402
