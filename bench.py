@@ -54,6 +54,9 @@ def parse():
                     help="also time the two-phase prefill (q4nx_dequant to bf16, then q4nx_gemm_bf16)")
     ap.add_argument("--quantize", type=int, default=1,
                     help="also time q4nx_quantize on the model's largest projection (float32 -> Q4NX)")
+    ap.add_argument("--flowkv", type=int, default=1,
+                    help="also time FlowKV decode attention over every layer at --context positions")
+    ap.add_argument("--context", type=int, default=32768, help="decode position + 1 for the FlowKV timing")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="run one eager decode step, one prefill step and a 1 GiB device copy (for rocprofv3 "
                          "counter passes), then exit")
@@ -481,6 +484,45 @@ def main():
                  "bytes": "4 B read + 0.625 B written per weight"}
         del Wq, Bq
 
+    fkv = None
+    if args.flowkv and do_decode:
+        from workloads import ATTENTION, SWA_WINDOW, is_global_layer
+        A = ATTENTION[cfg["model"]]
+        H, G, d = A["H"], A["G"], A["d"]
+        gk = torch.Generator(device="cuda")
+        gk.manual_seed(args.seed + 7)
+        sk = Step(q4, stream.cuda_stream)
+        kv_bytes, bufs = 0, []
+        T = args.context
+        wbytes = q4.q4nx_flowkv_workspace_size(H, d, T)
+        work = torch.empty(wbytes // 4, dtype=torch.float32, device="cuda")
+        for l in range(L):
+            glob = is_global_layer(l)
+            Lc = T if glob else min(T, SWA_WINDOW)   # a sliding-window layer keeps the last 1024 positions
+            t = Lc - 1
+            win = 0 if glob else SWA_WINDOW
+            Kc = (torch.randn((G, Lc, d), generator=gk, device="cuda")).to(torch.bfloat16)
+            Vc = (torch.randn((G, Lc, d), generator=gk, device="cuda")).to(torch.bfloat16)
+            qv = (torch.randn((H, d), generator=gk, device="cuda")).to(torch.bfloat16)
+            ov = torch.empty((H, d), dtype=torch.float32, device="cuda")
+            bufs += [Kc, Vc, qv, ov]
+            sk.calls.append((q4.lib.q4nx_flowkv_decode,
+                             (qv.data_ptr(), Kc.data_ptr(), Vc.data_ptr(), H, G, d, Lc, t, win,
+                              ctypes.c_float(1.0 / d ** 0.5), ov.data_ptr(), q4.Q4NX_F32, work.data_ptr(),
+                              wbytes, sk.s)))
+            kv_bytes += 2 * G * min(Lc, T) * d * 2
+        for _ in range(args.warmup):
+            sk.run()
+        _, k_ms, _ = timed(lambda: None, sk.run, args.steps)
+        tk = mean(k_ms)
+        fkv = {"context": T, "layers": L, "global_layers": sum(is_global_layer(l) for l in range(L)),
+               "window": SWA_WINDOW, "heads": H, "kv_groups": G, "head_dim": d,
+               "ms": round(tk, 4), "ms_min": round(min(k_ms), 4), "kv_GB": round(kv_bytes / 1e9, 4),
+               "GB_per_s": round(kv_bytes / (tk * 1e-3) / 1e9, 2),
+               "frac_hbm": round(kv_bytes / (tk * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+               "launches": 2 * L, "bytes": "K and V rows of the attended positions, bf16"}
+        del bufs, work
+
     dec_gbs = dec_bytes / (mean(dec_ms) * 1e-3) / 1e9 if do_decode else None
     pre_tflops = pre_flops / (mean(pre_ms) * 1e-3) / 1e12 if do_prefill else None
 
@@ -544,6 +586,8 @@ def main():
 
     if quant:
         result["quantize"] = quant
+    if fkv:
+        result["flowkv_decode_attention"] = fkv
     stored = stored_traffic(args.config)
     for key, fam in (("roofline", "gemm" if do_prefill else "gemv"), ("roofline_gemv", "gemv")):
         if key in result and stored and fam in stored["families"]:

@@ -209,6 +209,45 @@ q4nx_status q4nx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, cons
 q4nx_status q4nx_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const uint16_t* d_W,
                            void* d_Y, q4nx_dtype y_dtype, hipStream_t stream);
 
+/* Smallest chunk (cache positions per workgroup) of q4nx_flowkv_decode. */
+#define Q4NX_FLOWKV_MIN_CHUNK 64
+
+/*
+ * Bytes of the workspace q4nx_flowkv_decode needs for H query heads of
+ * dimension d attending to n_keys cache positions:
+ * H * ceil(n_keys / 64) * (d + 4) * 4.  Returns 0 for a non-positive or
+ * out-of-range argument.
+ */
+size_t q4nx_flowkv_workspace_size(int64_t H, int64_t d, int64_t n_keys);
+
+/*
+ * Device.  FlowKV decode attention (Sec. 3.2.2, FlowKV and FlowKV-SWA): the
+ * attention output of decode position t over the KV cache of positions
+ * 0..t (the causal-attention equation of Sec. 2.3, with the score scaling of
+ * Eq. 6 passed as `scale`, 1/sqrt(d) in the paper), computed with FlowKV's
+ * chunk sweep (Eq. 6-12 with a query chunk of 1):
+ *   o[h] = sum_j softmax_j(scale * q[h] . k[g][j]) v[g][j],  g = h / (H/G),
+ *   j over 0..t (window == 0) or max(0, t-window+1)..t (window > 0, SWA).
+ *   d_q     : device, [H][d] bf16, 16-byte aligned
+ *   d_k,d_v : device, [G][L][d] bf16 (row j of group g = cache position j);
+ *             only positions of the attended range are read; 16-byte aligned
+ *   H, G    : query heads and KV groups (GQA), H/G in {1, 2, 4, 8}
+ *   d       : head dimension, 64, 128 or 256
+ *   L       : cache capacity (row count per group), 0 <= t < L <= 2^30
+ *   d_o     : device, [H][d] of o_dtype, 4-byte aligned; fully written
+ *   d_work  : device, >= q4nx_flowkv_workspace_size(H, d, attended length)
+ *             bytes, 16-byte aligned, owned by the caller; its contents on
+ *             entry do not matter and are overwritten
+ * Scores are float32 sums of exact bf16 products; exponentials, sums and
+ * the final division are float32.  Calls that share a workspace must not
+ * overlap.  Errors: Q4NX_ERR_INVALID_ARG (NULL pointer, unknown dtype,
+ * non-finite scale), Q4NX_ERR_SHAPE, Q4NX_ERR_ALIGNMENT,
+ * Q4NX_ERR_BUFFER_TOO_SMALL (workspace), Q4NX_ERR_HIP.
+ */
+q4nx_status q4nx_flowkv_decode(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_v, int64_t H, int64_t G,
+                               int64_t d, int64_t L, int64_t t, int64_t window, float scale, void* d_o,
+                               q4nx_dtype o_dtype, void* d_work, size_t work_bytes, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* q4nx_status_str(q4nx_status status);
 

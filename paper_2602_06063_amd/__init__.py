@@ -30,7 +30,8 @@ Q4NX_BF16 = 1
 Q4NX_MAX_BATCH = 8
 
 EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_quantize", "q4nx_dequant", "q4nx_gemv",
-            "q4nx_gemv_batched", "q4nx_gemm", "q4nx_gemm_bf16", "q4nx_status_str", "q4nx_last_error"]
+            "q4nx_gemv_batched", "q4nx_gemm", "q4nx_gemm_bf16", "q4nx_flowkv_workspace_size",
+            "q4nx_flowkv_decode", "q4nx_status_str", "q4nx_last_error"]
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2602_06063_amd/build.py`")
@@ -71,6 +72,11 @@ lib.q4nx_gemm.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp]
 lib.q4nx_gemm.restype = ctypes.c_int
 lib.q4nx_gemm_bf16.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp]
 lib.q4nx_gemm_bf16.restype = ctypes.c_int
+lib.q4nx_flowkv_workspace_size.argtypes = [_i64, _i64, _i64]
+lib.q4nx_flowkv_workspace_size.restype = _sz
+lib.q4nx_flowkv_decode.argtypes = [_vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, ctypes.c_float, _vp,
+                                   ctypes.c_int, _vp, _sz, _vp]
+lib.q4nx_flowkv_decode.restype = ctypes.c_int
 lib.q4nx_status_str.argtypes = [ctypes.c_int]
 lib.q4nx_status_str.restype = ctypes.c_char_p
 lib.q4nx_last_error.argtypes = []
@@ -211,3 +217,20 @@ def q4nx_gemm_bf16(M: int, N: int, K: int, X, W, Y, stream=None):
     _need(Y, M * N * Y.element_size(), "Y")
     _check(lib.q4nx_gemm_bf16(M, N, K, _dptr(X), _dptr(W), _dptr(Y), _dtype_code(Y), _stream(stream)),
            "q4nx_gemm_bf16")
+
+
+def q4nx_flowkv_workspace_size(H: int, d: int, n_keys: int) -> int:
+    return lib.q4nx_flowkv_workspace_size(H, d, n_keys)
+
+
+def q4nx_flowkv_decode(q, K, V, H: int, G: int, d: int, L: int, t: int, window: int, scale: float, o, work,
+                       stream=None):
+    """o[H][d] <- FlowKV decode attention of the query q[H][d] over the cache
+    K, V [G][L][d] at position t (window 0 = full attention)."""
+    _need(q, 2 * H * d, "q")
+    _need(K, 2 * G * L * d, "K")
+    _need(V, 2 * G * L * d, "V")
+    _need(o, H * d * o.element_size(), "o")
+    _check(lib.q4nx_flowkv_decode(_dptr(q), _dptr(K), _dptr(V), H, G, d, L, t, window, scale, _dptr(o),
+                                  _dtype_code(o), _dptr(work), work.numel() * work.element_size(), _stream(stream)),
+           "q4nx_flowkv_decode")

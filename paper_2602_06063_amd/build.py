@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libq4nx.so")
 ARCH = "gfx950"
 
-SOURCES = ["q4nx_host.cpp", "q4nx_kernels.hip"]
+SOURCES = ["q4nx_host.cpp", "q4nx_kernels.hip", "q4nx_flowkv.hip"]
 
 
 def hipcc() -> str:

@@ -1,0 +1,330 @@
+// FlowKV decode attention for gfx950: the attention of one decode position
+// over the KV cache (the causal-attention equation of the decoding section),
+// computed with FlowKV's chunk sweep (Eq. 6-12 with a query chunk of 1), with
+// its sliding-window variant.
+//
+// The sweep is split in two launches.  Phase 1 gives every (KV group, chunk of
+// 64, 128 or 256 positions) to one workgroup, which computes for the H/G query heads
+// of the group the chunk's own running state: the max score m_c (Eq. 7), the
+// denominator l_c = sum exp(s - m_c) (Eq. 8, 10) and the weighted values
+// Y_c = sum exp(s - m_c) v (Eq. 11), into the caller's workspace.  Phase 2
+// merges the chunks of each head with the correction factor of Eq. 9 taken
+// relative to the largest chunk max, which is what the left-to-right
+// recurrence reaches after the last chunk, then divides (Eq. 12).  Reading the cache is the whole cost: each K and V
+// row is read once, by one workgroup, with full 128-byte rows per load.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <string>
+
+#include "q4nx_internal.h"
+
+namespace q4nx {
+
+typedef __bf16 bf16x2f __attribute__((ext_vector_type(2)));
+
+constexpr int kMinChunk = 64;      // smallest chunk: sizes the workspace
+constexpr int kFkvThreads = 256;   // 4 waves
+
+// a.lo * b.lo + a.hi * b.hi + c for two bf16 pairs (exact products, float32 sum).
+__device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2f, a), __builtin_bit_cast(bf16x2f, b), c, false);
+}
+
+__device__ __forceinline__ float bf16lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t v) { return __uint_as_float(v & 0xFFFF0000u); }
+
+// Wave-wide reductions in a fixed order (deterministic).
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// Phase 1.  grid (chunks, G); CH cache positions per workgroup, D = head
+// dimension, HG = query heads per group.  Partial of (head, chunk) at
+// work[(head * nchunks + chunk) * (D + 4)]: m_c, l_c, -, -, Y_c[D].
+template <int CH, int D, int HG>
+__global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_t* __restrict__ q,
+                                                                  const uint16_t* __restrict__ K,
+                                                                  const uint16_t* __restrict__ V, int64_t L,
+                                                                  int j0, int j1, float scale,
+                                                                  float* __restrict__ work) {
+  constexpr int kPart = D + 4;
+  constexpr int R = D / 8;        // lanes per V row (16 bytes each)
+  constexpr int P = 64 / R;       // V rows per wave load
+  __shared__ __attribute__((aligned(16))) uint32_t qs[HG][D / 2];   // query bf16 pairs
+  __shared__ float fs[CH][HG];                                       // scores, then exp(s - m_c)
+  __shared__ float red[4][HG];
+  __shared__ __attribute__((aligned(16))) float ys[4][HG][D];        // per-wave partial Y
+
+  const int c = blockIdx.x, g = blockIdx.y, nchunks = gridDim.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int k0 = j0 + c * CH, n = min(j1 - k0, CH);   // positions k0 .. k0+n-1
+  const uint16_t* Kg = K + (size_t)g * L * D + (size_t)k0 * D;
+  const uint16_t* Vg = V + (size_t)g * L * D + (size_t)k0 * D;
+
+  for (int e = tid; e < HG * D / 2; e += kFkvThreads) {
+    const int h = e / (D / 2), p = e % (D / 2);
+    qs[h][p] = reinterpret_cast<const uint32_t*>(q + (size_t)(g * HG + h) * D)[p];
+  }
+  __syncthreads();
+
+  // Scores (Eq. 6): 8 lanes per position (8 x 16 B = one 128-byte piece of
+  // the row per load); lane u of the 8 takes dims 64i + 8u .. +7.
+  const int u = lane & 7, kw = lane >> 3;
+#pragma unroll 2
+  for (int r = 0; r < CH / 32; ++r) {
+    const int pl = (r * 4 + wave) * 8 + kw;
+    float acc[HG];
+#pragma unroll
+    for (int h = 0; h < HG; ++h) acc[h] = 0.0f;
+    if (pl < n) {
+      const uint4* row = reinterpret_cast<const uint4*>(Kg + (size_t)pl * D);
+#pragma unroll
+      for (int i = 0; i < D / 64; ++i) {
+        const uint4 kv = row[8 * i + u];
+#pragma unroll
+        for (int h = 0; h < HG; ++h) {
+          const uint4 qv = *reinterpret_cast<const uint4*>(&qs[h][32 * i + 4 * u]);
+          acc[h] = dot2(kv.x, qv.x, acc[h]);
+          acc[h] = dot2(kv.y, qv.y, acc[h]);
+          acc[h] = dot2(kv.z, qv.z, acc[h]);
+          acc[h] = dot2(kv.w, qv.w, acc[h]);
+        }
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < HG; ++h) {
+      float v = acc[h];
+      v += __shfl_xor(v, 1);
+      v += __shfl_xor(v, 2);
+      v += __shfl_xor(v, 4);
+      if (u == 0) fs[pl][h] = pl < n ? v * scale : -INFINITY;
+    }
+  }
+  __syncthreads();
+
+  // Chunk max (Eq. 7), exponentials (Eq. 8) and their sum (Eq. 10);
+  // thread tid < CH owns position tid.
+  float m[HG], l[HG];
+#pragma unroll
+  for (int h = 0; h < HG; ++h) {
+    const float v = wave_max(tid < CH ? fs[tid][h] : -INFINITY);
+    if (lane == 0) red[wave][h] = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < HG; ++h) m[h] = fmaxf(fmaxf(red[0][h], red[1][h]), fmaxf(red[2][h], red[3][h]));
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < HG; ++h) {
+    float f = 0.0f;
+    if (tid < CH) {
+      f = expf(fs[tid][h] - m[h]);   // exp(-inf) = 0 past the range
+      fs[tid][h] = f;
+    }
+    const float sm = wave_sum(f);
+    if (lane == 0) red[wave][h] = sm;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int h = 0; h < HG; ++h) l[h] = (red[0][h] + red[1][h]) + (red[2][h] + red[3][h]);
+
+  // Weighted values (Eq. 11): R lanes per row, 16 bytes (8 dims) each; wave
+  // w reads rows w*P + rs, then every 4P rows.
+  const int rs = lane / R, db = lane % R;
+  float y[HG][8];
+#pragma unroll
+  for (int h = 0; h < HG; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[h][e] = 0.0f;
+#pragma unroll 2
+  for (int pl = wave * P + rs; pl < n; pl += 4 * P) {
+    const uint4 w = reinterpret_cast<const uint4*>(Vg + (size_t)pl * D)[db];
+    const float v[8] = {bf16lo(w.x), bf16hi(w.x), bf16lo(w.y), bf16hi(w.y),
+                        bf16lo(w.z), bf16hi(w.z), bf16lo(w.w), bf16hi(w.w)};
+#pragma unroll
+    for (int h = 0; h < HG; ++h) {
+      const float f = fs[pl][h];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) y[h][e] = fmaf(f, v[e], y[h][e]);
+    }
+  }
+  // Sum the P row slots of the wave (lanes db, db + R, ...), then the 4 waves.
+#pragma unroll
+  for (int h = 0; h < HG; ++h)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float v = y[h][e];
+#pragma unroll
+      for (int o = R; o < 64; o <<= 1) v += __shfl_xor(v, o);
+      y[h][e] = v;
+    }
+  if (rs == 0) {
+#pragma unroll
+    for (int h = 0; h < HG; ++h)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) ys[wave][h][8 * db + e] = y[h][e];
+  }
+  __syncthreads();
+
+  for (int e = tid; e < HG * D; e += kFkvThreads) {
+    const int h = e / D, dd = e % D;
+    float* part = work + ((size_t)(g * HG + h) * nchunks + c) * kPart;
+    part[4 + dd] = (ys[0][h][dd] + ys[1][h][dd]) + (ys[2][h][dd] + ys[3][h][dd]);
+    if (dd == 0) {
+      part[0] = m[h];
+      part[1] = l[h];
+    }
+  }
+}
+
+// Phase 2.  grid H, 256 threads: S = 256 / D slices of D threads; slice s
+// takes chunks s, s + S, ...  With M the largest chunk max, Eq. 9's
+// correction of chunk c relative to M is exp(m_c - M); the head's output is
+// sum_c exp(m_c - M) Y_c / sum_c exp(m_c - M) l_c (Eq. 10-12), summed over
+// the chunks in increasing order within a slice and then over the slices.
+template <int D>
+__global__ __launch_bounds__(kFkvThreads) void flowkv_merge_kernel(const float* __restrict__ work, int nchunks,
+                                                                   void* __restrict__ out, int out_bf16) {
+  constexpr int kPart = D + 4, S = kFkvThreads / D;
+  __shared__ float mx[kFkvThreads / 64];
+  __shared__ float ls[S], yls[S][D];
+  const int h = blockIdx.x, tid = threadIdx.x, dd = tid % D, sl = tid / D;
+  const float* part = work + (size_t)h * nchunks * kPart;
+  float mloc = -INFINITY;
+  for (int c = tid; c < nchunks; c += kFkvThreads) mloc = fmaxf(mloc, part[(size_t)c * kPart]);
+  mloc = wave_max(mloc);
+  if ((tid & 63) == 0) mx[tid >> 6] = mloc;
+  __syncthreads();
+  float M = mx[0];
+#pragma unroll
+  for (int w = 1; w < kFkvThreads / 64; ++w) M = fmaxf(M, mx[w]);
+  float l = 0.0f, y = 0.0f;
+#pragma unroll 4
+  for (int c = sl; c < nchunks; c += S) {
+    const float* pc = part + (size_t)c * kPart;
+    const float a = expf(pc[0] - M);
+    l = fmaf(a, pc[1], l);
+    y = fmaf(a, pc[4 + dd], y);
+  }
+  yls[sl][dd] = y;
+  if (dd == 0) ls[sl] = l;
+  __syncthreads();
+  if (sl == 0) {
+    float yt = yls[0][dd], lt = ls[0];
+#pragma unroll
+    for (int s2 = 1; s2 < S; ++s2) {
+      yt += yls[s2][dd];
+      lt += ls[s2];
+    }
+    const float o = yt / lt;
+    if (out_bf16) {
+      bf16x2f p = __builtin_convertvector((float __attribute__((ext_vector_type(2)))){o, 0.0f}, bf16x2f);
+      static_cast<uint16_t*>(out)[(size_t)h * D + dd] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
+    } else {
+      static_cast<float*>(out)[(size_t)h * D + dd] = o;
+    }
+  }
+}
+
+template <int CH, int D, int HG>
+static void launch_flowkv(const uint16_t* q, const uint16_t* K, const uint16_t* V, int64_t L, int G, int j0, int j1,
+                          float scale, float* work, void* out, int out_bf16, hipStream_t stream) {
+  const int nchunks = (int)ceil_div(j1 - j0, CH);
+  hipLaunchKernelGGL((flowkv_chunk_kernel<CH, D, HG>), dim3(nchunks, G), dim3(kFkvThreads), 0, stream, q, K, V, L,
+                     j0, j1, scale, work);
+  hipLaunchKernelGGL((flowkv_merge_kernel<D>), dim3(G * HG), dim3(kFkvThreads), 0, stream, work, nchunks, out,
+                     out_bf16);
+}
+
+// Chunk size: the largest of 256, 128, 64 positions that still gives at
+// least two workgroups per CU.
+template <int D, int HG>
+static void launch_chunked(const uint16_t* q, const uint16_t* K, const uint16_t* V, int64_t L, int G, int j0, int j1,
+                           float scale, float* work, void* out, int out_bf16, hipStream_t stream, int cus) {
+  const int64_t n = j1 - j0;
+  if (ceil_div(n, 256) * G >= 2 * cus)
+    launch_flowkv<256, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream);
+  else if (ceil_div(n, 128) * G >= 2 * cus)
+    launch_flowkv<128, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream);
+  else
+    launch_flowkv<64, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream);
+}
+
+template <int D>
+static bool dispatch_hg(int hg, const uint16_t* q, const uint16_t* K, const uint16_t* V, int64_t L, int G, int j0,
+                        int j1, float scale, float* work, void* out, int out_bf16, hipStream_t stream, int cus) {
+  switch (hg) {
+    case 1: launch_chunked<D, 1>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream, cus); return true;
+    case 2: launch_chunked<D, 2>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream, cus); return true;
+    case 4: launch_chunked<D, 4>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream, cus); return true;
+    case 8: launch_chunked<D, 8>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream, cus); return true;
+    default: return false;
+  }
+}
+
+static int fkv_device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int v = 0;
+    cus[dev] = (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) ? v : 256;
+  }
+  return cus[dev];
+}
+
+}  // namespace q4nx
+
+using namespace q4nx;
+
+extern "C" {
+
+size_t q4nx_flowkv_workspace_size(int64_t H, int64_t d, int64_t n_keys) {
+  if (H <= 0 || d <= 0 || n_keys <= 0 || H > (1 << 16) || d > 4096 || n_keys > (int64_t(1) << 30)) return 0;
+  return (size_t)H * (size_t)ceil_div(n_keys, kMinChunk) * (size_t)(d + 4) * sizeof(float);
+}
+
+q4nx_status q4nx_flowkv_decode(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_v, int64_t H, int64_t G,
+                               int64_t d, int64_t L, int64_t t, int64_t window, float scale, void* d_o,
+                               q4nx_dtype o_dtype, void* d_work, size_t work_bytes, hipStream_t stream) {
+  clear_error();
+  if (!d_q || !d_k || !d_v || !d_o || !d_work) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_flowkv_decode: NULL pointer");
+  if (o_dtype != Q4NX_F32 && o_dtype != Q4NX_BF16)
+    return fail(Q4NX_ERR_INVALID_ARG, "q4nx_flowkv_decode: unknown o_dtype");
+  if (!std::isfinite(scale)) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_flowkv_decode: scale must be finite");
+  if (H <= 0 || G <= 0 || H % G != 0 || G > 65535)
+    return fail(Q4NX_ERR_SHAPE, "q4nx_flowkv_decode: H must be a positive multiple of G");
+  const int64_t hg = H / G;
+  if (hg != 1 && hg != 2 && hg != 4 && hg != 8)
+    return fail(Q4NX_ERR_SHAPE, "q4nx_flowkv_decode: H/G must be 1, 2, 4 or 8");
+  if (d != 64 && d != 128 && d != 256) return fail(Q4NX_ERR_SHAPE, "q4nx_flowkv_decode: d must be 64, 128 or 256");
+  if (L <= 0 || L > (int64_t(1) << 30) || t < 0 || t >= L || window < 0)
+    return fail(Q4NX_ERR_SHAPE, "q4nx_flowkv_decode: need 0 <= t < L <= 2^30 and window >= 0");
+  if (!aligned(d_q, 16) || !aligned(d_k, 16) || !aligned(d_v, 16) || !aligned(d_o, 4) || !aligned(d_work, 16))
+    return fail(Q4NX_ERR_ALIGNMENT, "q4nx_flowkv_decode: q, K, V and workspace need 16-byte alignment, o 4-byte");
+  const int64_t j1 = t + 1, j0 = window == 0 ? 0 : std::max<int64_t>(0, j1 - window);
+  const size_t need = q4nx_flowkv_workspace_size(H, d, j1 - j0);
+  if (work_bytes < need)
+    return fail(Q4NX_ERR_BUFFER_TOO_SMALL, "q4nx_flowkv_decode: workspace smaller than q4nx_flowkv_workspace_size");
+  const int ob = o_dtype == Q4NX_BF16;
+  float* work = static_cast<float*>(d_work);
+  bool ok = false;
+  const int cus = fkv_device_cus();
+  if (d == 64) ok = dispatch_hg<64>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
+  if (d == 128) ok = dispatch_hg<128>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
+  if (d == 256) ok = dispatch_hg<256>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
+  if (!ok) return fail(Q4NX_ERR_SHAPE, "q4nx_flowkv_decode: unsupported shape");
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(Q4NX_ERR_HIP, std::string("q4nx_flowkv_decode: ") + hipGetErrorString(e));
+  return Q4NX_OK;
+}
+
+}  // extern "C"

@@ -199,3 +199,31 @@ def test_single_hip_runtime_in_process():
     import torch
     torch_lib = os.path.join(os.path.dirname(torch.__file__), "lib")
     assert next(iter(paths)).startswith(torch_lib), paths
+
+
+def test_flowkv_workspace_size_and_validation():
+    import paper_2602_06063_amd as q4
+    L = q4.lib
+    assert L.q4nx_flowkv_workspace_size(8, 256, 1) == 8 * 1 * 260 * 4
+    assert L.q4nx_flowkv_workspace_size(8, 256, 257) == 8 * 5 * 260 * 4
+    assert L.q4nx_flowkv_workspace_size(32, 128, 32768) == 32 * 512 * 132 * 4
+    assert L.q4nx_flowkv_workspace_size(0, 256, 10) == 0 and L.q4nx_flowkv_workspace_size(8, 256, 0) == 0
+    A = ctypes.c_void_p(1 << 20)      # aligned, never dereferenced: every call below fails validation
+    MIS = ctypes.c_void_p((1 << 20) + 2)
+    W = 1 << 30
+
+    def call(q=A, k=A, v=A, H=8, G=4, d=256, Lc=1024, t=10, win=0, scale=0.0625, o=A, odt=0, work=A, wb=W):
+        return L.q4nx_flowkv_decode(q, k, v, H, G, d, Lc, t, win, scale, o, odt, work, wb, None)
+    assert call(q=None) == q4.Q4NX_ERR_INVALID_ARG
+    assert call(work=None) == q4.Q4NX_ERR_INVALID_ARG
+    assert call(odt=5) == q4.Q4NX_ERR_INVALID_ARG
+    assert call(scale=float("inf")) == q4.Q4NX_ERR_INVALID_ARG
+    assert call(H=6, G=4) == q4.Q4NX_ERR_SHAPE
+    assert call(H=48, G=3) == q4.Q4NX_ERR_SHAPE        # H/G = 16
+    assert call(d=96) == q4.Q4NX_ERR_SHAPE
+    assert call(t=1024) == q4.Q4NX_ERR_SHAPE
+    assert call(t=-1) == q4.Q4NX_ERR_SHAPE
+    assert call(win=-2) == q4.Q4NX_ERR_SHAPE
+    assert call(k=MIS) == q4.Q4NX_ERR_ALIGNMENT
+    assert call(work=MIS) == q4.Q4NX_ERR_ALIGNMENT
+    assert call(wb=8 * 260 * 4 - 1) == q4.Q4NX_ERR_BUFFER_TOO_SMALL

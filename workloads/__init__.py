@@ -53,6 +53,23 @@ MODELS = {
     },
 }
 
+# Attention geometry (query heads H, KV groups G, head dimension d) and the
+# layer pattern: 5 sliding-window layers (window 1024) per global layer,
+# starting with a sliding-window layer (Sec. 2.2).  The 4B geometry is the
+# paper's; the 1B and 27B ones are the public Gemma3 configurations.
+ATTENTION = {
+    "1b": {"H": 4, "G": 1, "d": 256},
+    "4b": {"H": 8, "G": 4, "d": 256},
+    "27b": {"H": 32, "G": 16, "d": 128},
+}
+SWA_WINDOW = 1024
+GLOBAL_EVERY = 6
+
+
+def is_global_layer(layer: int) -> bool:
+    return (layer + 1) % GLOBAL_EVERY == 0
+
+
 # The five workloads: model, token rows M, whether lm_head runs once per step.
 CONFIGS = {
     0: {"name": "gemma3-1b q_proj GEMV 1024x1152", "model": "1b", "M": [1], "single": ("q", 1024, 1152)},
