@@ -223,7 +223,7 @@ size_t q4nx_flowkv_workspace_size(int64_t H, int64_t d, int64_t n_keys);
 /*
  * Device.  FlowKV decode attention (Sec. 3.2.2, FlowKV and FlowKV-SWA): the
  * attention output of decode position t over the KV cache of positions
- * 0..t (the causal-attention equation of Sec. 2.3, with the score scaling of
+ * 0..t (the causal-attention equation of Sec. 2.2, with the score scaling of
  * Eq. 6 passed as `scale`, 1/sqrt(d) in the paper), computed with FlowKV's
  * chunk sweep (Eq. 6-12 with a query chunk of 1):
  *   o[h] = sum_j softmax_j(scale * q[h] . k[g][j]) v[g][j],  g = h / (H/G),
