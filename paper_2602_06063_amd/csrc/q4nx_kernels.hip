@@ -49,17 +49,12 @@ __device__ __forceinline__ uint16_t f32_to_bf16_bits(float a) {
 }
 
 // Streaming loads of the packed weights (read once per call).
-#ifndef Q4NX_PLAIN_LOADS
 __device__ __forceinline__ u32x4 load_codes(const uint8_t* p) {
   return __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p));
 }
 __device__ __forceinline__ uint32_t load_u16(const uint8_t* p) {
   return (uint32_t)__builtin_nontemporal_load(reinterpret_cast<const uint16_t*>(p));
 }
-#else
-__device__ __forceinline__ u32x4 load_codes(const uint8_t* p) { return *reinterpret_cast<const u32x4*>(p); }
-__device__ __forceinline__ uint32_t load_u16(const uint8_t* p) { return *reinterpret_cast<const uint16_t*>(p); }
-#endif
 
 // A byte holding a 4-bit code q, read as an FP8 E4M3 value, is exactly
 // q * 2^-9 (codes 0..7 are the subnormals m * 2^-9, codes 8..15 the first
@@ -284,10 +279,7 @@ constexpr int kGemvChunkBlocks = 48;                    // x staged 48 x 256 col
 constexpr int kGroupPadDw = 20;  // dwords per staged group (16 bf16 pairs + 4 pad: conflict-free reads)
 constexpr int kRedFloats = kGemvMaxWaves * 32;
 // Blocks in flight per wave (register slots), by row octets per wave.
-#ifndef Q4NX_GEMV_D4
-#define Q4NX_GEMV_D4 1
-#endif
-constexpr int kGemvDepth4 = Q4NX_GEMV_D4, kGemvDepth2 = 3, kGemvDepth1 = 4;
+constexpr int kGemvDepth4 = 1, kGemvDepth2 = 3, kGemvDepth1 = 4;
 
 struct GemvJob {
   const uint8_t* blob;
@@ -1171,9 +1163,6 @@ static q4nx_status check_launch(const char* fn) {
 // ~160 CUs streaming (one CU sustains ~55 GB/s of the ~7 TB/s), else halves or
 // quarters of strips.  `strips` is the number of strips of the whole launch.
 static int gemv_tq(int64_t strips) {
-#ifdef Q4NX_TUNE
-  if (const char* e = getenv("Q4NX_TUNE_TQ")) return atoi(e);
-#endif
   if (strips >= 160) return 4;
   if (strips * 2 >= 160) return 2;
   return 1;
@@ -1186,9 +1175,6 @@ static int gemv_tq(int64_t strips) {
 // owns at least one block of every job.  Measured on MI355X over the Gemma3
 // 1B/4B/27B projection shapes.
 static int gemv_waves(int64_t row_groups, int min_kb) {
-#ifdef Q4NX_TUNE
-  if (const char* e = getenv("Q4NX_TUNE_WAVES")) return std::max(1, std::min(kGemvMaxWaves, atoi(e)));
-#endif
   int w = row_groups >= 4096 ? 2 : row_groups >= 512 ? 4 : row_groups >= 128 ? 8 : 16;
   while (w > 1 && w > min_kb) w >>= 1;
   return w;
