@@ -1,5 +1,6 @@
 """CPU oracle for the Q4NX projection path and its next steps (the quantizer
-into Q4NX, FlowKV decode attention) -- TEST INFRASTRUCTURE ONLY.
+into Q4NX, FlowKV decode attention, the MXFP4 block variant) -- TEST
+INFRASTRUCTURE ONLY.
 
 A plain, slow, obviously correct NumPy implementation of what the GPU path
 computes: the Q4NX block format, the block-wise asymmetric dequantization
@@ -27,3 +28,6 @@ from .q4nx import (  # noqa: F401
 )
 from .quantize import quantize, clamp_weights, group_scale_offset  # noqa: F401,E402
 from .attention import attended_range, decode_attention, decode_attention_chunked  # noqa: F401,E402
+from .mxfp4 import (  # noqa: F401,E402
+    MX_BLOCK_BYTES, fp4_value, e8m0_value, mx_packed_size, mx_pack, mx_unpack, mx_dequant_f32, mx_quantize,
+)
