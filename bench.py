@@ -13,7 +13,9 @@ activations.  Timing uses HIP events on the stream the kernels run on.
 
 Prints one JSON line: value = decode weight GB/s (0.625 B per weight: the
 4-bit code plus the per-32 bf16 scale and offset); the prefill TFLOP/s
-(2*M*N*K per projection) is reported beside it.
+(2*M*N*K per projection) is reported beside it.  The same steps over weights
+in the MXFP4 variant of the block (0.53125 B per weight: the FP4 code plus the
+per-32 E8M0 scale) are timed and reported under "mxfp4".
 
     python bench.py [--config 4] [--steps 5] [--warmup 2] [--gpus 1]
 """
@@ -33,6 +35,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 BF16_MFMA_PEAK_TFLOPS = 2516.6  # 256 CU x 4096 flop/clk x 2.4 GHz, dense
 WEIGHT_BYTES = 0.625            # per weight: 0.5 code + 1/16 scale + 1/16 offset
+MX_WEIGHT_BYTES = 0.53125       # MXFP4 variant: 0.5 code + 1/32 E8M0 scale
 
 
 def log(*a):
@@ -57,6 +60,8 @@ def parse():
     ap.add_argument("--flowkv", type=int, default=1,
                     help="also time FlowKV decode attention over every layer at --context positions")
     ap.add_argument("--context", type=int, default=32768, help="decode position + 1 for the FlowKV timing")
+    ap.add_argument("--mx", type=int, default=1,
+                    help="also time the decode and prefill steps over MXFP4-variant weights")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="run one eager decode step, one prefill step and a 1 GiB device copy (for rocprofv3 "
                          "counter passes), then exit")
@@ -65,9 +70,10 @@ def parse():
     return ap.parse_args()
 
 
-def build_weights(model, cfg, seed, mode, q4, torch):
-    """Generate, pack (q4nx_pack) and upload every projection's weights."""
-    from workloads import gen_weights
+def build_weights(model, cfg, seed, mode, q4, torch, mx=False):
+    """Generate, pack (q4nx_pack, or q4nx_mx_pack for the MXFP4 variant) and
+    upload every projection's weights."""
+    from workloads import gen_weights, gen_mx_weights
     L = model["layers"]
     tasks = [(l, p, N, K) for l in range(L) for p, (_, N, K) in enumerate(model["proj"])]
     if cfg.get("lm_head"):
@@ -75,6 +81,8 @@ def build_weights(model, cfg, seed, mode, q4, torch):
 
     def work(t):
         l, p, N, K = t
+        if mx:
+            return q4.q4nx_mx_pack(*gen_mx_weights(N, K, seed=seed, layer=l, proj=p))
         codes, s, o = gen_weights(N, K, seed=seed, layer=l, proj=p, offset_mode=mode)
         return q4.q4nx_pack(codes, s, o)
 
@@ -85,34 +93,38 @@ def build_weights(model, cfg, seed, mode, q4, torch):
         for i, (t, blob) in enumerate(zip(tasks, ex.map(work, tasks))):
             out[(t[0], t[1])] = torch.from_numpy(blob).cuda()
             if (i + 1) % 50 == 0 or i + 1 == len(tasks):
-                log(f"weights {i + 1}/{len(tasks)} packed+uploaded ({time.time() - t0:.0f}s)")
+                log(f"{'MXFP4 ' if mx else ''}weights {i + 1}/{len(tasks)} packed+uploaded ({time.time() - t0:.0f}s)")
     return out
 
 
 class Step:
     """Prebuilt C-ABI calls of one step (pointers marshalled once)."""
 
-    def __init__(self, q4, stream):
+    def __init__(self, q4, stream, mx=False):
         self.q4 = q4
         self.s = ctypes.c_void_p(stream)
         self.calls = []
         self.keep = []
+        # weight format of the packed launches: Q4NX or the MXFP4 variant
+        self.size = q4.q4nx_mx_packed_size if mx else q4.q4nx_packed_size
+        self.gemv_fn = q4.lib.q4nx_mx_gemv_batched if mx else q4.lib.q4nx_gemv_batched
+        self.gemm_fn = q4.lib.q4nx_mx_gemm if mx else q4.lib.q4nx_gemm
 
     def gemv_batched(self, items, ydt):
         arr = (self.q4.q4nx_gemv_desc * len(items))()
         for i, (blob, x, y, N, K) in enumerate(items):
-            self.q4._need(blob, self.q4.q4nx_packed_size(N, K), "blob")
+            self.q4._need(blob, self.size(N, K), "blob")
             self.q4._need(x, 2 * K, "x")
             self.q4._need(y, N * y.element_size(), "y")
             arr[i] = self.q4.q4nx_gemv_desc(blob.data_ptr(), x.data_ptr(), y.data_ptr(), N, K)
         self.keep.append(arr)
-        self.calls.append((self.q4.lib.q4nx_gemv_batched, (arr, len(items), ydt, self.s)))
+        self.calls.append((self.gemv_fn, (arr, len(items), ydt, self.s)))
 
     def gemm(self, M, N, K, X, blob, Y, ydt):
-        self.q4._need(blob, self.q4.q4nx_packed_size(N, K), "blob")
+        self.q4._need(blob, self.size(N, K), "blob")
         self.q4._need(X, 2 * M * K, "X")
         self.q4._need(Y, M * N * Y.element_size(), "Y")
-        self.calls.append((self.q4.lib.q4nx_gemm, (M, N, K, X.data_ptr(), blob.data_ptr(), Y.data_ptr(), ydt, self.s)))
+        self.calls.append((self.gemm_fn, (M, N, K, X.data_ptr(), blob.data_ptr(), Y.data_ptr(), ydt, self.s)))
 
     def dequant_bf16(self, blob, N, K, W):
         self.q4._need(blob, self.q4.q4nx_packed_size(N, K), "blob")
@@ -345,18 +357,24 @@ def main():
                 xs[(l, p)] = torch.from_numpy(gen_activations(K, seed=args.seed, layer=l, proj=p).view("int16")).cuda()
                 ys[(l, p)] = torch.empty(N, dtype=torch.float32, device="cuda")
                 dec_bytes += N * K * WEIGHT_BYTES
-        for l in range(L):
-            it = lambda p: (weights[(l, p)], xs[(l, p)], ys[(l, p)], model["proj"][p][1], model["proj"][p][2])
-            dec.gemv_batched([it(0), it(1), it(2)], F32)   # q, k, v
-            dec.gemv_batched([it(3)], F32)                 # o
-            dec.gemv_batched([it(4), it(5)], F32)          # gate, up
-            dec.gemv_batched([it(6)], F32)                 # down
         if cfg.get("lm_head"):
             _, N, K = model["lm_head"]
-            x = torch.from_numpy(gen_activations(K, seed=args.seed, layer=L, proj=7).view("int16")).cuda()
-            y = torch.empty(N, dtype=torch.float32, device="cuda")
-            dec.gemv_batched([(weights[(L, 7)], x, y, N, K)], F32)
+            xs[(L, 7)] = torch.from_numpy(gen_activations(K, seed=args.seed, layer=L, proj=7).view("int16")).cuda()
+            ys[(L, 7)] = torch.empty(N, dtype=torch.float32, device="cuda")
             dec_bytes += N * K * WEIGHT_BYTES
+
+        def decode_calls(step, wts):
+            for l in range(L):
+                it = lambda p: (wts[(l, p)], xs[(l, p)], ys[(l, p)], model["proj"][p][1], model["proj"][p][2])
+                step.gemv_batched([it(0), it(1), it(2)], F32)   # q, k, v
+                step.gemv_batched([it(3)], F32)                 # o
+                step.gemv_batched([it(4), it(5)], F32)          # gate, up
+                step.gemv_batched([it(6)], F32)                 # down
+            if cfg.get("lm_head"):
+                _, N, K = model["lm_head"]
+                step.gemv_batched([(wts[(L, 7)], xs[(L, 7)], ys[(L, 7)], N, K)], F32)
+
+        decode_calls(dec, weights)
         dec_launches = len(dec.calls)
 
     # ---------------------------------------------------------------- prefill
@@ -376,8 +394,22 @@ def main():
                 two.dequant_bf16(weights[(l, p)], N, K, Wtmp)
                 two.gemm_bf16(M_pre, N, K, Xs[(l, p)], Wtmp, Ys[p], F32)
                 pre_flops += 2.0 * M_pre * N * K
+    # MXFP4 variant: the same steps over MXFP4-variant weights (same
+    # activations and outputs).
+    mdec = Step(q4, stream.cuda_stream, mx=True)
+    mpre = Step(q4, stream.cuda_stream, mx=True)
+    mweights = None
+    if args.mx and not args.pmc_pass:
+        mweights = build_weights(model, cfg, args.seed, args.offset_mode, q4, torch, mx=True)
+        if do_decode:
+            decode_calls(mdec, mweights)
+        if do_prefill:
+            for l in range(L):
+                for p, (_, N, K) in enumerate(model["proj"]):
+                    mpre.gemm(M_pre, N, K, Xs[(l, p)], mweights[(l, p)], Ys[p], F32)
     torch.cuda.synchronize()
-    log(f"inputs resident: {sum(t.numel() for t in weights.values()) / 1e9:.2f} GB of packed weights")
+    log(f"inputs resident: {sum(t.numel() for t in weights.values()) / 1e9:.2f} GB of packed weights"
+        + (f" + {sum(t.numel() for t in mweights.values()) / 1e9:.2f} GB MXFP4-variant" if mweights else ""))
 
     if args.pmc_pass:
         # Exactly one step of each kind, then the calibration copy as the last dispatch.
@@ -399,16 +431,20 @@ def main():
     torch.cuda.synchronize()
     log("warmup done")
 
-    decode_fn = dec.run
-    graph_info = None
-    if do_decode and args.decode_graph:
-        # Capture the decode step once and replay it: no per-launch host cost.
-        # Every replay is checked bit for bit against the eager result (the
-        # kernels are deterministic), with eager work between replays.
+    graphs = []
+
+    def graph_of(step):
+        """Capture a decode step once and replay it (no per-launch host cost).
+        Every replay is checked bit for bit against the eager result (the
+        kernels are deterministic), with eager work between replays; on a
+        mismatch the eager launches are timed instead."""
+        step.run()
+        torch.cuda.synchronize()
         ref = [y.clone() for y in ys.values()]
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g, stream=stream):
-            dec.run()
+            step.run()
+        graphs.append(g)
         ok = True
         for _ in range(3):
             for y in ys.values():
@@ -416,16 +452,21 @@ def main():
             g.replay()
             torch.cuda.synchronize()
             ok = ok and all(torch.equal(a.view(torch.int32), b.view(torch.int32)) for a, b in zip(ys.values(), ref))
-            dec.run()
+            step.run()
             torch.cuda.synchronize()
-        graph_info = {"replays_checked": 3, "bitwise_equal_to_eager": bool(ok)}
-        if ok:
-            decode_fn = g.replay
-        else:
+        info = {"replays_checked": 3, "bitwise_equal_to_eager": bool(ok)}
+        fn = g.replay if ok else step.run
+        if not ok:
             log("graph replay differs from eager: timing eager launches")
         for _ in range(args.warmup):
-            decode_fn()
+            fn()
         torch.cuda.synchronize()
+        return fn, info
+
+    decode_fn = dec.run
+    graph_info = None
+    if do_decode and args.decode_graph:
+        decode_fn, graph_info = graph_of(dec)
 
     def timed(run_dec, run_pre, steps):
         ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
@@ -461,6 +502,31 @@ def main():
         _, N, K = model["lm_head"]
         alg_dec += N * K * WEIGHT_BYTES + 2 * K + 4 * N
     alg_pre = sum(2 * M_pre * K + N * K * WEIGHT_BYTES + 4 * M_pre * N for _, N, K in model["proj"]) * L if do_prefill else 0
+    mx = None
+    if mweights is not None:
+        mx = {"what": "the same decode and prefill steps over MXFP4-variant weights (FP4 E2M1 codes, one E8M0 "
+                      "scale per 32 weights; q4nx_mx_gemv_batched / q4nx_mx_gemm)"}
+        if do_decode:
+            mdec_fn, minfo = graph_of(mdec) if args.decode_graph else (mdec.run, None)
+            mdec_ms, _, _ = timed(mdec_fn, lambda: None, args.steps)
+            mbytes = dec_bytes / WEIGHT_BYTES * MX_WEIGHT_BYTES
+            t = mean(mdec_ms)
+            mx["decode"] = {"ms": round(t, 4), "ms_min": round(min(mdec_ms), 4), "weight_GB": round(mbytes / 1e9, 4),
+                            "GB_per_s": round(mbytes / (t * 1e-3) / 1e9, 2),
+                            "frac_hbm": round(mbytes / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                            "launches": len(mdec.calls), "graph_check": minfo,
+                            "bytes": "0.53125 B per weight (FP4 code + E8M0 scale per 32)"}
+        if do_prefill:
+            for _ in range(args.warmup):
+                mpre.run()
+            _, mpre_ms, _ = timed(lambda: None, mpre.run, args.steps)
+            t = mean(mpre_ms)
+            mx["prefill"] = {"ms": round(t, 4), "ms_min": round(min(mpre_ms), 4), "M": M_pre,
+                             "TFLOP_per_s": round(pre_flops / (t * 1e-3) / 1e12, 2),
+                             "frac_mfma": round(pre_flops / (t * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+                             "launches": len(mpre.calls)}
+
+
     quant = None
     if args.quantize:
         # The offline conversion on the GPU: one float32 matrix of the largest
@@ -584,6 +650,8 @@ def main():
              "algorithmic_bytes": round(alg_dec)}
         result["roofline" if not do_prefill else "roofline_gemv"] = r
 
+    if mx:
+        result["mxfp4"] = mx
     if quant:
         result["quantize"] = quant
     if fkv:

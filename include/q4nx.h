@@ -248,6 +248,44 @@ q4nx_status q4nx_flowkv_decode(const uint16_t* d_q, const uint16_t* d_k, const u
                                int64_t d, int64_t L, int64_t t, int64_t window, float scale, void* d_o,
                                q4nx_dtype o_dtype, void* d_work, size_t work_bytes, hipStream_t stream);
 
+/*
+ * MXFP4 variant of the Q4NX block (the paper notes that Q4NX can be extended
+ * to MXFP4, Sec. 3.1.1; element and scale encodings from the OCP Microscaling
+ * (MX) specification v1.0): the same 32 x 256 blocks, strip-major order,
+ * nibble layout and groups of 32 as Q4NX, with FP4 E2M1 codes (values 0, 0.5,
+ * 1, 1.5, 2, 3, 4, 6, code bit 3 = sign) and one E8M0 scale byte per group,
+ * X = 2^(e - 127), at index 8r + g after the codes -- 4352 bytes per block;
+ * no offset.  w = X * fp4(q), exact in float32 and bf16.  Value domain of the
+ * scales: e in [27, 227]; padding is code 0 with scale byte 127.
+ */
+size_t q4nx_mx_packed_size(int64_t N, int64_t K);  /* ceil(N/32)*ceil(K/256)*4352, 0 if invalid */
+
+/* Host, synchronous: codes [N][K] (0..15) and E8M0 scales [N][K/32] -> blob.
+ * Errors as q4nx_pack (a scale outside [27, 227] is Q4NX_ERR_INVALID_ARG). */
+q4nx_status q4nx_mx_pack(const uint8_t* codes, const uint8_t* scales, int64_t N, int64_t K, void* blob,
+                         size_t blob_bytes);
+
+/* Host, synchronous: the inverse of q4nx_mx_pack. */
+q4nx_status q4nx_mx_unpack(const void* blob, size_t blob_bytes, int64_t N, int64_t K, uint8_t* codes,
+                           uint8_t* scales);
+
+/* Device: q4nx_dequant for an MXFP4-variant blob (exact values; bf16 exact too). */
+q4nx_status q4nx_mx_dequant(const void* d_blob, int64_t N, int64_t K, void* d_W, q4nx_dtype w_dtype,
+                            hipStream_t stream);
+
+/* Device: q4nx_gemv for an MXFP4-variant blob: y[n] = sum_k w[n][k] x[k] with the
+ * same accumulation contract (float32, deterministic). */
+q4nx_status q4nx_mx_gemv(const void* d_blob, const uint16_t* d_x, void* d_y, q4nx_dtype y_dtype, int64_t N,
+                         int64_t K, hipStream_t stream);
+
+/* Device: q4nx_gemv_batched for MXFP4-variant blobs (every descriptor's blob is one). */
+q4nx_status q4nx_mx_gemv_batched(const q4nx_gemv_desc* descs, int32_t count, q4nx_dtype y_dtype,
+                                 hipStream_t stream);
+
+/* Device: q4nx_gemm for an MXFP4-variant blob (the bf16 weights are exact). */
+q4nx_status q4nx_mx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_blob, void* d_Y,
+                         q4nx_dtype y_dtype, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* q4nx_status_str(q4nx_status status);
 

@@ -31,7 +31,8 @@ Q4NX_MAX_BATCH = 8
 
 EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_quantize", "q4nx_dequant", "q4nx_gemv",
             "q4nx_gemv_batched", "q4nx_gemm", "q4nx_gemm_bf16", "q4nx_flowkv_workspace_size",
-            "q4nx_flowkv_decode", "q4nx_status_str", "q4nx_last_error"]
+            "q4nx_flowkv_decode", "q4nx_mx_packed_size", "q4nx_mx_pack", "q4nx_mx_unpack", "q4nx_mx_dequant",
+            "q4nx_mx_gemv", "q4nx_mx_gemv_batched", "q4nx_mx_gemm", "q4nx_status_str", "q4nx_last_error"]
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2602_06063_amd/build.py`")
@@ -77,6 +78,20 @@ lib.q4nx_flowkv_workspace_size.restype = _sz
 lib.q4nx_flowkv_decode.argtypes = [_vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, ctypes.c_float, _vp,
                                    ctypes.c_int, _vp, _sz, _vp]
 lib.q4nx_flowkv_decode.restype = ctypes.c_int
+lib.q4nx_mx_packed_size.argtypes = [_i64, _i64]
+lib.q4nx_mx_packed_size.restype = _sz
+lib.q4nx_mx_pack.argtypes = [_vp, _vp, _i64, _i64, _vp, _sz]
+lib.q4nx_mx_pack.restype = ctypes.c_int
+lib.q4nx_mx_unpack.argtypes = [_vp, _sz, _i64, _i64, _vp, _vp]
+lib.q4nx_mx_unpack.restype = ctypes.c_int
+lib.q4nx_mx_dequant.argtypes = [_vp, _i64, _i64, _vp, ctypes.c_int, _vp]
+lib.q4nx_mx_dequant.restype = ctypes.c_int
+lib.q4nx_mx_gemv.argtypes = [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _vp]
+lib.q4nx_mx_gemv.restype = ctypes.c_int
+lib.q4nx_mx_gemv_batched.argtypes = [ctypes.POINTER(q4nx_gemv_desc), _i32, ctypes.c_int, _vp]
+lib.q4nx_mx_gemv_batched.restype = ctypes.c_int
+lib.q4nx_mx_gemm.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp]
+lib.q4nx_mx_gemm.restype = ctypes.c_int
 lib.q4nx_status_str.argtypes = [ctypes.c_int]
 lib.q4nx_status_str.restype = ctypes.c_char_p
 lib.q4nx_last_error.argtypes = []
@@ -118,6 +133,31 @@ def q4nx_pack(codes: np.ndarray, scales: np.ndarray, offsets: np.ndarray) -> np.
     _check(lib.q4nx_pack(_np_ptr(codes), _np_ptr(scales), _np_ptr(offsets), N, K, _np_ptr(blob), size),
            "q4nx_pack")
     return blob[:size]
+
+
+def q4nx_mx_packed_size(N: int, K: int) -> int:
+    return int(lib.q4nx_mx_packed_size(N, K))
+
+
+def q4nx_mx_pack(codes: np.ndarray, scales: np.ndarray) -> np.ndarray:
+    """codes u8[N][K] (FP4 E2M1), scales u8[N][K/32] (E8M0) -> MXFP4-variant blob u8."""
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    N, K = codes.shape
+    scales = np.ascontiguousarray(scales, dtype=np.uint8)
+    if scales.size != N * (K // 32):
+        raise ValueError("scales need N * K/32 entries")
+    size = q4nx_mx_packed_size(N, K)
+    blob = np.empty(max(size, 1), dtype=np.uint8)
+    _check(lib.q4nx_mx_pack(_np_ptr(codes), _np_ptr(scales), N, K, _np_ptr(blob), size), "q4nx_mx_pack")
+    return blob[:size]
+
+
+def q4nx_mx_unpack(blob: np.ndarray, N: int, K: int):
+    blob = np.ascontiguousarray(blob, dtype=np.uint8)
+    codes = np.empty((N, K), np.uint8)
+    scales = np.empty((N, max(K // 32, 1)), np.uint8)
+    _check(lib.q4nx_mx_unpack(_np_ptr(blob), blob.size, N, K, _np_ptr(codes), _np_ptr(scales)), "q4nx_mx_unpack")
+    return codes, scales
 
 
 def q4nx_unpack(blob: np.ndarray, N: int, K: int):
@@ -217,6 +257,46 @@ def q4nx_gemm_bf16(M: int, N: int, K: int, X, W, Y, stream=None):
     _need(Y, M * N * Y.element_size(), "Y")
     _check(lib.q4nx_gemm_bf16(M, N, K, _dptr(X), _dptr(W), _dptr(Y), _dtype_code(Y), _stream(stream)),
            "q4nx_gemm_bf16")
+
+
+def q4nx_mx_dequant(blob, N: int, K: int, W, stream=None):
+    """W[N][K] (float32 or bfloat16 tensor) <- X * fp4(q) of every weight of an MXFP4-variant blob."""
+    _need(blob, q4nx_mx_packed_size(N, K), "blob")
+    _need(W, N * K * W.element_size(), "W")
+    _check(lib.q4nx_mx_dequant(_dptr(blob), N, K, _dptr(W), _dtype_code(W), _stream(stream)), "q4nx_mx_dequant")
+
+
+def q4nx_mx_gemv(blob, x, y, N: int, K: int, stream=None):
+    """y[N] <- W x for an MXFP4-variant blob."""
+    _need(blob, q4nx_mx_packed_size(N, K), "blob")
+    _need(x, 2 * K, "x")
+    _need(y, N * y.element_size(), "y")
+    _check(lib.q4nx_mx_gemv(_dptr(blob), _dptr(x), _dptr(y), _dtype_code(y), N, K, _stream(stream)),
+           "q4nx_mx_gemv")
+
+
+def q4nx_mx_gemv_batched(items, stream=None):
+    """items: sequence of (blob, x, y, N, K) over MXFP4-variant blobs; all y share one dtype."""
+    items = list(items)
+    arr = (q4nx_gemv_desc * max(len(items), 1))()
+    for i, (blob, x, y, N, K) in enumerate(items):
+        _need(blob, q4nx_mx_packed_size(N, K), "blob")
+        _need(x, 2 * K, "x")
+        _need(y, N * y.element_size(), "y")
+        arr[i] = q4nx_gemv_desc(_dptr(blob), _dptr(x), _dptr(y), N, K)
+    ydt = _dtype_code(items[0][2]) if items else Q4NX_F32
+    if any(_dtype_code(it[2]) != ydt for it in items):
+        raise ValueError("all outputs of a batch must share one dtype")
+    _check(lib.q4nx_mx_gemv_batched(arr, len(items), ydt, _stream(stream)), "q4nx_mx_gemv_batched")
+
+
+def q4nx_mx_gemm(M: int, N: int, K: int, X, blob, Y, stream=None):
+    """Y[M][N] <- X[M][K] W^T for an MXFP4-variant blob (W exact in bf16)."""
+    _need(blob, q4nx_mx_packed_size(N, K), "blob")
+    _need(X, 2 * M * K, "X")
+    _need(Y, M * N * Y.element_size(), "Y")
+    _check(lib.q4nx_mx_gemm(M, N, K, _dptr(X), _dptr(blob), _dptr(Y), _dtype_code(Y), _stream(stream)),
+           "q4nx_mx_gemm")
 
 
 def q4nx_flowkv_workspace_size(H: int, d: int, n_keys: int) -> int:

@@ -169,6 +169,93 @@ q4nx_status q4nx_unpack(const void* blob, size_t blob_bytes, int64_t N, int64_t 
   return Q4NX_OK;
 }
 
+size_t q4nx_mx_packed_size(int64_t N, int64_t K) {
+  if (N <= 0 || K <= 0 || K % kGroup != 0 || N > Q4NX_MAX_DIM || K > Q4NX_MAX_DIM) return 0;
+  return (size_t)ceil_div(N, kBlockRows) * (size_t)ceil_div(K, kBlockCols) * (size_t)kMxBlockBytes;
+}
+
+q4nx_status q4nx_mx_pack(const uint8_t* codes, const uint8_t* scales, int64_t N, int64_t K, void* blob,
+                         size_t blob_bytes) {
+  clear_error();
+  if (q4nx_status st = check_shape(N, K, "q4nx_mx_pack")) return st;
+  if (!codes || !scales || !blob) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_mx_pack: NULL pointer");
+  if (blob_bytes < q4nx_mx_packed_size(N, K))
+    return fail(Q4NX_ERR_BUFFER_TOO_SMALL, "q4nx_mx_pack: blob_bytes < q4nx_mx_packed_size(N, K)");
+  const int64_t G = K / kGroup;
+  // Validate everything before writing anything.
+  std::atomic<int64_t> bad_code{-1}, bad_val{-1};
+  parallel_for(N, 64, [&](int64_t r0, int64_t r1) {
+    for (int64_t r = r0; r < r1; ++r) {
+      const uint8_t* c = codes + r * K;
+      uint8_t acc = 0;
+      for (int64_t k = 0; k < K; ++k) acc |= c[k];
+      if (acc & 0xF0) {
+        for (int64_t k = 0; k < K; ++k)
+          if (c[k] > 15) { bad_code.store(r * K + k); break; }
+      }
+      for (int64_t g = 0; g < G; ++g)
+        if (scales[r * G + g] < kMxExpMin || scales[r * G + g] > kMxExpMax) {
+          bad_val.store(r * G + g);
+          break;
+        }
+    }
+  });
+  if (bad_code.load() >= 0)
+    return fail(Q4NX_ERR_INVALID_ARG, "q4nx_mx_pack: code > 15 at flat index " + std::to_string(bad_code.load()));
+  if (bad_val.load() >= 0)
+    return fail(Q4NX_ERR_INVALID_ARG, "q4nx_mx_pack: E8M0 scale outside [27, 227] at group index " +
+                                          std::to_string(bad_val.load()));
+  const int64_t NS = ceil_div(N, kBlockRows), KB = ceil_div(K, kBlockCols);
+  uint8_t* out = static_cast<uint8_t*>(blob);
+  parallel_for(NS, 4, [&](int64_t s0, int64_t s1) {
+    for (int64_t i = s0; i < s1; ++i) {
+      for (int64_t j = 0; j < KB; ++j) {
+        uint8_t* blk = out + (i * KB + j) * kMxBlockBytes;
+        std::memset(blk, 0, kCodeBytes);
+        std::memset(blk + kCodeBytes, kMxPadScale, kMxScaleBytes);
+        for (int r = 0; r < kBlockRows; ++r) {
+          const int64_t n = i * kBlockRows + r;
+          if (n >= N) break;
+          const int64_t k0 = j * kBlockCols;
+          const int64_t kn = std::min<int64_t>(kBlockCols, K - k0);
+          const uint8_t* src = codes + n * K + k0;
+          uint8_t* dst = blk + r * (kBlockCols / 2);
+          for (int64_t c = 0; c + 1 < kn; c += 2) dst[c / 2] = (uint8_t)(src[c] | (src[c + 1] << 4));
+          for (int64_t g = 0; g < kn / kGroup; ++g)
+            blk[kCodeBytes + r * kGroupsPerRow + g] = scales[n * G + k0 / kGroup + g];
+        }
+      }
+    }
+  });
+  return Q4NX_OK;
+}
+
+q4nx_status q4nx_mx_unpack(const void* blob, size_t blob_bytes, int64_t N, int64_t K, uint8_t* codes,
+                           uint8_t* scales) {
+  clear_error();
+  if (q4nx_status st = check_shape(N, K, "q4nx_mx_unpack")) return st;
+  if (!blob || !codes || !scales) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_mx_unpack: NULL pointer");
+  if (blob_bytes < q4nx_mx_packed_size(N, K))
+    return fail(Q4NX_ERR_BUFFER_TOO_SMALL, "q4nx_mx_unpack: blob_bytes < q4nx_mx_packed_size(N, K)");
+  const int64_t G = K / kGroup, KB = ceil_div(K, kBlockCols);
+  const uint8_t* in = static_cast<const uint8_t*>(blob);
+  parallel_for(N, 64, [&](int64_t r0, int64_t r1) {
+    for (int64_t n = r0; n < r1; ++n) {
+      const int64_t i = n / kBlockRows, r = n % kBlockRows;
+      for (int64_t k = 0; k < K; ++k) {
+        const uint8_t* blk = in + (i * KB + k / kBlockCols) * kMxBlockBytes;
+        const uint8_t b = blk[r * (kBlockCols / 2) + (k % kBlockCols) / 2];
+        codes[n * K + k] = (k & 1) ? (b >> 4) : (b & 0xF);
+      }
+      for (int64_t g = 0; g < G; ++g) {
+        const uint8_t* blk = in + (i * KB + (g * kGroup) / kBlockCols) * kMxBlockBytes;
+        scales[n * G + g] = blk[kCodeBytes + r * kGroupsPerRow + g % kGroupsPerRow];
+      }
+    }
+  });
+  return Q4NX_OK;
+}
+
 const char* q4nx_status_str(q4nx_status s) {
   switch (s) {
     case Q4NX_OK: return "ok";

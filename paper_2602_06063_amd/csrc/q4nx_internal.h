@@ -19,6 +19,14 @@ constexpr int kCodeBytes = kBlockRows * kBlockCols / 2;        // 4096
 constexpr int kScaleBytes = kBlockRows * kGroupsPerRow * 2;    // 512
 constexpr int kBlockBytes = kCodeBytes + 2 * kScaleBytes;      // 5120
 
+// MXFP4 variant of the block (OCP MX v1.0 element and scale encodings): the
+// same 32 x 256 codes as FP4 E2M1 values, one E8M0 scale byte per group,
+// no offset.
+constexpr int kMxScaleBytes = kBlockRows * kGroupsPerRow;      // 256
+constexpr int kMxBlockBytes = kCodeBytes + kMxScaleBytes;      // 4352
+constexpr int kMxExpMin = 27, kMxExpMax = 227;                 // accepted scales 2^-100 .. 2^100
+constexpr uint8_t kMxPadScale = 127;                           // scale 1 in padded groups
+
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Records a detail message for q4nx_last_error() and returns `st`.

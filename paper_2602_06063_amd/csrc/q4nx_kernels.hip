@@ -1,7 +1,8 @@
 // Device half of libq4nx for gfx950: the Q4NX dequantization kernel
 // (Sec. 3.1.1), the fused dequant mat-vec of the decode phase (FusedDQP,
 // Sec. 3.2.1, Eq. 14/15) and the fused dequant matrix product of the prefill
-// phase (Sec. 3.1.2), with their C-ABI launchers.
+// phase (Sec. 3.1.2), with their C-ABI launchers -- for Q4NX blocks and for
+// the MXFP4 variant of the block (FP4 E2M1 codes, one E8M0 scale per group).
 //
 // Common lane mapping inside a 32 x 256 block: a 16-byte load by lane l at
 // byte 1024t + 16l of the block holds the 32 codes of one quantization group,
@@ -115,6 +116,60 @@ __device__ __forceinline__ float eq3(float q_scaled, float d_times_512, float m)
   return fmaf(q_scaled, d_times_512, m);
 }
 
+// ---- MXFP4 variant of the block --------------------------------------------
+// Codes are FP4 E2M1 values and each group has one E8M0 scale byte e,
+// X = 2^(e-127) (OCP MX v1.0).  gfx950 converts one code byte (low nibble =
+// the even column) into two bf16 or float32 values times a float32 scale in
+// one instruction; an FP4 value times a power of two in [2^-100, 2^100] is
+// exact in both types.  Shifted into the float32 exponent field, e is X
+// itself (e = 0, what a load past the end of a tile returns, gives +0).
+__device__ __forceinline__ float e8m0_f32(uint32_t e) { return __uint_as_float(e << 23); }
+
+__device__ __forceinline__ uint32_t load_u8(const uint8_t* p) { return (uint32_t)__builtin_nontemporal_load(p); }
+
+template <int BYTE>
+__device__ __forceinline__ uint32_t fp4x2_bf16(uint32_t codes, float scale) {
+  return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(codes, scale, BYTE));
+}
+
+// 8 weights (one 32-bit word of codes) times X, as bf16 pairs in column order.
+__device__ __forceinline__ u32x4 mx8_bf16(uint32_t codes, float X) {
+  u32x4 o;
+  o[0] = fp4x2_bf16<0>(codes, X);
+  o[1] = fp4x2_bf16<1>(codes, X);
+  o[2] = fp4x2_bf16<2>(codes, X);
+  o[3] = fp4x2_bf16<3>(codes, X);
+  return o;
+}
+
+// sum_i fp4(q_i) * x_i over one group (one 16-byte word of codes), x given as
+// 16 bf16 pairs in natural column order.  The products are exact; v_dot2 adds
+// two of them to the float32 accumulator.
+__device__ __forceinline__ float group_dot_mx(u32x4 q, const uint32_t (&xp)[16]) {
+  float a = 0.0f, b = 0.0f;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const uint32_t w = q[u];
+    a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, fp4x2_bf16<0>(w, 1.0f)),
+                                        __builtin_bit_cast(bf16x2, xp[4 * u + 0]), a, false);
+    b = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, fp4x2_bf16<1>(w, 1.0f)),
+                                        __builtin_bit_cast(bf16x2, xp[4 * u + 1]), b, false);
+    a = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, fp4x2_bf16<2>(w, 1.0f)),
+                                        __builtin_bit_cast(bf16x2, xp[4 * u + 2]), a, false);
+    b = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, fp4x2_bf16<3>(w, 1.0f)),
+                                        __builtin_bit_cast(bf16x2, xp[4 * u + 3]), b, false);
+  }
+  return a + b;
+}
+
+// Weight operand of the matrix kernels: a Q4NX blob, an MXFP4-variant blob or
+// a plain bf16 matrix [N][K].
+enum WFmt : int { kWBf16 = 0, kWQ4NX = 1, kWMX = 2 };
+template <int F>
+constexpr int wblock_bytes() {
+  return F == kWMX ? kMxBlockBytes : kBlockBytes;
+}
+
 // ---------------------------------------------------------------------------
 // q4nx_dequant: Eq. 3 for every weight, written row-major [N][K]
 // ---------------------------------------------------------------------------
@@ -157,6 +212,41 @@ __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict_
       for (int v = 0; v < 8; ++v) {
         f32x4 o = {f[4 * v + 0], f[4 * v + 1], f[4 * v + 2], f[4 * v + 3]};
         __builtin_nontemporal_store(o, out + v);
+      }
+    }
+  }
+}
+
+// q4nx_mx_dequant: w = X * fp4(q) for every weight of an MXFP4-variant blob,
+// with the lane mapping of dequant_kernel.
+__global__ __launch_bounds__(256) void mx_dequant_kernel(const uint8_t* __restrict__ blob, int64_t N, int64_t K,
+                                                         int64_t KB, int64_t nblocks, void* __restrict__ W,
+                                                         int w_bf16) {
+  const int t = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = 8 * t + (lane >> 3), c = lane & 7;
+  for (int64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
+    const int64_t i = b / KB, j = b - i * KB;
+    const int64_t n = i * kBlockRows + r;
+    const int64_t k0 = j * kBlockCols + kGroup * c;
+    if (n >= N || k0 >= K) continue;
+    const uint8_t* blk = blob + b * kMxBlockBytes;
+    const u32x4 q = load_codes(blk + 1024 * t + 16 * lane);
+    const float X = e8m0_f32(load_u8(blk + kCodeBytes + 64 * t + lane));
+    if (w_bf16) {
+      u32x4* out = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(W) + n * K + k0);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) __builtin_nontemporal_store(mx8_bf16(q[v], X), out + v);
+    } else {
+      f32x4* out = reinterpret_cast<f32x4*>(static_cast<float*>(W) + n * K + k0);
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const uint32_t w = q[v];
+        const f32x2 a = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, X, 0);
+        const f32x2 b = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, X, 1);
+        const f32x2 e = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, X, 2);
+        const f32x2 g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, X, 3);
+        __builtin_nontemporal_store((f32x4){a[0], a[1], b[0], b[1]}, out + 2 * v);
+        __builtin_nontemporal_store((f32x4){e[0], e[1], g[0], g[1]}, out + 2 * v + 1);
       }
     }
   }
@@ -274,6 +364,8 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
 // for a given launch (results are reproducible call to call); it depends on
 // the wave count W, which is chosen for the launch as a whole.
 // Each wave prefetches its next block while computing the current one.
+// For the MXFP4 variant the per-group term is X_g * (sum_{k in g} fp4(q_k) x_k)
+// (no offset), with x staged in natural column order.
 constexpr int kGemvMaxWaves = 16;
 constexpr int kGemvChunkBlocks = 48;                    // x staged 48 x 256 columns at a time
 constexpr int kGroupPadDw = 20;  // dwords per staged group (16 bf16 pairs + 4 pad: conflict-free reads)
@@ -302,14 +394,15 @@ struct GemvArgs {
   int pad;
 };
 
-// Registers of one in-flight block: TQ row octets of codes, scales, offsets.
+// Registers of one in-flight block: TQ row octets of codes, scales, offsets
+// (E8M0 scale bytes and no offsets for the MXFP4 variant).
 template <int TQ>
 struct GemvSlot {
   u32x4 q[TQ];
   uint32_t s[TQ], m[TQ];
 };
 
-// Buffer descriptor over one chunk of one strip (at most 48 blocks = 240 KiB,
+// Buffer descriptor over one chunk of one strip (at most 48 blocks <= 240 KiB,
 // so every offset fits the 32-bit descriptor range); raw, stride 0.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t chunk_rsrc(const uint8_t* base, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), (short)0, bytes, 0x00020000);
@@ -321,19 +414,23 @@ constexpr int kNtLoad = 2;
 // Loads row octets t0..t0+TQ-1 of block `jj` of the chunk.  Every lane loads
 // (all addresses lie inside the chunk); the caller skips blocks past the end
 // with a wave-uniform branch.
-template <int TQ>
+template <int TQ, int F>
 __device__ __forceinline__ void gemv_load(__amdgpu_buffer_rsrc_t rs, int jj, int t0, int lane, GemvSlot<TQ>& R) {
-  const int boff = jj * kBlockBytes;
+  const int boff = jj * wblock_bytes<F>();
 #pragma unroll
   for (int t = 0; t < TQ; ++t) {
     const int tt = t0 + t;
     R.q[t] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, 16 * lane, boff + 1024 * tt, kNtLoad));
-    R.s[t] = __builtin_amdgcn_raw_buffer_load_b16(rs, 2 * lane, boff + kCodeBytes + 128 * tt, kNtLoad);
-    R.m[t] = __builtin_amdgcn_raw_buffer_load_b16(rs, 2 * lane, boff + kCodeBytes + kScaleBytes + 128 * tt, kNtLoad);
+    if constexpr (F == kWMX) {
+      R.s[t] = __builtin_amdgcn_raw_buffer_load_b8(rs, lane, boff + kCodeBytes + 64 * tt, kNtLoad);
+    } else {
+      R.s[t] = __builtin_amdgcn_raw_buffer_load_b16(rs, 2 * lane, boff + kCodeBytes + 128 * tt, kNtLoad);
+      R.m[t] = __builtin_amdgcn_raw_buffer_load_b16(rs, 2 * lane, boff + kCodeBytes + kScaleBytes + 128 * tt, kNtLoad);
+    }
   }
 }
 
-template <int TQ>
+template <int TQ, int F>
 __device__ __forceinline__ void gemv_compute(const GemvSlot<TQ>& R, bool gvalid, const uint32_t* __restrict__ xg,
                                              float S, float (&acc)[4]) {
   uint32_t xp[16];
@@ -344,6 +441,14 @@ __device__ __forceinline__ void gemv_compute(const GemvSlot<TQ>& R, bool gvalid,
     xp[4 * v + 1] = xv[1];
     xp[4 * v + 2] = xv[2];
     xp[4 * v + 3] = xv[3];
+  }
+  if constexpr (F == kWMX) {
+#pragma unroll
+    for (int t = 0; t < TQ; ++t) {
+      const float dot = group_dot_mx(R.q[t], xp);
+      acc[t] = fmaf(gvalid ? e8m0_f32(R.s[t]) : 0.0f, dot, acc[t]);
+    }
+    return;
   }
 #pragma unroll
   for (int t = 0; t < TQ; ++t) {
@@ -356,8 +461,9 @@ __device__ __forceinline__ void gemv_compute(const GemvSlot<TQ>& R, bool gvalid,
   }
 }
 
-template <int TQ, int D>
+template <int TQ, int D, int F>
 __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs args) {
+  constexpr int kBytes = wblock_bytes<F>();
   // Dynamic LDS: red[16*32] | ssum[chunk*8] | xs[chunk*8*36], chunk = the
   // launch's largest staged block count (at most kGemvChunkBlocks).
   extern __shared__ __attribute__((aligned(16))) float lds[];
@@ -386,28 +492,33 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
   for (int rg = wg - J.wg_begin; rg < J.nrg; rg += J.nwg) {
     const int row0 = rg * 8 * TQ;
     const int strip = row0 >> 5, t0 = (row0 & 31) >> 3;
-    const uint8_t* sblob = J.blob + (size_t)strip * J.KB * kBlockBytes;
+    const uint8_t* sblob = J.blob + (size_t)strip * J.KB * kBytes;
     float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
 
     for (int ch = 0; ch < nchunks; ++ch) {
       const int jc0 = ch * CB;
       const int nb = min(CB, J.KB - jc0);
-      const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(sblob + (size_t)jc0 * kBlockBytes, nb * kBlockBytes);
+      const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(sblob + (size_t)jc0 * kBytes, nb * kBytes);
       const int kvalid = J.K - jc0 * kBlockCols;  // columns of this chunk inside K
       // The wave's first D blocks go in flight before the x staging.
       GemvSlot<TQ> buf[D];
 #pragma unroll
       for (int d = 0; d < D; ++d)
-        if (wave_on && w + d * W < nb) gemv_load<TQ>(rs, w + d * W, t0, lane, buf[d]);
+        if (wave_on && w + d * W < nb) gemv_load<TQ, F>(rs, w + d * W, t0, lane, buf[d]);
       if (staged != ch) {
         __syncthreads();  // every wave is done with the previous chunk
         // Thread e stages columns 8e..8e+7 as the four bf16 pairs
-        // (x0,x2) (x4,x6) (x1,x3) (x5,x7) and adds them to its group's sum.
+        // (x0,x2) (x4,x6) (x1,x3) (x5,x7) and adds them to its group's sum
+        // (MXFP4 variant: the pairs in natural order, no sum).
         const int kbeg = jc0 * kBlockCols;
         for (int e = threadIdx.x; e < nb * (kBlockCols / 8); e += nthreads) {
           const int k = kbeg + 8 * e;
           u32x4 v = (u32x4){0u, 0u, 0u, 0u};
           if (k < J.K) v = *reinterpret_cast<const u32x4*>(J.x + k);
+          if constexpr (F == kWMX) {
+            *reinterpret_cast<u32x4*>(xs + (e >> 2) * kGroupPadDw + 4 * (e & 3)) = v;
+            continue;
+          }
           const uint32_t p02 = (v[0] & 0xFFFFu) | (v[1] << 16), p46 = (v[2] & 0xFFFFu) | (v[3] << 16);
           const uint32_t p13 = (v[0] >> 16) | (v[1] & 0xFFFF0000u), p57 = (v[2] >> 16) | (v[3] & 0xFFFF0000u);
           const int g = e >> 2;
@@ -430,9 +541,10 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
           for (int d = 0; d < D; ++d) {
             const int jj = w + (i0 + d) * W;
             if (jj < nb) {
-              gemv_compute<TQ>(buf[d], jj * kBlockCols + kGroup * c < kvalid,
-                               xs + (jj * kGroupsPerRow + c) * kGroupPadDw, ssum[jj * kGroupsPerRow + c], acc);
-              if (jj + D * W < nb) gemv_load<TQ>(rs, jj + D * W, t0, lane, buf[d]);
+              gemv_compute<TQ, F>(buf[d], jj * kBlockCols + kGroup * c < kvalid,
+                                  xs + (jj * kGroupsPerRow + c) * kGroupPadDw,
+                                  F == kWMX ? 0.0f : ssum[jj * kGroupsPerRow + c], acc);
+              if (jj + D * W < nb) gemv_load<TQ, F>(rs, jj + D * W, t0, lane, buf[d]);
             }
           }
         }
@@ -477,7 +589,8 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
 // 72 elements (144 B) so that the 16-byte fragment reads of 8 consecutive
 // rows, and the 16-byte tile writes, hit distinct banks.  Each output is the
 // float32 sum of its MFMA chain over K in increasing order, so every kernel
-// and every tile shape gives the same bits.
+// and every tile shape gives the same bits.  MXFP4-variant weights take the
+// same path with the Eq. 3 step replaced by the exact FP4 x scale conversion.
 constexpr int kBK = 64;
 constexpr int kLdsStride = kBK + 8;  // bf16 elements per LDS row
 
@@ -536,7 +649,8 @@ __device__ __forceinline__ u32x4 dequant8_bf16(uint32_t codes, float d512, float
 // W are read through buffer descriptors limited to the tile's rows and strips;
 // in the last step of a K that is not a multiple of 64 the columns past K are
 // given an offset past the descriptor's end, which reads as zero -- code 0,
-// scale 0 and offset 0 give w = +0 -- so no mask is needed anywhere else.  X
+// scale 0 and offset 0 give w = +0 (code 0 with E8M0 byte 0 as well) -- so no
+// mask is needed anywhere else.  X
 // rows past M and W strips past the matrix are clamped to the last valid one;
 // their outputs are never stored.
 constexpr int kWideThreads = 256;
@@ -545,22 +659,23 @@ constexpr int64_t kWideMaxK = int64_t(1) << 22;               // 256 rows x K x 
 
 // Raw operands of one K step held by one thread.  X (and bf16 W): rows
 // tid/8 + 32i, columns 8(tid%8)..+7 of the step.  Packed W: codes, scale and
-// offset of group (row tid/2 + 128g, half tid%2 of the step).
-template <bool WQ4>
+// offset (no offset for the MXFP4 variant) of group (row tid/2 + 128g, half
+// tid%2 of the step).
+template <int WF>
 struct WideRegs {
   u32x4 x[8];
   u32x4 q[2];
   uint32_t s[2], m[2];
 };
 template <>
-struct WideRegs<false> {
+struct WideRegs<kWBf16> {
   u32x4 x[8];
   u32x4 w[8];
 };
 
-// WQ4: W is a packed Q4NX matrix (dequantized on the fly); otherwise W is
-// bf16 [N][K] and its tile is staged exactly like the X tile.
-template <bool KTAIL, bool WQ4>
+// WF: W is a packed Q4NX or MXFP4-variant matrix (dequantized on the fly), or
+// bf16 [N][K], whose tile is staged exactly like the X tile.
+template <bool KTAIL, int WF>
 __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* __restrict__ X,
                                                                const uint8_t* __restrict__ wsrc,
                                                                void* __restrict__ Y, int M, int N, int K, int ldy,
@@ -580,14 +695,17 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
   const int rows_x = min(256, M - m0);
   const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(X + (size_t)m0 * K), (short)0, rows_x * K * 2, 0x00020000);
+  constexpr bool WQ4 = WF != kWBf16;  // packed weights
+  constexpr int kBB = wblock_bytes<WF>();
   const int s0 = n0 >> 5, nst = min(8, NS - s0), rows_w = min(256, N - n0);
   const __amdgpu_buffer_rsrc_t rsw =
-      WQ4 ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wsrc + (size_t)s0 * KB * kBlockBytes), (short)0,
-                                              nst * KB * kBlockBytes, 0x00020000)
+      WQ4 ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wsrc + (size_t)s0 * KB * kBB), (short)0,
+                                              nst * KB * kBB, 0x00020000)
           : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wsrc + (size_t)n0 * K * 2), (short)0,
                                               rows_w * K * 2, 0x00020000);
   constexpr int kPastEnd = 0x7FFFFFF0;  // beyond every descriptor: loads return 0
-  constexpr int kLoads = WQ4 ? 14 : 16;  // global loads per thread and K step
+  // Global loads per thread and K step.
+  constexpr int kLoads = WF == kWQ4NX ? 14 : WF == kWMX ? 12 : 16;
 
   const int c8 = tid & 7, half = tid & 1;
   int vx[8];
@@ -599,8 +717,8 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
     for (int g = 0; g < 2; ++g) {
       const int r = (tid >> 1) + 128 * g;
       const int st = min(r >> 5, nst - 1), rr = r & 31;
-      vq[g] = st * KB * kBlockBytes + 128 * rr + 16 * half;
-      vs[g] = st * KB * kBlockBytes + kCodeBytes + 2 * (8 * rr + half);
+      vq[g] = st * KB * kBB + 128 * rr + 16 * half;
+      vs[g] = st * KB * kBB + kCodeBytes + (WF == kWMX ? 1 : 2) * (8 * rr + half);
     }
   } else {
 #pragma unroll
@@ -618,10 +736,10 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
 
   // Global loads of step t (clamped to the last step) into R, one of the
   // kLoads loads per call, so that they can be spread over MFMA slots.
-  auto load1 = [&](WideRegs<WQ4>& R, int t, int i) {
+  auto load1 = [&](WideRegs<WF>& R, int t, int i) {
     const int k0 = min(t, nsteps - 1) * kBK;
-    const int sq = (k0 >> 8) * kBlockBytes + 16 * ((k0 & 255) >> 5);
-    const int ss = (k0 >> 8) * kBlockBytes + 2 * ((k0 & 255) >> 5);
+    const int sq = (k0 >> 8) * kBB + 16 * ((k0 & 255) >> 5);
+    const int ss = (k0 >> 8) * kBB + (WF == kWMX ? 1 : 2) * ((k0 & 255) >> 5);
     const bool okx = !KTAIL || k0 + 8 * c8 < K;
     const bool okw = !KTAIL || k0 + kGroup * half < K;
     if (i < 8) {
@@ -644,7 +762,10 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
           u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsw, okw ? vq[g] + sq : kPastEnd, 0, kNtLoad));
     } else if (i < 12) {
       const int g = i - 10;
-      R.s[g] = __builtin_amdgcn_raw_buffer_load_b16(rsw, okw ? vs[g] + ss : kPastEnd, 0, kNtLoad);
+      if constexpr (WF == kWMX)
+        R.s[g] = __builtin_amdgcn_raw_buffer_load_b8(rsw, okw ? vs[g] + ss : kPastEnd, 0, kNtLoad);
+      else
+        R.s[g] = __builtin_amdgcn_raw_buffer_load_b16(rsw, okw ? vs[g] + ss : kPastEnd, 0, kNtLoad);
     } else {
       const int g = i - 12;
       R.m[g] = __builtin_amdgcn_raw_buffer_load_b16(rsw, okw ? vs[g] + ss + kScaleBytes : kPastEnd, 0, kNtLoad);
@@ -668,13 +789,25 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
     acc[i >> 2][i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[i >> 2], B[i & 3], acc[i >> 2][i & 3], 0, 0, 0);
   };
   // Dequantization of weight group g in 16 pieces: piece p handles a quarter
-  // of the 8 columns 8(p/4)..+7 (Eq. 3, as in dequant8_bf16).
+  // of the 8 columns 8(p/4)..+7 (Eq. 3, as in dequant8_bf16; for the MXFP4
+  // variant one FP4 x scale conversion of a code byte, as in mx8_bf16).
   uint32_t wlo = 0, whi = 0;
   float wd = 0.0f, wmo = 0.0f;
   f32x2 wa, we, wb, wg;
   u32x4 wo;
-  auto wpiece = [&](const WideRegs<WQ4>& R, int st, int g, int p) {
-    if constexpr (WQ4) {
+  auto wpiece = [&](const WideRegs<WF>& R, int st, int g, int p) {
+    if constexpr (WF == kWMX) {
+      const int u = p >> 2, qt = p & 3;
+      if (p == 0) wd = e8m0_f32(R.s[g]);
+      const uint32_t w = R.q[g][u];
+      if (qt == 0) wo[0] = fp4x2_bf16<0>(w, wd);
+      else if (qt == 1) wo[1] = fp4x2_bf16<1>(w, wd);
+      else if (qt == 2) wo[2] = fp4x2_bf16<2>(w, wd);
+      else {
+        wo[3] = fp4x2_bf16<3>(w, wd);
+        *reinterpret_cast<u32x4*>(ws_row(st, g) + 8 * u) = wo;
+      }
+    } else if constexpr (WQ4) {
     const int u = p >> 2, qt = p & 3;
     if (qt == 0) {
       if (u == 0) {
@@ -699,7 +832,7 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
     }
   };
   // bf16 W: chunk i of the thread's W rows, staged like X.
-  auto wchunk = [&](const WideRegs<WQ4>& R, int st, int i) {
+  auto wchunk = [&](const WideRegs<WF>& R, int st, int i) {
     if constexpr (!WQ4)
       *reinterpret_cast<u32x4*>(xs_row(st) + 2 * 256 * kLdsStride + 32 * i * kLdsStride) = R.w[i];
   };
@@ -707,7 +840,7 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
   // One K step: MFMAs of step s from stage s&1 while step s+1 (held in Rs) is
   // written to the other stage and step s+3 is loaded into Rs.
   bf16x8 A0[TI], B0[TJ], A1[TI], B1[TJ];
-  auto step = [&](int s, WideRegs<WQ4>& Rs) {
+  auto step = [&](int s, WideRegs<WF>& Rs) {
     const int cur = s & 1, nxt = cur ^ 1;
     uint16_t* xsn = xs_row(nxt);
 #pragma unroll
@@ -742,7 +875,7 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
     }
   };
 
-  WideRegs<WQ4> R0, R1;
+  WideRegs<WF> R0, R1;
 #pragma unroll
   for (int i = 0; i < kLoads; ++i) load1(R0, 0, i);
 #pragma unroll
@@ -751,7 +884,14 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
     uint16_t* xs = xs_row(0);
 #pragma unroll
     for (int i = 0; i < 8; ++i) *reinterpret_cast<u32x4*>(xs + 32 * i * kLdsStride) = R0.x[i];
-    if constexpr (WQ4) {
+    if constexpr (WF == kWMX) {
+#pragma unroll
+      for (int g = 0; g < 2; ++g) {
+        const float X = e8m0_f32(R0.s[g]);
+#pragma unroll
+        for (int u = 0; u < 4; ++u) *reinterpret_cast<u32x4*>(ws_row(0, g) + 8 * u) = mx8_bf16(R0.q[g][u], X);
+      }
+    } else if constexpr (WQ4) {
 #pragma unroll
       for (int g = 0; g < 2; ++g) {
         const float d512 = bf16_to_f32(R0.s[g]) * 512.0f, m = bf16_to_f32(R0.m[g]);
@@ -830,11 +970,12 @@ struct GemmRegs {
   u32x4 w[WC];
 };
 
-// WQ4: W is a packed Q4NX matrix (blob); otherwise W is bf16 [N][K].
-template <int BM, int BN, int WAVES_M, int WAVES_N, bool WQ4>
+// WF: W is a packed Q4NX or MXFP4-variant matrix (blob), or bf16 [N][K].
+template <int BM, int BN, int WAVES_M, int WAVES_N, int WF>
 __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
     const uint16_t* __restrict__ X, const uint8_t* __restrict__ blob, void* __restrict__ Y, int M, int N, int K,
     int ldy, int KB, int NS, int tiles_n, int y_bf16) {
+  constexpr bool WQ4 = WF != kWBf16;  // packed weights
   using C = GemmCfg<BM, BN, WAVES_M, WAVES_N>;
   using Regs = GemmRegs<C::kXChunks, WQ4 ? C::kWGroups : 1, WQ4 ? 1 : C::kWChunks>;
   const uint16_t* const Wb = reinterpret_cast<const uint16_t*>(blob);
@@ -884,10 +1025,14 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
       const int r = gi >> 1, gk = min(k0 + kGroup * (gi & 1), K - kGroup);
       const int gn = n0 + r, rr = gn & 31;
       const int j = gk >> 8, c = (gk & 255) >> 5;
-      const uint8_t* blk = blob + ((size_t)min(gn >> 5, NS - 1) * KB + j) * kBlockBytes;
+      const uint8_t* blk = blob + ((size_t)min(gn >> 5, NS - 1) * KB + j) * wblock_bytes<WF>();
       R.q[i] = load_codes(blk + 128 * rr + 16 * c);
-      R.s[i] = load_u16(blk + kCodeBytes + 2 * (8 * rr + c));
-      R.m[i] = load_u16(blk + kCodeBytes + kScaleBytes + 2 * (8 * rr + c));
+      if constexpr (WF == kWMX) {
+        R.s[i] = load_u8(blk + kCodeBytes + 8 * rr + c);
+      } else {
+        R.s[i] = load_u16(blk + kCodeBytes + 2 * (8 * rr + c));
+        R.m[i] = load_u16(blk + kCodeBytes + kScaleBytes + 2 * (8 * rr + c));
+      }
     }
   };
 
@@ -917,6 +1062,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
       if (C::kStepGroups % C::kThreads != 0 && gi >= C::kStepGroups) break;  // wave-uniform
       const bool ok = ((n0 + (gi >> 1)) >> 5) < NS && k0 + kGroup * (gi & 1) < K;
       const u32x4 q = ok ? R.q[i] : (u32x4){0u, 0u, 0u, 0u};
+      if constexpr (WF == kWMX) {
+        const float Xs = ok ? e8m0_f32(R.s[i]) : 0.0f;
+        u32x4* wd = reinterpret_cast<u32x4*>(ws + (gi >> 1) * kLdsStride + kGroup * (gi & 1));
+#pragma unroll
+        for (int v = 0; v < 4; ++v) wd[v] = mx8_bf16(q[v], Xs);
+        continue;
+      }
       const float d512 = ok ? bf16_to_f32(R.s[i]) * 512.0f : 0.0f, m = ok ? bf16_to_f32(R.m[i]) : 0.0f;
       u32x4* wd = reinterpret_cast<u32x4*>(ws + (gi >> 1) * kLdsStride + kGroup * (gi & 1));
 #pragma unroll
@@ -1068,13 +1220,13 @@ static int gemm_plan(int64_t M, int64_t N, int cus, GemmRegion (&plan)[2]) {
   return count;
 }
 
-template <int BM, int BN, int WAVES_M, int WAVES_N, bool WQ4>
+template <int BM, int BN, int WAVES_M, int WAVES_N, int WF>
 static q4nx_status launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* X, const void* blob, void* Y,
                                int64_t ldy, int y_bf16, hipStream_t stream) {
   using Cfg = GemmCfg<BM, BN, WAVES_M, WAVES_N>;
   const int64_t tiles_n = ceil_div(N, BN), tiles_m = ceil_div(M, BM);
   const size_t lds = sizeof(uint16_t) * Cfg::kLdsElems;
-  auto kern = gemm_kernel<BM, BN, WAVES_M, WAVES_N, WQ4>;
+  auto kern = gemm_kernel<BM, BN, WAVES_M, WAVES_N, WF>;
   static bool attr_set = false;  // LDS above 64 KiB must be requested once per kernel
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -1088,10 +1240,10 @@ static q4nx_status launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* 
   return Q4NX_OK;
 }
 
-template <bool KTAIL, bool WQ4>
+template <bool KTAIL, int WF>
 static q4nx_status launch_gemm256(int64_t M, int64_t N, int64_t K, const uint16_t* X, const void* blob, void* Y,
                                   int64_t ldy, int y_bf16, hipStream_t stream) {
-  auto kern = gemm256_kernel<KTAIL, WQ4>;
+  auto kern = gemm256_kernel<KTAIL, WF>;
   static bool attr_set = false;
   if (!attr_set) {
     if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -1109,29 +1261,30 @@ static q4nx_status launch_gemm256(int64_t M, int64_t N, int64_t K, const uint16_
 // One region of the output: X rows m0.., W rows n0.. (strips n0/32.. of a
 // packed matrix) and Y at (m0, n0) with row stride N, so each launch sees an
 // ordinary smaller problem.
-template <bool WQ4>
+template <int WF>
 static q4nx_status launch_region(const GemmRegion& r, int64_t N, int64_t K, const uint16_t* X, const void* w,
                                  void* Y, int y_bf16, hipStream_t stream) {
   const uint16_t* Xr = X + r.m0 * K;
-  const void* Wr = WQ4 ? static_cast<const void*>(static_cast<const uint8_t*>(w) +
-                                                  (r.n0 / kBlockRows) * ceil_div(K, kBlockCols) * kBlockBytes)
+  const void* Wr = WF != kWBf16
+                       ? static_cast<const void*>(static_cast<const uint8_t*>(w) +
+                                                  (r.n0 / kBlockRows) * ceil_div(K, kBlockCols) * wblock_bytes<WF>())
                        : static_cast<const void*>(static_cast<const uint16_t*>(w) + r.n0 * K);
   void* Yr = static_cast<uint8_t*>(Y) + (r.m0 * N + r.n0) * (y_bf16 ? 2 : 4);
   switch (r.tile) {
     case 0:
-      if (K >= kWideMaxK) return launch_gemm<256, 256, 2, 4, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
-      if (K % kBK != 0) return launch_gemm256<true, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
-      return launch_gemm256<false, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
-    case 1: return launch_gemm<256, 128, 4, 2, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
-    case 2: return launch_gemm<128, 128, 2, 4, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
-    default: return launch_gemm<128, 64, 2, 2, WQ4>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+      if (K >= kWideMaxK) return launch_gemm<256, 256, 2, 4, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+      if (K % kBK != 0) return launch_gemm256<true, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+      return launch_gemm256<false, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+    case 1: return launch_gemm<256, 128, 4, 2, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+    case 2: return launch_gemm<128, 128, 2, 4, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+    default: return launch_gemm<128, 64, 2, 2, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
   }
 }
 
 static q4nx_status check_launch(const char* fn);
 
-// Validation shared by q4nx_gemm and q4nx_gemm_bf16, then the planned launches.
-template <bool WQ4>
+// Validation shared by the matrix-product entry points, then the planned launches.
+template <int WF>
 static q4nx_status gemm_entry(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_W, void* d_Y,
                               q4nx_dtype y_dtype, hipStream_t stream, const char* fn) {
   clear_error();
@@ -1141,14 +1294,14 @@ static q4nx_status gemm_entry(int64_t M, int64_t N, int64_t K, const uint16_t* d
   if (y_dtype != Q4NX_F32 && y_dtype != Q4NX_BF16)
     return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": unknown y_dtype");
   if (!aligned(d_X, 16) || !aligned(d_W, 16) || !aligned(d_Y, 16))
-    return fail(Q4NX_ERR_ALIGNMENT, std::string(fn) + (WQ4 ? ": X, blob and Y need 16-byte alignment"
-                                                           : ": X, W and Y need 16-byte alignment"));
+    return fail(Q4NX_ERR_ALIGNMENT, std::string(fn) + (WF != kWBf16 ? ": X, blob and Y need 16-byte alignment"
+                                                                    : ": X, W and Y need 16-byte alignment"));
   if (M * N > (int64_t(1) << 40)) return fail(Q4NX_ERR_SHAPE, std::string(fn) + ": problem too large for one launch");
   GemmRegion plan[2];
   const int count = gemm_plan(M, N, device_cus(), plan);
   q4nx_status st = Q4NX_OK;
   for (int i = 0; i < count && st == Q4NX_OK; ++i)
-    st = launch_region<WQ4>(plan[i], N, K, d_X, d_W, d_Y, y_dtype == Q4NX_BF16, stream);
+    st = launch_region<WF>(plan[i], N, K, d_X, d_W, d_Y, y_dtype == Q4NX_BF16, stream);
   if (st != Q4NX_OK) return st;
   return check_launch(fn);
 }
@@ -1180,6 +1333,7 @@ static int gemv_waves(int64_t row_groups, int min_kb) {
   return w;
 }
 
+template <int F>
 static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtype y_dtype, hipStream_t stream,
                                const char* fn) {
   clear_error();
@@ -1229,10 +1383,34 @@ static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtyp
   const size_t lds = sizeof(float) * ((size_t)kRedFloats + (size_t)args.chunk_blocks * kGroupsPerRow * (1 + kGroupPadDw));
   const dim3 grid((unsigned)wg), block(64 * max_waves);
   switch (tq) {
-    case 4: hipLaunchKernelGGL((gemv_kernel<4, kGemvDepth4>), grid, block, lds, stream, args); break;
-    case 2: hipLaunchKernelGGL((gemv_kernel<2, kGemvDepth2>), grid, block, lds, stream, args); break;
-    default: hipLaunchKernelGGL((gemv_kernel<1, kGemvDepth1>), grid, block, lds, stream, args); break;
+    case 4: hipLaunchKernelGGL((gemv_kernel<4, kGemvDepth4, F>), grid, block, lds, stream, args); break;
+    case 2: hipLaunchKernelGGL((gemv_kernel<2, kGemvDepth2, F>), grid, block, lds, stream, args); break;
+    default: hipLaunchKernelGGL((gemv_kernel<1, kGemvDepth1, F>), grid, block, lds, stream, args); break;
   }
+  return check_launch(fn);
+}
+
+template <int F>
+static q4nx_status dequant_entry(const void* d_blob, int64_t N, int64_t K, void* d_W, q4nx_dtype w_dtype,
+                                 hipStream_t stream, const char* fn) {
+  clear_error();
+  if (q4nx_status st = check_shape(N, K, fn)) return st;
+  if (!d_blob || !d_W) return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": NULL pointer");
+  if (w_dtype != Q4NX_F32 && w_dtype != Q4NX_BF16)
+    return fail(Q4NX_ERR_INVALID_ARG, std::string(fn) + ": unknown w_dtype");
+  if (!aligned(d_blob, 16) || !aligned(d_W, 16))
+    return fail(Q4NX_ERR_ALIGNMENT, std::string(fn) + ": blob and W need 16-byte alignment");
+  const int64_t KB = ceil_div(K, kBlockCols);
+  const int64_t nblocks = ceil_div(N, kBlockRows) * KB;
+  const int64_t grid = std::min<int64_t>(nblocks, int64_t(1) << 20);
+  const uint8_t* blob = static_cast<const uint8_t*>(d_blob);
+  const int w_bf16 = (w_dtype == Q4NX_BF16);
+  if constexpr (F == kWMX)
+    hipLaunchKernelGGL(mx_dequant_kernel, dim3((unsigned)grid), dim3(256), 0, stream, blob, N, K, KB, nblocks, d_W,
+                       w_bf16);
+  else
+    hipLaunchKernelGGL(dequant_kernel, dim3((unsigned)grid), dim3(256), 0, stream, blob, N, K, KB, nblocks, d_W,
+                       w_bf16);
   return check_launch(fn);
 }
 
@@ -1244,19 +1422,12 @@ extern "C" {
 
 q4nx_status q4nx_dequant(const void* d_blob, int64_t N, int64_t K, void* d_W, q4nx_dtype w_dtype,
                          hipStream_t stream) {
-  clear_error();
-  if (q4nx_status st = check_shape(N, K, "q4nx_dequant")) return st;
-  if (!d_blob || !d_W) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_dequant: NULL pointer");
-  if (w_dtype != Q4NX_F32 && w_dtype != Q4NX_BF16)
-    return fail(Q4NX_ERR_INVALID_ARG, "q4nx_dequant: unknown w_dtype");
-  if (!aligned(d_blob, 16) || !aligned(d_W, 16))
-    return fail(Q4NX_ERR_ALIGNMENT, "q4nx_dequant: blob and W need 16-byte alignment");
-  const int64_t KB = ceil_div(K, kBlockCols);
-  const int64_t nblocks = ceil_div(N, kBlockRows) * KB;
-  const int64_t grid = std::min<int64_t>(nblocks, int64_t(1) << 20);
-  hipLaunchKernelGGL(dequant_kernel, dim3((unsigned)grid), dim3(256), 0, stream,
-                     static_cast<const uint8_t*>(d_blob), N, K, KB, nblocks, d_W, (int)(w_dtype == Q4NX_BF16));
-  return check_launch("q4nx_dequant");
+  return dequant_entry<kWQ4NX>(d_blob, N, K, d_W, w_dtype, stream, "q4nx_dequant");
+}
+
+q4nx_status q4nx_mx_dequant(const void* d_blob, int64_t N, int64_t K, void* d_W, q4nx_dtype w_dtype,
+                            hipStream_t stream) {
+  return dequant_entry<kWMX>(d_blob, N, K, d_W, w_dtype, stream, "q4nx_mx_dequant");
 }
 
 q4nx_status q4nx_quantize(const float* d_W, int64_t N, int64_t K, void* d_blob, hipStream_t stream) {
@@ -1276,22 +1447,38 @@ q4nx_status q4nx_quantize(const float* d_W, int64_t N, int64_t K, void* d_blob, 
 q4nx_status q4nx_gemv(const void* d_blob, const uint16_t* d_x, void* d_y, q4nx_dtype y_dtype, int64_t N,
                       int64_t K, hipStream_t stream) {
   q4nx_gemv_desc d = {d_blob, d_x, d_y, N, K};
-  return gemv_launch(&d, 1, y_dtype, stream, "q4nx_gemv");
+  return gemv_launch<kWQ4NX>(&d, 1, y_dtype, stream, "q4nx_gemv");
 }
 
 q4nx_status q4nx_gemv_batched(const q4nx_gemv_desc* descs, int32_t count, q4nx_dtype y_dtype,
                               hipStream_t stream) {
-  return gemv_launch(descs, count, y_dtype, stream, "q4nx_gemv_batched");
+  return gemv_launch<kWQ4NX>(descs, count, y_dtype, stream, "q4nx_gemv_batched");
+}
+
+q4nx_status q4nx_mx_gemv(const void* d_blob, const uint16_t* d_x, void* d_y, q4nx_dtype y_dtype, int64_t N,
+                         int64_t K, hipStream_t stream) {
+  q4nx_gemv_desc d = {d_blob, d_x, d_y, N, K};
+  return gemv_launch<kWMX>(&d, 1, y_dtype, stream, "q4nx_mx_gemv");
+}
+
+q4nx_status q4nx_mx_gemv_batched(const q4nx_gemv_desc* descs, int32_t count, q4nx_dtype y_dtype,
+                                 hipStream_t stream) {
+  return gemv_launch<kWMX>(descs, count, y_dtype, stream, "q4nx_mx_gemv_batched");
 }
 
 q4nx_status q4nx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_blob, void* d_Y,
                       q4nx_dtype y_dtype, hipStream_t stream) {
-  return gemm_entry<true>(M, N, K, d_X, d_blob, d_Y, y_dtype, stream, "q4nx_gemm");
+  return gemm_entry<kWQ4NX>(M, N, K, d_X, d_blob, d_Y, y_dtype, stream, "q4nx_gemm");
+}
+
+q4nx_status q4nx_mx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_blob, void* d_Y,
+                         q4nx_dtype y_dtype, hipStream_t stream) {
+  return gemm_entry<kWMX>(M, N, K, d_X, d_blob, d_Y, y_dtype, stream, "q4nx_mx_gemm");
 }
 
 q4nx_status q4nx_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const uint16_t* d_W, void* d_Y,
                            q4nx_dtype y_dtype, hipStream_t stream) {
-  return gemm_entry<false>(M, N, K, d_X, d_W, d_Y, y_dtype, stream, "q4nx_gemm_bf16");
+  return gemm_entry<kWBf16>(M, N, K, d_X, d_W, d_Y, y_dtype, stream, "q4nx_gemm_bf16");
 }
 
 }  // extern "C"

@@ -11,7 +11,7 @@ import pytest
 
 import oracle
 import paper_2602_06063_amd as q4
-from workloads import gen_weights, gen_edge_weights, MODELS
+from workloads import gen_weights, gen_edge_weights, gen_mx_weights, MODELS
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
@@ -183,6 +183,100 @@ def test_device_calls_validate_before_hip():
     assert L.q4nx_gemm_bf16(4, 32, 256, A16, A16, None, 0, None) == q4.Q4NX_ERR_INVALID_ARG
     assert L.q4nx_gemm_bf16(4, 32, 256, A16, MIS, A16, 0, None) == q4.Q4NX_ERR_ALIGNMENT
     assert L.q4nx_gemm_bf16(4, 32, 256, A16, A16, A16, 3, None) == q4.Q4NX_ERR_INVALID_ARG
+
+
+# ----------------------------------------------------------------- MXFP4 variant
+@pytest.mark.parametrize("N,K", [(1, 32), (32, 256), (33, 288), (300, 5376), (64, 21504)])
+def test_mx_packed_size_matches_oracle(N, K):
+    assert q4.q4nx_mx_packed_size(N, K) == oracle.mx_packed_size(N, K)
+    assert q4.q4nx_mx_packed_size(N, K) == ((N + 31) // 32) * ((K + 255) // 256) * 4352
+
+
+def test_mx_packed_size_rejects():
+    for N, K in [(0, 256), (-1, 256), (32, 0), (32, 33), (1 << 31, 256), (32, 1 << 31)]:
+        assert q4.q4nx_mx_packed_size(N, K) == 0
+
+
+@pytest.mark.parametrize("N,K,mode", [(1, 32, "model"), (32, 256, "model"), (33, 288, "edge"), (100, 1152, "model"),
+                                      (70, 800, "edge"), (64, 5376, "model")])
+def test_mx_pack_bit_exact_vs_oracle_and_roundtrip(N, K, mode):
+    codes, sc = gen_mx_weights(N, K, seed=N + K, mode=mode)
+    blob = q4.q4nx_mx_pack(codes, sc)
+    ref = oracle.mx_pack(codes, sc)
+    assert blob.size == ref.size
+    assert np.array_equal(blob, ref)
+    c2, s2 = q4.q4nx_mx_unpack(blob, N, K)
+    assert np.array_equal(c2, codes) and np.array_equal(s2, sc)
+
+
+def test_mx_pack_full_size_projection_shape_is_bit_exact():
+    N, K = MODELS["4b"]["proj"][4][1:]
+    codes, sc = gen_mx_weights(N, K, seed=0, proj=4)
+    assert np.array_equal(q4.q4nx_mx_pack(codes, sc), oracle.mx_pack(codes, sc))
+
+
+def test_mx_pack_error_paths():
+    N, K = 32, 256
+    codes, sc = gen_mx_weights(N, K, seed=3)
+    size = q4.q4nx_mx_packed_size(N, K)
+    P = q4._np_ptr
+
+    def raw(c, s, n, k, nbytes):
+        blob = np.zeros(max(nbytes, 1), np.uint8)
+        return q4.lib.q4nx_mx_pack(P(c), P(s), n, k, P(blob), nbytes), blob
+
+    assert raw(codes, sc, N, K, size)[0] == q4.Q4NX_OK
+    assert raw(codes, sc, 0, K, size)[0] == q4.Q4NX_ERR_SHAPE
+    assert raw(codes, sc, N, 48, size)[0] == q4.Q4NX_ERR_SHAPE
+    assert raw(codes, sc, N, K, size - 1)[0] == q4.Q4NX_ERR_BUFFER_TOO_SMALL
+    blob = np.zeros(size, np.uint8)
+    assert q4.lib.q4nx_mx_pack(None, P(sc), N, K, P(blob), size) == q4.Q4NX_ERR_INVALID_ARG
+    assert q4.lib.q4nx_mx_pack(P(codes), None, N, K, P(blob), size) == q4.Q4NX_ERR_INVALID_ARG
+    assert q4.lib.q4nx_mx_pack(P(codes), P(sc), N, K, None, size) == q4.Q4NX_ERR_INVALID_ARG
+    bad = codes.copy()
+    bad[17, 201] = 16
+    st, blob = raw(bad, sc, N, K, size)
+    assert st == q4.Q4NX_ERR_INVALID_ARG and not blob.any()
+    for e in (0, 1, 26, 228, 254, 255):        # outside [27, 227]; 255 is NaN in E8M0
+        s2 = sc.copy()
+        s2[5, 3] = e
+        st, blob = raw(codes, s2, N, K, size)
+        assert st == q4.Q4NX_ERR_INVALID_ARG and not blob.any(), e
+        assert "scale" in q4.lib.q4nx_last_error().decode()
+    for e in (27, 127, 227):
+        s2 = sc.copy()
+        s2[0, 0] = e
+        assert raw(codes, s2, N, K, size)[0] == q4.Q4NX_OK, e
+    c = np.empty((N, K), np.uint8)
+    ss = np.empty((N, K // 32), np.uint8)
+    good = q4.q4nx_mx_pack(codes, sc)
+    assert q4.lib.q4nx_mx_unpack(P(good), good.size - 1, N, K, P(c), P(ss)) == q4.Q4NX_ERR_BUFFER_TOO_SMALL
+    assert q4.lib.q4nx_mx_unpack(None, good.size, N, K, P(c), P(ss)) == q4.Q4NX_ERR_INVALID_ARG
+    assert q4.lib.q4nx_mx_unpack(P(good), good.size, N, 40, P(c), P(ss)) == q4.Q4NX_ERR_SHAPE
+
+
+def test_mx_device_calls_validate_before_hip():
+    L = q4.lib
+    assert L.q4nx_mx_dequant(None, 32, 256, A16, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_mx_dequant(A16, 32, 250, A16, 0, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_mx_dequant(MIS, 32, 256, A16, 0, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_mx_dequant(A16, 32, 256, A16, 7, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_mx_gemv(None, A16, A16, 0, 32, 256, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_mx_gemv(A16, A16, A16, 0, 32, 100, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_mx_gemv(A16, MIS, A16, 0, 32, 256, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_mx_gemv(A16, A16, A16, 2, 32, 256, None) == q4.Q4NX_ERR_INVALID_ARG
+    arr = (q4.q4nx_gemv_desc * 9)()
+    for i in range(9):
+        arr[i] = q4.q4nx_gemv_desc(A16, A16, A16, 32, 256)
+    assert L.q4nx_mx_gemv_batched(arr, 0, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_mx_gemv_batched(arr, 9, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    arr[1] = q4.q4nx_gemv_desc(A16, A16, A16, 32, 40)
+    assert L.q4nx_mx_gemv_batched(arr, 2, 0, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_mx_gemm(0, 32, 256, A16, A16, A16, 0, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_mx_gemm(4, 32, 80, A16, A16, A16, 0, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_mx_gemm(4, 32, 256, A16, None, A16, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_mx_gemm(4, 32, 256, A16, MIS, A16, 0, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_mx_gemm(4, 32, 256, A16, A16, A16, 3, None) == q4.Q4NX_ERR_INVALID_ARG
 
 
 def test_status_strings():

@@ -171,6 +171,27 @@ def gen_edge_weights(N: int, K: int, seed: int = 0):
     return codes, scales, offsets
 
 
+def gen_mx_weights(N: int, K: int, seed: int = 0, layer: int = 0, proj: int = 0, mode: str = "model"):
+    """MXFP4-variant weights: FP4 E2M1 codes u8[N][K] (uniform 0..15) and E8M0
+    scale bytes u8[N][K/32].  "model": scale exponents 2^-8..2^-5, the range a
+    weight matrix of standard deviation ~0.02 gets (largest FP4 magnitude 6);
+    "edge": scale bytes over the whole accepted range 27..227, both ends and
+    1 (byte 127) included."""
+    if K % 32:
+        raise ValueError("K must be a multiple of 32")
+    rng = weight_rng(seed, layer, proj + 100)
+    codes = draw_codes(rng, N, K)
+    G = K // 32
+    if mode == "model":
+        scales = rng.integers(119, 123, size=(N, G), dtype=np.int64).astype(np.uint8)
+    elif mode == "edge":
+        pick = np.array([27, 28, 60, 100, 126, 127, 128, 150, 200, 226, 227], dtype=np.uint8)
+        scales = pick[rng.integers(0, len(pick), size=(N, G))]
+    else:
+        raise ValueError(f"unknown mode {mode!r}")
+    return codes, scales
+
+
 def device_act_seed(seed: int, layer: int, proj: int) -> int:
     """64-bit seed of the on-device activation stream of (seed, layer, proj)."""
     st = np.random.SeedSequence([seed, layer, proj, 2]).generate_state(2, dtype=np.uint32)
