@@ -354,10 +354,11 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
 // wave accumulates, per lane, the rows 8t + l/8 (t = t0..t0+tq-1) of group
 // l%8 as
 //     acc += d_g * (sum_{k in g} q_k x_k) + m_g * S_g ,  S_g = sum_{k in g} x_k
-// (Eq. 3 folded into Eq. 15), so the per-weight work is one exact code ->
-// float32 convert and one FMA.  x is staged in LDS as float32 with its group
-// sums, a chunk of K at a time; groups are padded to 36 floats so the eight
-// groups a wave reads at once fall in distinct banks.  At the end a 3-step
+// (Eq. 3 folded into Eq. 15), so the per-weight work is the exact code ->
+// bf16 conversion and one v_dot2 per two weights.  x is staged in LDS as bf16
+// pairs in the order the nibble split produces, with its group sums, a chunk
+// of K at a time; groups are padded to 20 dwords so the eight groups a wave
+// reads at once fall in distinct banks.  At the end a 3-step
 // butterfly adds the 8 groups of a row and the W waves' partial sums are added
 // in wave order through LDS.  No workgroup talks to another, so there is no
 // cross-XCD traffic and no device-wide fence.  The summation order is fixed
@@ -367,11 +368,19 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
 // For the MXFP4 variant the per-group term is X_g * (sum_{k in g} fp4(q_k) x_k)
 // (no offset), with x staged in natural column order.
 constexpr int kGemvMaxWaves = 16;
-constexpr int kGemvChunkBlocks = 48;                    // x staged 48 x 256 columns at a time
+// x is staged up to 88 x 256 columns at a time (at most 61 KiB of LDS with the
+// padding and group sums): every Gemma3 K in one piece, so no workgroup drains
+// its waves to restage x in the middle of a row group.
+constexpr int kGemvChunkBlocks = 88;
 constexpr int kGroupPadDw = 20;  // dwords per staged group (16 bf16 pairs + 4 pad: conflict-free reads)
 constexpr int kRedFloats = kGemvMaxWaves * 32;
 // Blocks in flight per wave (register slots), by row octets per wave.
 constexpr int kGemvDepth4 = 1, kGemvDepth2 = 3, kGemvDepth1 = 4;
+// 16-byte pieces of x per thread requested before the first weight blocks.
+template <int TQ>
+constexpr int gemv_xpre() {
+  return TQ == 2 ? 2 : 4;
+}
 
 struct GemvJob {
   const uint8_t* blob;
@@ -402,7 +411,7 @@ struct GemvSlot {
   uint32_t s[TQ], m[TQ];
 };
 
-// Buffer descriptor over one chunk of one strip (at most 48 blocks <= 240 KiB,
+// Buffer descriptor over one chunk of one strip (at most 88 blocks <= 440 KiB,
 // so every offset fits the 32-bit descriptor range); raw, stride 0.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t chunk_rsrc(const uint8_t* base, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(base), (short)0, bytes, 0x00020000);
@@ -464,7 +473,7 @@ __device__ __forceinline__ void gemv_compute(const GemvSlot<TQ>& R, bool gvalid,
 template <int TQ, int D, int F>
 __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs args) {
   constexpr int kBytes = wblock_bytes<F>();
-  // Dynamic LDS: red[16*32] | ssum[chunk*8] | xs[chunk*8*36], chunk = the
+  // Dynamic LDS: red[16*32] | ssum[chunk*8] | xs[chunk*8*20], chunk = the
   // launch's largest staged block count (at most kGemvChunkBlocks).
   extern __shared__ __attribute__((aligned(16))) float lds[];
   float* red = lds;
@@ -500,6 +509,20 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
       const int nb = min(CB, J.KB - jc0);
       const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(sblob + (size_t)jc0 * kBytes, nb * kBytes);
       const int kvalid = J.K - jc0 * kBlockCols;  // columns of this chunk inside K
+      // The first pieces of this chunk's x are requested before the weight
+      // blocks, so that they are not queued behind them (every workgroup
+      // waits for x before it computes anything).
+      constexpr int kXPre = gemv_xpre<TQ>();
+      u32x4 xpre[kXPre];
+      if (staged != ch) {
+#pragma unroll
+        for (int i = 0; i < kXPre; ++i) {
+          const int e = threadIdx.x + i * nthreads;
+          const int k = jc0 * kBlockCols + 8 * e;
+          xpre[i] = (u32x4){0u, 0u, 0u, 0u};
+          if (e < nb * (kBlockCols / 8) && k < J.K) xpre[i] = *reinterpret_cast<const u32x4*>(J.x + k);
+        }
+      }
       // The wave's first D blocks go in flight before the x staging.
       GemvSlot<TQ> buf[D];
 #pragma unroll
@@ -511,10 +534,17 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
         // (x0,x2) (x4,x6) (x1,x3) (x5,x7) and adds them to its group's sum
         // (MXFP4 variant: the pairs in natural order, no sum).
         const int kbeg = jc0 * kBlockCols;
-        for (int e = threadIdx.x; e < nb * (kBlockCols / 8); e += nthreads) {
+        int it = 0;
+        for (int e = threadIdx.x; e < nb * (kBlockCols / 8); e += nthreads, ++it) {
           const int k = kbeg + 8 * e;
           u32x4 v = (u32x4){0u, 0u, 0u, 0u};
-          if (k < J.K) v = *reinterpret_cast<const u32x4*>(J.x + k);
+          if (it < kXPre) {
+#pragma unroll
+            for (int i = 0; i < kXPre; ++i)
+              if (i == it) v = xpre[i];
+          } else if (k < J.K) {
+            v = *reinterpret_cast<const u32x4*>(J.x + k);
+          }
           if constexpr (F == kWMX) {
             *reinterpret_cast<u32x4*>(xs + (e >> 2) * kGroupPadDw + 4 * (e & 3)) = v;
             continue;

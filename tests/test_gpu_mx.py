@@ -80,7 +80,7 @@ def _gemv_case(q4, N, K, seed, mode="model", bf16_out=False, proj=0):
 
 
 @pytest.mark.parametrize("N,K", [(1, 32), (32, 256), (33, 288), (64, 512), (1024, 1152), (257, 1184), (8, 4096),
-                                 (3000, 256), (40, 21504)])
+                                 (3000, 256), (40, 21504), (40, 22560), (33, 51232)])
 @pytest.mark.parametrize("mode", ["model", "edge"])
 def test_mx_gemv_parity_small(q4, N, K, mode):
     _say("mx gemv", N, K, mode)

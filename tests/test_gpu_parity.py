@@ -93,8 +93,9 @@ def _gemv_case(q4, N, K, seed, mode="zp", bf16_out=False, layer=0, proj=0):
     return ok, worst
 
 
+# K = 22560 and 51232 span 89 and 201 blocks: x is staged in more than one chunk.
 GEMV_SHAPES = [(1, 32), (32, 256), (33, 288), (64, 512), (1024, 1152), (100, 544), (257, 1184), (8, 4096),
-               (3000, 256), (40, 21504)]
+               (3000, 256), (40, 21504), (40, 22560), (33, 51232)]
 
 
 @pytest.mark.parametrize("N,K", GEMV_SHAPES)
