@@ -6,7 +6,10 @@ One step = one pass of the whole path over one batch of synthetic input:
     order -- per layer q/k/v in one batched launch, o, gate/up in one batched
     launch, down (+ lm_head once for the 4B decode step);
   * prefill: the fused dequant-GEMM of every projection of every layer on an
-    M-token chunk.
+    M-token chunk; projections that read the same input (q/k/v, gate/up) run
+    as one GEMM over their stacked weights, as an inference engine lays them
+    out (a stacked Q4NX matrix is the projections' blobs back to back, since
+    blocks are stored strip by strip and every N is a multiple of 32).
 Inputs (packed weights, activations) are resident in HBM before the timed
 region; every (layer, projection) has its own independently seeded weights and
 activations.  Timing uses HIP events on the stream the kernels run on.
@@ -36,6 +39,8 @@ HBM_PEAK_GBS = 8000.0           # MI355X HBM3E
 BF16_MFMA_PEAK_TFLOPS = 2516.6  # 256 CU x 4096 flop/clk x 2.4 GHz, dense
 WEIGHT_BYTES = 0.625            # per weight: 0.5 code + 1/16 scale + 1/16 offset
 MX_WEIGHT_BYTES = 0.53125       # MXFP4 variant: 0.5 code + 1/32 E8M0 scale
+# Projections of a layer that read the same input, in order: q/k/v, o, gate/up, down.
+GROUPS = [[0, 1, 2], [3], [4, 5], [6]]
 
 
 def log(*a):
@@ -72,7 +77,10 @@ def parse():
 
 def build_weights(model, cfg, seed, mode, q4, torch, mx=False):
     """Generate, pack (q4nx_pack, or q4nx_mx_pack for the MXFP4 variant) and
-    upload every projection's weights."""
+    upload every projection's weights.  The blobs of a group of projections
+    that share an input lie back to back in one device buffer, which is the
+    packed blob of the stacked matrix; returns ({(layer, proj): blob view},
+    {(layer, group): stacked blob})."""
     from workloads import gen_weights, gen_mx_weights
     L = model["layers"]
     tasks = [(l, p, N, K) for l in range(L) for p, (_, N, K) in enumerate(model["proj"])]
@@ -86,15 +94,30 @@ def build_weights(model, cfg, seed, mode, q4, torch, mx=False):
         codes, s, o = gen_weights(N, K, seed=seed, layer=l, proj=p, offset_mode=mode)
         return q4.q4nx_pack(codes, s, o)
 
-    out = {}
+    size = q4.q4nx_mx_packed_size if mx else q4.q4nx_packed_size
+    out, stacked = {}, {}
+    for l in range(L):
+        for gi, g in enumerate(GROUPS):
+            buf = torch.empty(sum(size(model["proj"][p][1], model["proj"][p][2]) for p in g), dtype=torch.uint8,
+                              device="cuda")
+            stacked[(l, gi)] = buf
+            off = 0
+            for p in g:
+                n = size(model["proj"][p][1], model["proj"][p][2])
+                out[(l, p)] = buf[off:off + n]
+                off += n
     t0 = time.time()
     workers = max(1, min(16, len(os.sched_getaffinity(0))))
     with ThreadPoolExecutor(workers) as ex:
         for i, (t, blob) in enumerate(zip(tasks, ex.map(work, tasks))):
-            out[(t[0], t[1])] = torch.from_numpy(blob).cuda()
+            key = (t[0], t[1])
+            if key in out:
+                out[key].copy_(torch.from_numpy(blob))
+            else:
+                out[key] = torch.from_numpy(blob).cuda()
             if (i + 1) % 50 == 0 or i + 1 == len(tasks):
                 log(f"{'MXFP4 ' if mx else ''}weights {i + 1}/{len(tasks)} packed+uploaded ({time.time() - t0:.0f}s)")
-    return out
+    return out, stacked
 
 
 class Step:
@@ -158,12 +181,13 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
     dec_t = dec_bytes = 0.0
     pre_t = pre_flops = 0.0
     rows = 16
+    first = {p: g[0] for g in GROUPS for p in g}   # projections of a group share the prefill input
     for l in range(layers):
         for p, (_, N, K) in enumerate(model["proj"]):
             codes, s, o = gen_weights(N, K, seed=seed, layer=l, proj=p, offset_mode=mode)
             blob = oracle.pack(codes, s, o)
             x = gen_activations(K, seed=seed, layer=l, proj=p)
-            X = gen_activations((rows, K), seed=seed, layer=l, proj=p)
+            X = gen_activations((rows, K), seed=seed, layer=l, proj=first[p])
             t0 = time.perf_counter()
             w = oracle.dequant_blob_f32(blob, N, K)
             t_deq = time.perf_counter() - t0
@@ -341,7 +365,7 @@ def main():
     do_prefill = M_pre > 0
     log(f"config {args.config}: {cfg['name']}, {L} layers, M={Ms}")
 
-    weights = build_weights(model, cfg, args.seed, args.offset_mode, q4, torch)
+    weights, stacked = build_weights(model, cfg, args.seed, args.offset_mode, q4, torch)
     stream = torch.cuda.Stream()      # every launch, capture and event lives here
     torch.cuda.set_stream(stream)
     F32 = q4.Q4NX_F32
@@ -381,32 +405,35 @@ def main():
     pre = Step(q4, stream.cuda_stream)
     two = Step(q4, stream.cuda_stream)   # two-phase: dequant to bf16 W, then the plain bf16 GEMM
     pre_flops = 0.0
+    alg_pre = 0.0
+    # One GEMM per group of projections that share an input: N = the group's
+    # stacked outputs, X drawn per (layer, first projection of the group).
+    shapes = [(sum(model["proj"][p][1] for p in g), model["proj"][g[0]][2]) for g in GROUPS]
     if do_prefill:
         Xs = {}
-        Ys = {}
-        for p, (_, N, K) in enumerate(model["proj"]):
-            Ys[p] = torch.empty((M_pre, N), dtype=torch.float32, device="cuda")
-        Wtmp = torch.empty(max(N * K for _, N, K in model["proj"]), dtype=torch.bfloat16, device="cuda")
+        Ys = [torch.empty((M_pre, N), dtype=torch.float32, device="cuda") for N, _ in shapes]
+        Wtmp = torch.empty(max(N * K for N, K in shapes), dtype=torch.bfloat16, device="cuda")
         for l in range(L):
-            for p, (_, N, K) in enumerate(model["proj"]):
-                Xs[(l, p)] = gen_activations_device((M_pre, K), seed=args.seed, layer=l, proj=p)
-                pre.gemm(M_pre, N, K, Xs[(l, p)], weights[(l, p)], Ys[p], F32)
-                two.dequant_bf16(weights[(l, p)], N, K, Wtmp)
-                two.gemm_bf16(M_pre, N, K, Xs[(l, p)], Wtmp, Ys[p], F32)
+            for gi, (N, K) in enumerate(shapes):
+                Xs[(l, gi)] = gen_activations_device((M_pre, K), seed=args.seed, layer=l, proj=GROUPS[gi][0])
+                pre.gemm(M_pre, N, K, Xs[(l, gi)], stacked[(l, gi)], Ys[gi], F32)
+                two.dequant_bf16(stacked[(l, gi)], N, K, Wtmp)
+                two.gemm_bf16(M_pre, N, K, Xs[(l, gi)], Wtmp, Ys[gi], F32)
                 pre_flops += 2.0 * M_pre * N * K
+                alg_pre += 2 * M_pre * K + N * K * WEIGHT_BYTES + 4 * M_pre * N
     # MXFP4 variant: the same steps over MXFP4-variant weights (same
     # activations and outputs).
     mdec = Step(q4, stream.cuda_stream, mx=True)
     mpre = Step(q4, stream.cuda_stream, mx=True)
     mweights = None
     if args.mx and not args.pmc_pass:
-        mweights = build_weights(model, cfg, args.seed, args.offset_mode, q4, torch, mx=True)
+        mweights, mstacked = build_weights(model, cfg, args.seed, args.offset_mode, q4, torch, mx=True)
         if do_decode:
             decode_calls(mdec, mweights)
         if do_prefill:
             for l in range(L):
-                for p, (_, N, K) in enumerate(model["proj"]):
-                    mpre.gemm(M_pre, N, K, Xs[(l, p)], mweights[(l, p)], Ys[p], F32)
+                for gi, (N, K) in enumerate(shapes):
+                    mpre.gemm(M_pre, N, K, Xs[(l, gi)], mstacked[(l, gi)], Ys[gi], F32)
     torch.cuda.synchronize()
     log(f"inputs resident: {sum(t.numel() for t in weights.values()) / 1e9:.2f} GB of packed weights"
         + (f" + {sum(t.numel() for t in mweights.values()) / 1e9:.2f} GB MXFP4-variant" if mweights else ""))
@@ -501,7 +528,6 @@ def main():
     if do_decode and cfg.get("lm_head"):
         _, N, K = model["lm_head"]
         alg_dec += N * K * WEIGHT_BYTES + 2 * K + 4 * N
-    alg_pre = sum(2 * M_pre * K + N * K * WEIGHT_BYTES + 4 * M_pre * N for _, N, K in model["proj"]) * L if do_prefill else 0
     mx = None
     if mweights is not None:
         mx = {"what": "the same decode and prefill steps over MXFP4-variant weights (FP4 E2M1 codes, one E8M0 "
@@ -628,14 +654,16 @@ def main():
         result["prefill"] = {"ms": round(mean(pre_ms), 4), "ms_min": round(min(pre_ms), 4), "M": M_pre,
                              "TFLOP": round(pre_flops / 1e12, 4), "TFLOP_per_s": round(pre_tflops, 2),
                              "frac_mfma": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4),
-                             "launches": len(pre.calls), "dtype": "bf16 MFMA, f32 accumulate"}
+                             "launches": len(pre.calls), "dtype": "bf16 MFMA, f32 accumulate",
+                             "gemms": "per layer: q/k/v stacked, o, gate/up stacked, down ("
+                                      + ", ".join(f"{N}x{K}" for N, K in shapes) + ")"}
         if two_ms:
             t = mean(two_ms)
             result["prefill"]["two_phase"] = {
                 "ms": round(t, 4), "ms_min": round(min(two_ms), 4),
                 "TFLOP_per_s": round(pre_flops / (t * 1e-3) / 1e12, 2),
                 "launches": len(two.calls),
-                "what": "per projection: q4nx_dequant to a bf16 W buffer, then q4nx_gemm_bf16 (same bits as q4nx_gemm)"}
+                "what": "per GEMM: q4nx_dequant to a bf16 W buffer, then q4nx_gemm_bf16 (same bits as q4nx_gemm)"}
         if do_decode:
             result["value_gemm"] = round(pre_tflops, 2)
     # Dominant kernel by time: the GEMM when the step has a prefill chunk.

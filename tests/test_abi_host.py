@@ -65,6 +65,19 @@ def test_pack_full_size_projection_shape_is_bit_exact():
     assert np.array_equal(q4.q4nx_pack(codes, s, o), oracle.pack(codes, s, o))
 
 
+def test_stacked_matrix_blob_is_the_blobs_back_to_back():
+    """Blocks are stored strip by strip, so the blob of row-stacked matrices
+    whose N are multiples of 32 is their blobs concatenated (the prefill runs
+    q/k/v and gate/up as one product over such a stacked blob)."""
+    K = 800
+    parts = [gen_weights(N, K, seed=20 + i) for i, N in enumerate((64, 32, 96))]
+    stacked = q4.q4nx_pack(*(np.concatenate([p[j] for p in parts]) for j in range(3)))
+    assert np.array_equal(stacked, np.concatenate([q4.q4nx_pack(*p) for p in parts]))
+    mparts = [gen_mx_weights(N, K, seed=30 + i) for i, N in enumerate((64, 32, 96))]
+    mstacked = q4.q4nx_mx_pack(*(np.concatenate([p[j] for p in mparts]) for j in range(2)))
+    assert np.array_equal(mstacked, np.concatenate([q4.q4nx_mx_pack(*p) for p in mparts]))
+
+
 def _raw_pack(codes, s, o, N, K, blob_bytes):
     blob = np.zeros(max(blob_bytes, 1), np.uint8)
     st = q4.lib.q4nx_pack(q4._np_ptr(codes), q4._np_ptr(s), q4._np_ptr(o), N, K, q4._np_ptr(blob), blob_bytes)

@@ -269,6 +269,19 @@ def test_gemm_full_size_sampled_rows(q4, model, p):
     assert tight, name
 
 
+# The stacked prefill products (q/k/v and gate/up of one layer as one GEMM):
+# 27B 4096 x 8192 and 4096 x 43008 (columns 0..40959 in 256 x 256 tiles, the
+# rest in 256 x 128), 4B 2048 x 4096 and 2048 x 20480, all at the model's K.
+@pytest.mark.parametrize("M,N,K", [(4096, 8192, 5376), (4096, 43008, 5376), (2048, 4096, 2560), (2048, 20480, 2560)])
+def test_gemm_stacked_prefill_shapes_sampled_rows(q4, M, N, K):
+    rng = np.random.default_rng(3)
+    rows = np.unique(np.concatenate([np.arange(16), M - 16 + np.arange(16), rng.integers(0, M, 32)]))
+    _say("gemm stacked", M, N, K)
+    ok, worst, tight = _gemm_case(q4, M, N, K, seed=N, rows=rows)
+    assert ok, worst
+    assert tight
+
+
 # Shapes that take each launch plan of q4nx_gemm on a 256-CU device, with
 # ragged M and N and a K that is not a multiple of the 64-column step:
 #   3996 x 4080 x 5344  one launch of 256 x 256 tiles (the K-tail variant)
