@@ -9,7 +9,9 @@ One step = one pass of the whole path over one batch of synthetic input:
     M-token chunk; projections that read the same input (q/k/v, gate/up) run
     as one GEMM over their stacked weights, as an inference engine lays them
     out (a stacked Q4NX matrix is the projections' blobs back to back, since
-    blocks are stored strip by strip and every N is a multiple of 32).
+    blocks are stored strip by strip and every N is a multiple of 32); each
+    GEMM is q4nx_gemm_ex with a workspace, so shapes with few output tiles
+    over a long K (the down projections) are split along K.
 Inputs (packed weights, activations) are resident in HBM before the timed
 region; every (layer, projection) has its own independently seeded weights and
 activations.  Timing uses HIP events on the stream the kernels run on.
@@ -131,7 +133,15 @@ class Step:
         # weight format of the packed launches: Q4NX or the MXFP4 variant
         self.size = q4.q4nx_mx_packed_size if mx else q4.q4nx_packed_size
         self.gemv_fn = q4.lib.q4nx_mx_gemv_batched if mx else q4.lib.q4nx_gemv_batched
-        self.gemm_fn = q4.lib.q4nx_mx_gemm if mx else q4.lib.q4nx_gemm
+        self.wformat = q4.Q4NX_WEIGHTS_MXFP4 if mx else q4.Q4NX_WEIGHTS_Q4NX
+        self.work = None  # GEMM workspace (q4nx_gemm_ex may split K with it), shared by the step's launches
+
+    def _work(self, M, N, K):
+        need = self.q4.q4nx_gemm_workspace_size(M, N, K)
+        have = 0 if self.work is None else self.work.numel() * 4
+        if need > have:
+            raise ValueError(f"GEMM workspace: {have} bytes, {M}x{N}x{K} needs {need}")
+        return (self.work.data_ptr() if self.work is not None else None), have
 
     def gemv_batched(self, items, ydt):
         arr = (self.q4.q4nx_gemv_desc * len(items))()
@@ -147,7 +157,9 @@ class Step:
         self.q4._need(blob, self.size(N, K), "blob")
         self.q4._need(X, 2 * M * K, "X")
         self.q4._need(Y, M * N * Y.element_size(), "Y")
-        self.calls.append((self.gemm_fn, (M, N, K, X.data_ptr(), blob.data_ptr(), Y.data_ptr(), ydt, self.s)))
+        wp, wn = self._work(M, N, K)
+        self.calls.append((self.q4.lib.q4nx_gemm_ex, (self.wformat, M, N, K, X.data_ptr(), blob.data_ptr(),
+                                                      Y.data_ptr(), ydt, wp, wn, self.s)))
 
     def dequant_bf16(self, blob, N, K, W):
         self.q4._need(blob, self.q4.q4nx_packed_size(N, K), "blob")
@@ -158,7 +170,9 @@ class Step:
         self.q4._need(W, 2 * N * K, "W")
         self.q4._need(X, 2 * M * K, "X")
         self.q4._need(Y, M * N * Y.element_size(), "Y")
-        self.calls.append((self.q4.lib.q4nx_gemm_bf16, (M, N, K, X.data_ptr(), W.data_ptr(), Y.data_ptr(), ydt, self.s)))
+        wp, wn = self._work(M, N, K)
+        self.calls.append((self.q4.lib.q4nx_gemm_ex, (self.q4.Q4NX_WEIGHTS_BF16, M, N, K, X.data_ptr(), W.data_ptr(),
+                                                      Y.data_ptr(), ydt, wp, wn, self.s)))
 
     def run(self):
         for fn, args in self.calls:
@@ -404,6 +418,7 @@ def main():
     # ---------------------------------------------------------------- prefill
     pre = Step(q4, stream.cuda_stream)
     two = Step(q4, stream.cuda_stream)   # two-phase: dequant to bf16 W, then the plain bf16 GEMM
+    mpre = Step(q4, stream.cuda_stream, mx=True)
     pre_flops = 0.0
     alg_pre = 0.0
     # One GEMM per group of projections that share an input: N = the group's
@@ -413,6 +428,10 @@ def main():
         Xs = {}
         Ys = [torch.empty((M_pre, N), dtype=torch.float32, device="cuda") for N, _ in shapes]
         Wtmp = torch.empty(max(N * K for N, K in shapes), dtype=torch.bfloat16, device="cuda")
+        # One split-K workspace for every GEMM of the step (they run one after another).
+        work_bytes = max(q4.q4nx_gemm_workspace_size(M_pre, N, K) for N, K in shapes)
+        gemm_work = torch.empty(max(work_bytes // 4, 1), dtype=torch.float32, device="cuda")
+        pre.work = two.work = mpre.work = gemm_work
         for l in range(L):
             for gi, (N, K) in enumerate(shapes):
                 Xs[(l, gi)] = gen_activations_device((M_pre, K), seed=args.seed, layer=l, proj=GROUPS[gi][0])
@@ -424,7 +443,6 @@ def main():
     # MXFP4 variant: the same steps over MXFP4-variant weights (same
     # activations and outputs).
     mdec = Step(q4, stream.cuda_stream, mx=True)
-    mpre = Step(q4, stream.cuda_stream, mx=True)
     mweights = None
     if args.mx and not args.pmc_pass:
         mweights, mstacked = build_weights(model, cfg, args.seed, args.offset_mode, q4, torch, mx=True)
@@ -668,7 +686,7 @@ def main():
             result["value_gemm"] = round(pre_tflops, 2)
     # Dominant kernel by time: the GEMM when the step has a prefill chunk.
     if do_prefill:
-        result["roofline"] = {"kernel": "q4nx_gemm launches (gemm256_kernel, gemm_kernel)", "bound": "mfma", "achieved": round(pre_tflops, 2),
+        result["roofline"] = {"kernel": "q4nx_gemm_ex launches (gemm256_kernel, gemm_kernel, splitk_sum_kernel)", "bound": "mfma", "achieved": round(pre_tflops, 2),
                               "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                               "frac": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
                               "algorithmic_bytes": round(alg_pre)}

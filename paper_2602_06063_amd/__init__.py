@@ -28,11 +28,15 @@ Q4NX_ERR_HIP = 5
 Q4NX_F32 = 0
 Q4NX_BF16 = 1
 Q4NX_MAX_BATCH = 8
+Q4NX_WEIGHTS_Q4NX = 0
+Q4NX_WEIGHTS_MXFP4 = 1
+Q4NX_WEIGHTS_BF16 = 2
 
 EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_quantize", "q4nx_dequant", "q4nx_gemv",
             "q4nx_gemv_batched", "q4nx_gemm", "q4nx_gemm_bf16", "q4nx_flowkv_workspace_size",
             "q4nx_flowkv_decode", "q4nx_mx_packed_size", "q4nx_mx_pack", "q4nx_mx_unpack", "q4nx_mx_dequant",
-            "q4nx_mx_gemv", "q4nx_mx_gemv_batched", "q4nx_mx_gemm", "q4nx_status_str", "q4nx_last_error"]
+            "q4nx_mx_gemv", "q4nx_mx_gemv_batched", "q4nx_mx_gemm", "q4nx_gemm_workspace_size", "q4nx_gemm_ex",
+            "q4nx_status_str", "q4nx_last_error"]
 
 if not os.path.exists(LIB_PATH):
     raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2602_06063_amd/build.py`")
@@ -92,6 +96,10 @@ lib.q4nx_mx_gemv_batched.argtypes = [ctypes.POINTER(q4nx_gemv_desc), _i32, ctype
 lib.q4nx_mx_gemv_batched.restype = ctypes.c_int
 lib.q4nx_mx_gemm.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp]
 lib.q4nx_mx_gemm.restype = ctypes.c_int
+lib.q4nx_gemm_workspace_size.argtypes = [_i64, _i64, _i64]
+lib.q4nx_gemm_workspace_size.restype = _sz
+lib.q4nx_gemm_ex.argtypes = [ctypes.c_int, _i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp, _sz, _vp]
+lib.q4nx_gemm_ex.restype = ctypes.c_int
 lib.q4nx_status_str.argtypes = [ctypes.c_int]
 lib.q4nx_status_str.restype = ctypes.c_char_p
 lib.q4nx_last_error.argtypes = []
@@ -297,6 +305,23 @@ def q4nx_mx_gemm(M: int, N: int, K: int, X, blob, Y, stream=None):
     _need(Y, M * N * Y.element_size(), "Y")
     _check(lib.q4nx_mx_gemm(M, N, K, _dptr(X), _dptr(blob), _dptr(Y), _dtype_code(Y), _stream(stream)),
            "q4nx_mx_gemm")
+
+
+def q4nx_gemm_workspace_size(M: int, N: int, K: int) -> int:
+    return int(lib.q4nx_gemm_workspace_size(M, N, K))
+
+
+def q4nx_gemm_ex(w_format: int, M: int, N: int, K: int, X, W, Y, work=None, stream=None):
+    """Y[M][N] <- X[M][K] W^T for W in the given format (Q4NX_WEIGHTS_*); with a
+    workspace of q4nx_gemm_workspace_size(M, N, K) bytes the plan may split K."""
+    wbytes = {Q4NX_WEIGHTS_Q4NX: q4nx_packed_size(N, K), Q4NX_WEIGHTS_MXFP4: q4nx_mx_packed_size(N, K),
+              Q4NX_WEIGHTS_BF16: 2 * N * K}.get(w_format, 0)
+    _need(W, wbytes, "W")
+    _need(X, 2 * M * K, "X")
+    _need(Y, M * N * Y.element_size(), "Y")
+    wp, wn = (None, 0) if work is None else (_dptr(work), work.numel() * work.element_size())
+    _check(lib.q4nx_gemm_ex(w_format, M, N, K, _dptr(X), _dptr(W), _dptr(Y), _dtype_code(Y), wp, wn, _stream(stream)),
+           "q4nx_gemm_ex")
 
 
 def q4nx_flowkv_workspace_size(H: int, d: int, n_keys: int) -> int:

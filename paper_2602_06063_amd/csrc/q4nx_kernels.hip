@@ -705,11 +705,15 @@ struct WideRegs<kWBf16> {
 
 // WF: W is a packed Q4NX or MXFP4-variant matrix (dequantized on the fly), or
 // bf16 [N][K], whose tile is staged exactly like the X tile.
+// Split K: workgroup (x, y) computes tile x over K steps [y*ksteps,
+// min((y+1)*ksteps, all steps)) and, when `part` is given, writes its float32
+// partial product to part + y*M*ldy (row stride ldy) instead of Y.
 template <bool KTAIL, int WF>
 __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* __restrict__ X,
                                                                const uint8_t* __restrict__ wsrc,
                                                                void* __restrict__ Y, int M, int N, int K, int ldy,
-                                                               int KB, int NS, int tiles_n, int y_bf16) {
+                                                               int KB, int NS, int tiles_n, int y_bf16, int ksteps,
+                                                               float* __restrict__ part) {
   constexpr int TI = 4, TJ = 4;
   extern __shared__ __attribute__((aligned(16))) uint16_t gl[];
   uint16_t* const xs0 = gl;                          // [2][256][72]
@@ -754,7 +758,9 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
 #pragma unroll
     for (int i = 0; i < 8; ++i) vw[i] = (min((tid >> 3) + 32 * i, rows_w - 1) * K + 8 * c8) * 2;
   }
-  const int nsteps = (K + kBK - 1) / kBK;
+  // K steps of this workgroup's segment: sb .. sb + nsteps - 1.
+  const int sb = blockIdx.y * ksteps;
+  const int nsteps = min((K + kBK - 1) / kBK, sb + ksteps) - sb;
 
   f32x16 acc[TI][TJ];
 #pragma unroll
@@ -764,10 +770,11 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
 
-  // Global loads of step t (clamped to the last step) into R, one of the
-  // kLoads loads per call, so that they can be spread over MFMA slots.
+  // Global loads of step t of the segment (clamped to its last step) into R,
+  // one of the kLoads loads per call, so that they can be spread over MFMA
+  // slots.
   auto load1 = [&](WideRegs<WF>& R, int t, int i) {
-    const int k0 = min(t, nsteps - 1) * kBK;
+    const int k0 = (sb + min(t, nsteps - 1)) * kBK;
     const int sq = (k0 >> 8) * kBB + 16 * ((k0 & 255) >> 5);
     const int ss = (k0 >> 8) * kBB + (WF == kWMX ? 1 : 2) * ((k0 & 255) >> 5);
     const bool okx = !KTAIL || k0 + 8 * c8 < K;
@@ -947,7 +954,15 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
   if (s < nsteps) step(s, R1);
 
   // Accumulator element e of lane l: column l%32, row 8(e/4) + 4(l/32) + e%4.
+  // (One output pointer and one format flag, chosen before the loop: three
+  // store paths inside it make the compiler hoist per-element addresses and
+  // spill.)
   const bool full = m0 + 256 <= M && n0 + 256 <= N;
+  // (The slab offset is formed in unsigned 32-bit pieces: a 64-bit copy of
+  // ldy shared with the element addresses below turns each of them into a
+  // full 64 x 64-bit multiply.)
+  void* const Yo = part ? static_cast<void*>(part + (size_t)(blockIdx.y * (unsigned)M) * (unsigned)ldy) : Y;
+  const int obf16 = part ? 0 : y_bf16;
 #pragma unroll
   for (int a = 0; a < TI; ++a)
 #pragma unroll
@@ -957,13 +972,41 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
       for (int e = 0; e < 16; ++e) {
         const int row = m0 + 128 * wm + 32 * a + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         if (full || (row < M && col < N)) {
-          if (y_bf16)
-            static_cast<uint16_t*>(Y)[(size_t)row * ldy + col] = f32_to_bf16_bits(acc[a][b][e]);
+          if (obf16)
+            static_cast<uint16_t*>(Yo)[(size_t)row * ldy + col] = f32_to_bf16_bits(acc[a][b][e]);
           else
-            static_cast<float*>(Y)[(size_t)row * ldy + col] = acc[a][b][e];
+            static_cast<float*>(Yo)[(size_t)row * ldy + col] = acc[a][b][e];
         }
       }
     }
+}
+
+// Sum of the split-K partial products part[0..ks-1][M][N] (row stride N), in
+// segment order, to Y (row stride ldy) in float32 or bf16.  Thread t handles
+// four consecutive columns of one row.
+__global__ __launch_bounds__(256) void splitk_sum_kernel(const float* __restrict__ part, int ks, int M, int N,
+                                                         void* __restrict__ Y, int64_t ldy, int y_bf16) {
+  const int q = (N + 3) >> 2;  // column quads per row
+  const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (id >= (int64_t)M * q) return;
+  const int row = (int)(id / q), col = (int)(id - (int64_t)row * q) * 4;
+  const int64_t MN = (int64_t)M * N;
+  const float* p = part + (int64_t)row * N + col;
+  float v[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) v[j] = col + j < N ? p[j] : 0.0f;
+  for (int s = 1; s < ks; ++s)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (col + j < N) v[j] += p[s * MN + j];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (col + j >= N) break;
+    if (y_bf16)
+      static_cast<uint16_t*>(Y)[row * ldy + col + j] = f32_to_bf16_bits(v[j]);
+    else
+      static_cast<float*>(Y)[row * ldy + col + j] = v[j];
+  }
 }
 
 // ---- general tiles, two waves per SIMD --------------------------------------
@@ -1189,11 +1232,35 @@ struct GemmTile {
 // Round costs measured on MI355X for the Gemma3 prefill projections (K = 5376).
 constexpr GemmTile kGemmTiles[4] = {{256, 256, 1.0f}, {256, 128, 0.68f}, {128, 128, 0.52f}, {128, 64, 0.38f}};
 
-// A rectangle of the output computed by one launch.
+// A rectangle of the output computed by one launch (ks > 1: by ks K segments
+// of the 256 x 256 kernel and a second launch that adds their partials).
 struct GemmRegion {
   int tile;
   int64_t m0, n0, M, N;
+  int ks;
 };
+
+// Split K.  With a caller workspace, a 256 x 256 launch may run every tile as
+// ks K segments on ks workgroups that write float32 partial products, which a
+// second launch adds in segment order (deterministic).  It pays where a long
+// K meets few tiles (Gemma3 down projections).  Split plans are costed in the
+// planner's unit, a round of 256 x 256 tiles at the full K, through a time
+// model fitted on MI355X: such a round over K columns takes about
+// 40 + 0.0226 K us, and the sum streams its operands at about 5 TB/s after a
+// ~5 us launch.
+constexpr double kRoundFixedUs = 40.0, kRoundPerKUs = 0.0226;
+constexpr double kSumLaunchUs = 5.0, kSumBytesPerUs = 5.0e6;
+constexpr int kMinSegmentSteps = 8;
+
+static double round_us(int64_t K) { return kRoundFixedUs + kRoundPerKUs * (double)K; }
+
+// K steps per segment when K is split into ks non-empty segments of at least
+// kMinSegmentSteps steps each; 0 if it cannot be.
+static int split_steps(int64_t K, int ks) {
+  if (ks < 2 || K >= kWideMaxK) return 0;
+  const int64_t nsteps = ceil_div(K, kBK), per = ceil_div(nsteps, ks);
+  return (per >= kMinSegmentSteps && (ks - 1) * per < nsteps) ? (int)per : 0;
+}
 
 static int device_cus() {
   static int cus[64] = {0};
@@ -1211,18 +1278,35 @@ static int device_cus() {
 // CUs) x (round cost of the tile shape), plus a small cost per extra launch.
 // A launch whose last round is only partly filled still pays a whole round,
 // so a shape with 336 256x256 tiles on 256 CUs is better done as one full
-// round of 256 x 256 tiles and the rest in smaller tiles.
-static int gemm_plan(int64_t M, int64_t N, int cus, GemmRegion (&plan)[2]) {
+// round of 256 x 256 tiles and the rest in smaller tiles.  With split_ok, the
+// whole product or the second region may also be split along K.
+static int gemm_plan(int64_t M, int64_t N, int64_t K, int cus, bool split_ok, GemmRegion (&plan)[2]) {
   const auto rounds = [&](int t, int64_t m, int64_t n) {
     return (double)ceil_div(ceil_div(m, kGemmTiles[t].bm) * ceil_div(n, kGemmTiles[t].bn), cus);
   };
+  // Cost of an (m x n) region as ks K segments of 256 x 256 tiles plus the sum.
+  const auto split_cost = [&](int64_t m, int64_t n, int ks) {
+    const int per = split_steps(K, ks);
+    if (!split_ok || per == 0) return 1e300;
+    const double r = (double)ceil_div(ceil_div(m, 256) * ceil_div(n, 256) * ks, cus);
+    const double sum_us = kSumLaunchUs + (4.0 * ks + 4.0) * (double)m * (double)n / kSumBytesPerUs;
+    return (r * round_us((int64_t)per * kBK) + sum_us) / round_us(K);
+  };
   double best = 1e300;
   int count = 0;
+  for (int ks = 2; ks <= 4; ++ks) {
+    const double c = split_cost(M, N, ks);
+    if (c < best) {
+      best = c;
+      plan[0] = {0, 0, 0, M, N, ks};
+      count = 1;
+    }
+  }
   for (int a = 0; a < 4; ++a) {
     const double c1 = rounds(a, M, N) * kGemmTiles[a].round_cost;
     if (c1 < best) {
       best = c1;
-      plan[0] = {a, 0, 0, M, N};
+      plan[0] = {a, 0, 0, M, N, 1};
       count = 1;
     }
     const int64_t tm = ceil_div(M, kGemmTiles[a].bm), tn = ceil_div(N, kGemmTiles[a].bn);
@@ -1240,14 +1324,32 @@ static int gemm_plan(int64_t M, int64_t N, int cus, GemmRegion (&plan)[2]) {
                           rounds(b, mb, nb) * kGemmTiles[b].round_cost + 0.02 + 0.001 * dir;
         if (c2 < best) {
           best = c2;
-          plan[0] = {a, 0, 0, ma, na};
-          plan[1] = {b, dir == 0 ? split : 0, dir == 0 ? 0 : split, mb, nb};
+          plan[0] = {a, 0, 0, ma, na, 1};
+          plan[1] = {b, dir == 0 ? split : 0, dir == 0 ? 0 : split, mb, nb, 1};
+          count = 2;
+        }
+      }
+      for (int ks = 2; ks <= 4; ++ks) {
+        const double c2 = rounds(a, ma, na) * kGemmTiles[a].round_cost + split_cost(mb, nb, ks) + 0.02 + 0.001 * dir;
+        if (c2 < best) {
+          best = c2;
+          plan[0] = {a, 0, 0, ma, na, 1};
+          plan[1] = {0, dir == 0 ? split : 0, dir == 0 ? 0 : split, mb, nb, ks};
           count = 2;
         }
       }
     }
   }
   return count;
+}
+
+// Workspace bytes a plan needs: the regions run one after the other on one
+// stream, so they share it.
+static size_t plan_work_bytes(const GemmRegion* plan, int count) {
+  size_t b = 0;
+  for (int i = 0; i < count; ++i)
+    if (plan[i].ks > 1) b = std::max(b, (size_t)plan[i].ks * (size_t)plan[i].M * (size_t)plan[i].N * sizeof(float));
+  return b;
 }
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int WF>
@@ -1272,7 +1374,7 @@ static q4nx_status launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* 
 
 template <bool KTAIL, int WF>
 static q4nx_status launch_gemm256(int64_t M, int64_t N, int64_t K, const uint16_t* X, const void* blob, void* Y,
-                                  int64_t ldy, int y_bf16, hipStream_t stream) {
+                                  int64_t ldy, int y_bf16, hipStream_t stream, int ks = 1, float* part = nullptr) {
   auto kern = gemm256_kernel<KTAIL, WF>;
   static bool attr_set = false;
   if (!attr_set) {
@@ -1282,9 +1384,11 @@ static q4nx_status launch_gemm256(int64_t M, int64_t N, int64_t K, const uint16_
     attr_set = true;
   }
   const int64_t tiles_n = ceil_div(N, 256), tiles_m = ceil_div(M, 256);
-  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_n * tiles_m)), dim3(kWideThreads), kWideLdsBytes, stream, X,
-                     static_cast<const uint8_t*>(blob), Y, (int)M, (int)N, (int)K, (int)ldy,
-                     (int)ceil_div(K, kBlockCols), (int)ceil_div(N, kBlockRows), (int)tiles_n, y_bf16);
+  const int ksteps = ks > 1 ? split_steps(K, ks) : (int)ceil_div(K, kBK);
+  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_n * tiles_m), (unsigned)ks), dim3(kWideThreads), kWideLdsBytes,
+                     stream, X, static_cast<const uint8_t*>(blob), Y, (int)M, (int)N, (int)K, (int)ldy,
+                     (int)ceil_div(K, kBlockCols), (int)ceil_div(N, kBlockRows), (int)tiles_n, y_bf16, ksteps,
+                     ks > 1 ? part : nullptr);
   return Q4NX_OK;
 }
 
@@ -1293,13 +1397,24 @@ static q4nx_status launch_gemm256(int64_t M, int64_t N, int64_t K, const uint16_
 // ordinary smaller problem.
 template <int WF>
 static q4nx_status launch_region(const GemmRegion& r, int64_t N, int64_t K, const uint16_t* X, const void* w,
-                                 void* Y, int y_bf16, hipStream_t stream) {
+                                 void* Y, int y_bf16, hipStream_t stream, float* work) {
   const uint16_t* Xr = X + r.m0 * K;
   const void* Wr = WF != kWBf16
                        ? static_cast<const void*>(static_cast<const uint8_t*>(w) +
                                                   (r.n0 / kBlockRows) * ceil_div(K, kBlockCols) * wblock_bytes<WF>())
                        : static_cast<const void*>(static_cast<const uint16_t*>(w) + r.n0 * K);
   void* Yr = static_cast<uint8_t*>(Y) + (r.m0 * N + r.n0) * (y_bf16 ? 2 : 4);
+  if (r.ks > 1) {
+    // Partials [ks][r.M][r.N] in the workspace, then their sum into Y.
+    const q4nx_status st = K % kBK != 0
+                               ? launch_gemm256<true, WF>(r.M, r.N, K, Xr, Wr, Yr, r.N, y_bf16, stream, r.ks, work)
+                               : launch_gemm256<false, WF>(r.M, r.N, K, Xr, Wr, Yr, r.N, y_bf16, stream, r.ks, work);
+    if (st != Q4NX_OK) return st;
+    const int64_t threads = r.M * ceil_div(r.N, 4);
+    hipLaunchKernelGGL(splitk_sum_kernel, dim3((unsigned)ceil_div(threads, 256)), dim3(256), 0, stream, work, r.ks,
+                       (int)r.M, (int)r.N, Yr, N, y_bf16);
+    return Q4NX_OK;
+  }
   switch (r.tile) {
     case 0:
       if (K >= kWideMaxK) return launch_gemm<256, 256, 2, 4, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
@@ -1313,10 +1428,12 @@ static q4nx_status launch_region(const GemmRegion& r, int64_t N, int64_t K, cons
 
 static q4nx_status check_launch(const char* fn);
 
-// Validation shared by the matrix-product entry points, then the planned launches.
+// Validation shared by the matrix-product entry points, then the planned
+// launches (split along K only when a workspace is given).
 template <int WF>
 static q4nx_status gemm_entry(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_W, void* d_Y,
-                              q4nx_dtype y_dtype, hipStream_t stream, const char* fn) {
+                              q4nx_dtype y_dtype, void* d_work, size_t work_bytes, hipStream_t stream,
+                              const char* fn) {
   clear_error();
   if (q4nx_status st = check_shape(N, K, fn)) return st;
   if (M <= 0 || M > Q4NX_MAX_DIM) return fail(Q4NX_ERR_SHAPE, std::string(fn) + ": M must lie in 1..2^30");
@@ -1327,11 +1444,14 @@ static q4nx_status gemm_entry(int64_t M, int64_t N, int64_t K, const uint16_t* d
     return fail(Q4NX_ERR_ALIGNMENT, std::string(fn) + (WF != kWBf16 ? ": X, blob and Y need 16-byte alignment"
                                                                     : ": X, W and Y need 16-byte alignment"));
   if (M * N > (int64_t(1) << 40)) return fail(Q4NX_ERR_SHAPE, std::string(fn) + ": problem too large for one launch");
+  if (d_work && !aligned(d_work, 16)) return fail(Q4NX_ERR_ALIGNMENT, std::string(fn) + ": work needs 16-byte alignment");
   GemmRegion plan[2];
-  const int count = gemm_plan(M, N, device_cus(), plan);
+  const int count = gemm_plan(M, N, K, device_cus(), d_work != nullptr, plan);
+  if (plan_work_bytes(plan, count) > work_bytes)
+    return fail(Q4NX_ERR_BUFFER_TOO_SMALL, std::string(fn) + ": work_bytes < q4nx_gemm_workspace_size(M, N, K)");
   q4nx_status st = Q4NX_OK;
   for (int i = 0; i < count && st == Q4NX_OK; ++i)
-    st = launch_region<WF>(plan[i], N, K, d_X, d_W, d_Y, y_dtype == Q4NX_BF16, stream);
+    st = launch_region<WF>(plan[i], N, K, d_X, d_W, d_Y, y_dtype == Q4NX_BF16, stream, static_cast<float*>(d_work));
   if (st != Q4NX_OK) return st;
   return check_launch(fn);
 }
@@ -1498,17 +1618,42 @@ q4nx_status q4nx_mx_gemv_batched(const q4nx_gemv_desc* descs, int32_t count, q4n
 
 q4nx_status q4nx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_blob, void* d_Y,
                       q4nx_dtype y_dtype, hipStream_t stream) {
-  return gemm_entry<kWQ4NX>(M, N, K, d_X, d_blob, d_Y, y_dtype, stream, "q4nx_gemm");
+  return gemm_entry<kWQ4NX>(M, N, K, d_X, d_blob, d_Y, y_dtype, nullptr, 0, stream, "q4nx_gemm");
 }
 
 q4nx_status q4nx_mx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_blob, void* d_Y,
                          q4nx_dtype y_dtype, hipStream_t stream) {
-  return gemm_entry<kWMX>(M, N, K, d_X, d_blob, d_Y, y_dtype, stream, "q4nx_mx_gemm");
+  return gemm_entry<kWMX>(M, N, K, d_X, d_blob, d_Y, y_dtype, nullptr, 0, stream, "q4nx_mx_gemm");
 }
 
 q4nx_status q4nx_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const uint16_t* d_W, void* d_Y,
                            q4nx_dtype y_dtype, hipStream_t stream) {
-  return gemm_entry<kWBf16>(M, N, K, d_X, d_W, d_Y, y_dtype, stream, "q4nx_gemm_bf16");
+  return gemm_entry<kWBf16>(M, N, K, d_X, d_W, d_Y, y_dtype, nullptr, 0, stream, "q4nx_gemm_bf16");
+}
+
+size_t q4nx_gemm_workspace_size(int64_t M, int64_t N, int64_t K) {
+  if (M <= 0 || N <= 0 || K <= 0 || K % kGroup != 0 || M > Q4NX_MAX_DIM || N > Q4NX_MAX_DIM || K > Q4NX_MAX_DIM ||
+      M * N > (int64_t(1) << 40))
+    return 0;
+  GemmRegion plan[2];
+  const int count = gemm_plan(M, N, K, device_cus(), true, plan);
+  return plan_work_bytes(plan, count);
+}
+
+q4nx_status q4nx_gemm_ex(q4nx_weights w_format, int64_t M, int64_t N, int64_t K, const uint16_t* d_X,
+                         const void* d_W, void* d_Y, q4nx_dtype y_dtype, void* d_work, size_t work_bytes,
+                         hipStream_t stream) {
+  switch (w_format) {
+    case Q4NX_WEIGHTS_Q4NX:
+      return gemm_entry<kWQ4NX>(M, N, K, d_X, d_W, d_Y, y_dtype, d_work, work_bytes, stream, "q4nx_gemm_ex");
+    case Q4NX_WEIGHTS_MXFP4:
+      return gemm_entry<kWMX>(M, N, K, d_X, d_W, d_Y, y_dtype, d_work, work_bytes, stream, "q4nx_gemm_ex");
+    case Q4NX_WEIGHTS_BF16:
+      return gemm_entry<kWBf16>(M, N, K, d_X, d_W, d_Y, y_dtype, d_work, work_bytes, stream, "q4nx_gemm_ex");
+    default:
+      clear_error();
+      return fail(Q4NX_ERR_INVALID_ARG, "q4nx_gemm_ex: unknown w_format");
+  }
 }
 
 }  // extern "C"

@@ -292,6 +292,29 @@ def test_mx_device_calls_validate_before_hip():
     assert L.q4nx_mx_gemm(4, 32, 256, A16, A16, A16, 3, None) == q4.Q4NX_ERR_INVALID_ARG
 
 
+def test_gemm_ex_workspace_size_and_validation():
+    """The split-K plan (device of 256 CUs: the planner's fallback without a
+    GPU) and every argument error of q4nx_gemm_ex before any launch."""
+    ws = q4.q4nx_gemm_workspace_size
+    for M, N, K in [(0, 256, 256), (4, 0, 256), (4, 32, 80), (-1, 32, 256), (4, 32, (1 << 30) + 32)]:
+        assert ws(M, N, K) == 0
+    assert ws(4096, 8192, 5376) == 0      # 512 tiles: two full rounds, nothing to split
+    w = ws(2048, 2560, 10240)             # 80 tiles over a long K: split
+    assert w > 0 and w % (4 * 2048 * 2560) == 0 and 2 <= w // (4 * 2048 * 2560) <= 4
+    L = q4.lib
+    args = lambda fmt, M, N, K, work, nbytes: (fmt, M, N, K, A16, A16, A16, 0, work, nbytes, None)
+    assert L.q4nx_gemm_ex(*args(3, 4, 32, 256, None, 0)) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_gemm_ex(*args(-1, 4, 32, 256, None, 0)) == q4.Q4NX_ERR_INVALID_ARG
+    for fmt in (q4.Q4NX_WEIGHTS_Q4NX, q4.Q4NX_WEIGHTS_MXFP4, q4.Q4NX_WEIGHTS_BF16):
+        assert L.q4nx_gemm_ex(*args(fmt, 0, 32, 256, None, 0)) == q4.Q4NX_ERR_SHAPE
+        assert L.q4nx_gemm_ex(*args(fmt, 4, 32, 80, None, 0)) == q4.Q4NX_ERR_SHAPE
+        assert L.q4nx_gemm_ex(fmt, 4, 32, 256, None, A16, A16, 0, None, 0, None) == q4.Q4NX_ERR_INVALID_ARG
+        assert L.q4nx_gemm_ex(fmt, 4, 32, 256, A16, MIS, A16, 0, None, 0, None) == q4.Q4NX_ERR_ALIGNMENT
+        assert L.q4nx_gemm_ex(*args(fmt, 2048, 2560, 10240, MIS, w)) == q4.Q4NX_ERR_ALIGNMENT
+        assert L.q4nx_gemm_ex(*args(fmt, 2048, 2560, 10240, A16, w - 1)) == q4.Q4NX_ERR_BUFFER_TOO_SMALL
+        assert L.q4nx_gemm_ex(*args(fmt, 2048, 2560, 10240, A16, 0)) == q4.Q4NX_ERR_BUFFER_TOO_SMALL
+
+
 def test_status_strings():
     for st in range(6):
         assert q4.lib.q4nx_status_str(st).decode()

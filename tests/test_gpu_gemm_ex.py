@@ -1,0 +1,139 @@
+"""q4nx_gemm_ex through the C ABI: the matrix product with a caller workspace,
+where the launch plan splits K for shapes with few output tiles.
+
+  * every case here takes a split plan (q4nx_gemm_workspace_size > 0), with
+    ragged M and N, K not a multiple of 64, float32 and bf16 outputs;
+  * parity with the float64 oracle: the projection tolerance and the tight
+    bound against the product of the bf16 weights;
+  * the three weight formats give the same bits for the same bf16 weights
+    (same plan, same partial products, same order of the final sum);
+  * the workspace starts filled with NaN, so a partial that is read before it
+    is written would show; repeated calls are bitwise identical;
+  * without a workspace the result equals q4nx_gemm bit for bit.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from workloads import gen_weights, gen_mx_weights, gen_activations
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def q4():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2602_06063_amd as mod
+    return mod
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def dev_u8(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def dev_bf16(bits):
+    return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).cuda().view(torch.bfloat16)
+
+
+def host_f32(t):
+    torch.cuda.synchronize()
+    return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
+
+
+def work_for(q4, M, N, K):
+    nbytes = q4.q4nx_gemm_workspace_size(M, N, K)
+    assert nbytes > 0, "this shape is meant to take a split-K plan"
+    return torch.full((nbytes // 4,), float("nan"), dtype=torch.float32, device="cuda")
+
+
+# (M, N, K, rows checked by the oracle: None = all)
+SPLIT_SHAPES = [(512, 512, 16384, None), (512, 512, 16352, None), (300, 520, 20000, None), (260, 257, 12000, None),
+                (1, 256, 20480, None), (2048, 2560, 10240, 64), (2048, 2560, 10208, 64), (4096, 5376, 21504, 48)]
+
+
+def _rows(M, n):
+    if n is None:
+        return None
+    rng = np.random.default_rng(M)
+    return np.unique(np.concatenate([np.arange(8), M - 8 + np.arange(8), rng.integers(0, M, n)]))
+
+
+@pytest.mark.parametrize("M,N,K,nrows", SPLIT_SHAPES)
+@pytest.mark.parametrize("bf16_out", [False, True])
+def test_gemm_ex_split_parity(q4, M, N, K, nrows, bf16_out):
+    _say("gemm_ex split", M, N, K, "bf16" if bf16_out else "f32")
+    codes, s, o = gen_weights(N, K, seed=M + K)
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    X = gen_activations((M, K), seed=N + K)
+    Y = torch.empty((M, N), dtype=torch.bfloat16 if bf16_out else torch.float32, device="cuda")
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, dev_bf16(X), blob, Y, work=work_for(q4, M, N, K))
+    Yh = host_f32(Y)
+    rows = _rows(M, nrows)
+    if rows is not None:
+        X, Yh = X[rows], Yh[rows]
+    w32 = oracle.dequant_f32(codes, s, o)
+    ok, worst = oracle.check_close(Yh, oracle.gemm_f64(X, w32), oracle.abs_bound(X, w32), bf16_out=bf16_out)
+    assert ok, worst
+    w16 = oracle.bf16_to_f32(oracle.f32_to_bf16(w32))
+    ref16 = oracle.gemm_f64(X, w16)
+    tight = np.abs(Yh.astype(np.float64) - ref16) <= (
+        1e-5 * oracle.abs_bound(X, w16) + 1e-6 + (2.0 ** -8 * np.abs(ref16) if bf16_out else 0))
+    assert tight.all()
+
+
+@pytest.mark.parametrize("M,N,K", [(300, 520, 20000), (260, 257, 12000), (2048, 2560, 10208)])
+def test_gemm_ex_formats_agree_bitwise(q4, M, N, K):
+    """Q4NX and MXFP4-variant blobs against the bf16 weights they dequantize
+    to, all through split plans: identical bits."""
+    _say("gemm_ex formats", M, N, K)
+    X = dev_bf16(gen_activations((M, K), seed=M))
+    work = work_for(q4, M, N, K)
+    W = torch.empty((N, K), dtype=torch.bfloat16, device="cuda")
+    Y1 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    Y2 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    codes, s, o = gen_weights(N, K, seed=K)
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, Y1, work=work)
+    q4.q4nx_dequant(blob, N, K, W)
+    work.fill_(float("nan"))
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_BF16, M, N, K, X, W, Y2, work=work)
+    torch.cuda.synchronize()
+    assert torch.equal(Y1.view(torch.int32), Y2.view(torch.int32))
+    mcodes, msc = gen_mx_weights(N, K, seed=K, mode="edge")
+    mblob = dev_u8(q4.q4nx_mx_pack(mcodes, msc))
+    work.fill_(float("nan"))
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_MXFP4, M, N, K, X, mblob, Y1, work=work)
+    q4.q4nx_mx_dequant(mblob, N, K, W)
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_BF16, M, N, K, X, W, Y2, work=work)
+    torch.cuda.synchronize()
+    assert torch.equal(Y1.view(torch.int32), Y2.view(torch.int32))
+    w32 = oracle.mx_dequant_f32(mcodes, msc)
+    Xh = gen_activations((M, K), seed=M)
+    ok, worst = oracle.check_close(host_f32(Y1), oracle.gemm_f64(Xh, w32), oracle.abs_bound(Xh, w32))
+    assert ok, worst
+
+
+def test_gemm_ex_repeatable_and_unsplit_without_workspace(q4):
+    M, N, K = 512, 512, 16352
+    _say("gemm_ex repeat / no workspace", M, N, K)
+    codes, s, o = gen_weights(N, K, seed=9)
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    X = dev_bf16(gen_activations((M, K), seed=9))
+    work = work_for(q4, M, N, K)
+    Ys = [torch.empty((M, N), dtype=torch.float32, device="cuda") for _ in range(4)]
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, Ys[0], work=work)
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, Ys[1], work=work)
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, Ys[2])      # no workspace: nothing split
+    q4.q4nx_gemm(M, N, K, X, blob, Ys[3])
+    torch.cuda.synchronize()
+    assert torch.equal(Ys[0].view(torch.int32), Ys[1].view(torch.int32))
+    assert torch.equal(Ys[2].view(torch.int32), Ys[3].view(torch.int32))
+    # split and unsplit differ only by the order of the float32 sums
+    d = (Ys[0] - Ys[3]).abs().max().item()
+    assert d <= 1e-4 * Ys[3].abs().max().item()
