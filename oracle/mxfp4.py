@@ -18,13 +18,16 @@ scale X = 2^(e - 127).  Reading used for the Q4NX-shaped variant:
     the shared exponent is floor(log2(amax)) - 2 (2 = the largest FP4
     exponent), clamped to [-100, 100] (0 for an all-zero group); each element
     is w / X rounded to the nearest FP4 value, ties to the even mantissa,
-    saturating at +-6.
+    saturating at +-6.  Inputs are first taken into the domain exactly as
+    for the Q4NX quantizer: NaN -> 0, everything else clamped to
+    [-2^100, 2^100].
 """
 from __future__ import annotations
 
 import numpy as np
 
 from .q4nx import BLOCK_ROWS, BLOCK_COLS, GROUP, GROUPS_PER_BLOCK_ROW, CODE_BYTES, _ceil_div
+from .quantize import clamp_weights
 
 MX_SCALE_BYTES = BLOCK_ROWS * GROUPS_PER_BLOCK_ROW  # 256 E8M0 bytes
 MX_BLOCK_BYTES = CODE_BYTES + MX_SCALE_BYTES        # 4352
@@ -109,7 +112,7 @@ def _round_fp4(r: np.ndarray) -> np.ndarray:
 
 def mx_quantize(W: np.ndarray):
     """float32 W[N][K] -> codes u8[N][K], E8M0 scales u8[N][K/32]."""
-    W = np.asarray(W, dtype=np.float64)
+    W = clamp_weights(W).astype(np.float64)
     N, K = W.shape
     g = W.reshape(N, K // GROUP, GROUP)
     amax = np.abs(g).max(axis=2)

@@ -91,3 +91,21 @@ def test_quantize_error_bound_and_zero_group():
     a = np.abs(W.astype(np.float64))
     bound = np.where(a <= 6 * X, X, a - 6 * X)   # half the largest FP4 spacing (2) below 6, saturation above
     assert (np.abs(w_hat - W) <= bound + 1e-30).all()
+
+
+def test_quantize_domain_and_exponent_clamps():
+    """Out-of-domain inputs follow the Q4NX quantizer's reading (NaN -> 0,
+    clamp to +-2^100); the shared exponent is clamped to [-100, 100]."""
+    W = np.zeros((1, 128), np.float32)
+    W[0, 0:32] = np.nan                       # group 0: all NaN -> an all-zero group
+    W[0, 32] = np.inf                         # group 1: clamped to 2^100 -> X = 2^98, code of 4.0
+    W[0, 33] = -np.inf
+    W[0, 64] = np.float32(2.0 ** -120)        # group 2: floor(log2) - 2 = -122 -> clamped to -100
+    W[0, 96] = np.float32(3.0)                # group 3: floor(log2 3) - 2 = -1 -> X = 1/2, 3 / (1/2) = 6
+    c, s = mx.mx_quantize(W)
+    assert s[0].tolist() == [127, 127 + 98, 27, 126]
+    assert (c[0, :32] == 0).all()
+    assert c[0, 32] == 6 and c[0, 33] == 14   # +4.0 and -4.0
+    assert c[0, 64] == 0                       # 2^-120 / 2^-100 rounds to 0
+    assert c[0, 96] == 7                       # 6.0
+    assert mx.mx_dequant_f32(c, s)[0, 32] == np.float32(2.0 ** 100)
