@@ -621,7 +621,20 @@ def main():
                  "GB_per_s": round(qbytes / (tq * 1e-3) / 1e9, 2),
                  "frac_hbm": round(qbytes / (tq * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                  "bytes": "4 B read + 0.625 B written per weight"}
-        del Wq, Bq
+        # The MXFP4 variant's quantizer on the same matrix.
+        Bm = torch.empty(q4.q4nx_mx_packed_size(Nq, Kq), dtype=torch.uint8, device="cuda")
+        sm = Step(q4, stream.cuda_stream)
+        sm.calls.append((q4.lib.q4nx_mx_quantize, (Wq.data_ptr(), Nq, Kq, Bm.data_ptr(), sm.s)))
+        for _ in range(args.warmup):
+            sm.run()
+        _, m_ms, _ = timed(lambda: None, sm.run, args.steps)
+        tm = mean(m_ms)
+        mbytes = Nq * Kq * (4 + MX_WEIGHT_BYTES)
+        quant["mxfp4"] = {"ms": round(tm, 4), "Gweights_per_s": round(Nq * Kq / (tm * 1e-3) / 1e9, 2),
+                          "GB_per_s": round(mbytes / (tm * 1e-3) / 1e9, 2),
+                          "frac_hbm": round(mbytes / (tm * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                          "bytes": "4 B read + 0.53125 B written per weight"}
+        del Wq, Bq, Bm
 
     fkv = None
     if args.flowkv and do_decode:

@@ -298,6 +298,16 @@ q4nx_status q4nx_mx_pack(const uint8_t* codes, const uint8_t* scales, int64_t N,
 q4nx_status q4nx_mx_unpack(const void* blob, size_t blob_bytes, int64_t N, int64_t K, uint8_t* codes,
                            uint8_t* scales);
 
+/* Device: float32 W [N][K] -> MXFP4-variant blob (the OCP MX v1.0 conversion):
+ * per group the shared exponent e = floor(log2 max|w|) - 2, clamped to
+ * [-100, 100] (0 for an all-zero group), and each element w / 2^e rounded to
+ * the nearest FP4 value, ties to the even mantissa, saturating at 6.  Inputs
+ * are first taken into the domain as by q4nx_quantize (NaN -> 0, clamp to
+ * +-2^100), so every input gives a valid blob; padding is code 0 with scale
+ * byte 127.  Arguments, alignment and errors as q4nx_quantize, with a blob of
+ * q4nx_mx_packed_size(N, K) bytes. */
+q4nx_status q4nx_mx_quantize(const float* d_W, int64_t N, int64_t K, void* d_blob, hipStream_t stream);
+
 /* Device: q4nx_dequant for an MXFP4-variant blob (exact values; bf16 exact too). */
 q4nx_status q4nx_mx_dequant(const void* d_blob, int64_t N, int64_t K, void* d_W, q4nx_dtype w_dtype,
                             hipStream_t stream);

@@ -34,7 +34,7 @@ Q4NX_WEIGHTS_BF16 = 2
 
 EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_quantize", "q4nx_dequant", "q4nx_gemv",
             "q4nx_gemv_batched", "q4nx_gemm", "q4nx_gemm_bf16", "q4nx_flowkv_workspace_size",
-            "q4nx_flowkv_decode", "q4nx_mx_packed_size", "q4nx_mx_pack", "q4nx_mx_unpack", "q4nx_mx_dequant",
+            "q4nx_flowkv_decode", "q4nx_mx_packed_size", "q4nx_mx_pack", "q4nx_mx_unpack", "q4nx_mx_quantize", "q4nx_mx_dequant",
             "q4nx_mx_gemv", "q4nx_mx_gemv_batched", "q4nx_mx_gemm", "q4nx_gemm_workspace_size", "q4nx_gemm_ex",
             "q4nx_status_str", "q4nx_last_error"]
 
@@ -88,6 +88,8 @@ lib.q4nx_mx_pack.argtypes = [_vp, _vp, _i64, _i64, _vp, _sz]
 lib.q4nx_mx_pack.restype = ctypes.c_int
 lib.q4nx_mx_unpack.argtypes = [_vp, _sz, _i64, _i64, _vp, _vp]
 lib.q4nx_mx_unpack.restype = ctypes.c_int
+lib.q4nx_mx_quantize.argtypes = [_vp, _i64, _i64, _vp, _vp]
+lib.q4nx_mx_quantize.restype = ctypes.c_int
 lib.q4nx_mx_dequant.argtypes = [_vp, _i64, _i64, _vp, ctypes.c_int, _vp]
 lib.q4nx_mx_dequant.restype = ctypes.c_int
 lib.q4nx_mx_gemv.argtypes = [_vp, _vp, _vp, ctypes.c_int, _i64, _i64, _vp]
@@ -265,6 +267,13 @@ def q4nx_gemm_bf16(M: int, N: int, K: int, X, W, Y, stream=None):
     _need(Y, M * N * Y.element_size(), "Y")
     _check(lib.q4nx_gemm_bf16(M, N, K, _dptr(X), _dptr(W), _dptr(Y), _dtype_code(Y), _stream(stream)),
            "q4nx_gemm_bf16")
+
+
+def q4nx_mx_quantize(W, N: int, K: int, blob, stream=None):
+    """blob <- MXFP4-variant quantization of the float32 weights W[N][K] (device)."""
+    _need(W, 4 * N * K, "W")
+    _need(blob, q4nx_mx_packed_size(N, K), "blob")
+    _check(lib.q4nx_mx_quantize(_dptr(W), N, K, _dptr(blob), _stream(stream)), "q4nx_mx_quantize")
 
 
 def q4nx_mx_dequant(blob, N: int, K: int, W, stream=None):

@@ -345,6 +345,64 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
   }
 }
 
+// q4nx_mx_quantize: float32 weights -> MXFP4-variant blob, with the lane
+// mapping of quantize_kernel.  Per group (OCP MX v1.0 conversion): inputs
+// taken into the domain as above; amax = max |w|; shared exponent
+// e = floor(log2 amax) - 2 (2 = the largest FP4 exponent), clamped to
+// [-100, 100], 0 for an all-zero group; each element w / 2^e rounded to the
+// nearest FP4 magnitude -- the midpoints of {0, .5, 1, 1.5, 2, 3, 4, 6} go to
+// the even mantissa -- saturating at 6, with the sign of w.  w / 2^e is exact
+// (a power-of-two scaling; a result below 2^-126 only ever rounds to 0).
+// The group maximum and the sign are read from the bit patterns, so that
+// denormal inputs give the same exponent and sign whatever the denormal mode.
+__device__ __forceinline__ uint32_t fp4_code(float w, float inv_x) {
+  const float a = fabsf(w) * inv_x;
+  const uint32_t m = (uint32_t)(a > 0.25f) + (uint32_t)(a >= 0.75f) + (uint32_t)(a > 1.25f) +
+                     (uint32_t)(a >= 1.75f) + (uint32_t)(a > 2.5f) + (uint32_t)(a >= 3.5f) + (uint32_t)(a > 5.0f);
+  const uint32_t bits = __float_as_uint(w);
+  return m | ((bits >> 31) && (bits & 0x7FFFFFFFu) ? 8u : 0u);  // -0 keeps code 0
+}
+
+__global__ __launch_bounds__(256) void mx_quantize_kernel(const float* __restrict__ W, int64_t N, int64_t K,
+                                                          int64_t KB, int64_t nblocks, uint8_t* __restrict__ blob) {
+  const int t = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int r = 8 * t + (lane >> 3), c = lane & 7;
+  for (int64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
+    const int64_t i = b / KB, j = b - i * KB;
+    const int64_t n = i * kBlockRows + r;
+    const int64_t k0 = j * kBlockCols + kGroup * c;
+    uint8_t* blk = blob + b * kMxBlockBytes;
+    u32x4 codes = (u32x4){0u, 0u, 0u, 0u};
+    uint32_t eb = kMxPadScale;  // padding: code 0 with scale 1
+    if (n < N && k0 < K) {
+      float w[32];
+      const f32x4* src = reinterpret_cast<const f32x4*>(W + n * K + k0);
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        const f32x4 x = src[v];
+        w[4 * v + 0] = x[0];
+        w[4 * v + 1] = x[1];
+        w[4 * v + 2] = x[2];
+        w[4 * v + 3] = x[3];
+      }
+      uint32_t amax = 0;  // bits of max |w|
+#pragma unroll
+      for (int e = 0; e < 32; ++e) {
+        const float x = w[e] != w[e] ? 0.0f : (fabsf(w[e]) > kQuantClamp ? copysignf(kQuantClamp, w[e]) : w[e]);
+        w[e] = x;
+        amax = max(amax, __float_as_uint(x) & 0x7FFFFFFFu);
+      }
+      const int ex = amax == 0 ? 0 : max(-100, min(100, (int)(amax >> 23) - 127 - 2));
+      eb = (uint32_t)(ex + 127);
+      const float inv_x = __uint_as_float((uint32_t)(127 - ex) << 23);  // 2^-ex
+#pragma unroll
+      for (int e = 0; e < 32; ++e) codes[e >> 3] |= fp4_code(w[e], inv_x) << (4 * (e & 7));
+    }
+    *reinterpret_cast<u32x4*>(blk + 1024 * t + 16 * lane) = codes;
+    blk[kCodeBytes + 64 * t + lane] = (uint8_t)eb;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // q4nx_gemv / q4nx_gemv_batched: FusedDQP
 // ---------------------------------------------------------------------------
@@ -1592,6 +1650,20 @@ q4nx_status q4nx_quantize(const float* d_W, int64_t N, int64_t K, void* d_blob, 
   hipLaunchKernelGGL(quantize_kernel, dim3((unsigned)grid), dim3(256), 0, stream, d_W, N, K, KB, nblocks,
                      static_cast<uint8_t*>(d_blob));
   return check_launch("q4nx_quantize");
+}
+
+q4nx_status q4nx_mx_quantize(const float* d_W, int64_t N, int64_t K, void* d_blob, hipStream_t stream) {
+  clear_error();
+  if (q4nx_status st = check_shape(N, K, "q4nx_mx_quantize")) return st;
+  if (!d_W || !d_blob) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_mx_quantize: NULL pointer");
+  if (!aligned(d_W, 16) || !aligned(d_blob, 16))
+    return fail(Q4NX_ERR_ALIGNMENT, "q4nx_mx_quantize: W and blob need 16-byte alignment");
+  const int64_t KB = ceil_div(K, kBlockCols);
+  const int64_t nblocks = ceil_div(N, kBlockRows) * KB;
+  const int64_t grid = std::min<int64_t>(nblocks, int64_t(1) << 20);
+  hipLaunchKernelGGL(mx_quantize_kernel, dim3((unsigned)grid), dim3(256), 0, stream, d_W, N, K, KB, nblocks,
+                     static_cast<uint8_t*>(d_blob));
+  return check_launch("q4nx_mx_quantize");
 }
 
 q4nx_status q4nx_gemv(const void* d_blob, const uint16_t* d_x, void* d_y, q4nx_dtype y_dtype, int64_t N,

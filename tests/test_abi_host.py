@@ -270,6 +270,11 @@ def test_mx_pack_error_paths():
 
 def test_mx_device_calls_validate_before_hip():
     L = q4.lib
+    assert L.q4nx_mx_quantize(A16, 32, 80, A16, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_mx_quantize(None, 32, 256, A16, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_mx_quantize(A16, 32, 256, None, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_mx_quantize(MIS, 32, 256, A16, None) == q4.Q4NX_ERR_ALIGNMENT
+    assert L.q4nx_mx_quantize(A16, 32, 256, MIS, None) == q4.Q4NX_ERR_ALIGNMENT
     assert L.q4nx_mx_dequant(None, 32, 256, A16, 0, None) == q4.Q4NX_ERR_INVALID_ARG
     assert L.q4nx_mx_dequant(A16, 32, 250, A16, 0, None) == q4.Q4NX_ERR_SHAPE
     assert L.q4nx_mx_dequant(MIS, 32, 256, A16, 0, None) == q4.Q4NX_ERR_ALIGNMENT

@@ -223,3 +223,47 @@ def test_mx_gemm_equals_dequant_then_gemm_bf16_bitwise(q4, M, N, K):
     q4.q4nx_gemm_bf16(M, N, K, X, W, Y2)
     torch.cuda.synchronize()
     assert torch.equal(Y1.view(torch.int32), Y2.view(torch.int32))
+
+
+# ----------------------------------------------------------------- quantizer
+def _mx_edge_weights(N, K, seed):
+    """Groups on the FP4 grid's midpoints (ties), saturating values, zeros,
+    signed zeros, tiny and huge magnitudes, NaN and infinities."""
+    rng = np.random.default_rng(seed)
+    W = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
+    mids = np.array([0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0, 7.0], np.float32)
+    for n in range(N):
+        for g in range(K // 32):
+            sl = W[n, 32 * g:32 * g + 32]
+            kind = rng.integers(0, 8)
+            X = np.float32(2.0 ** int(rng.integers(-20, 20)))
+            if kind == 1:
+                sl[:] = (mids[rng.integers(0, 8, 32)] * X * np.where(rng.random(32) < 0.5, -1, 1)).astype(np.float32)
+                sl[0] = 7.0 * X                                        # keeps the exponent at log2(X)
+            elif kind == 2:
+                sl[:] = 0.0
+                sl[5] = -0.0
+            elif kind == 3:
+                sl[:] = (rng.standard_normal(32) * 2.0 ** -110).astype(np.float32)   # exponent clamped at -100
+            elif kind == 4:
+                sl[:] = (rng.standard_normal(32) * 1e31).astype(np.float32)        # clamped to 2^100
+                sl[3], sl[4], sl[5] = np.inf, -np.inf, np.nan
+            elif kind == 5:
+                sl[:] = np.float32(1e-42)                                         # denormal inputs
+                sl[1] = -np.float32(1e-42)
+    return W
+
+
+@pytest.mark.parametrize("N,K,kind", [(1, 32, "normal"), (33, 288, "edge"), (64, 1152, "edge"),
+                                      (1024, 1152, "normal"), (2048, 5376, "normal"), (100, 21504, "edge")])
+def test_mx_quantize_bit_exact(q4, N, K, kind):
+    _say("mx quantize", N, K, kind)
+    if kind == "edge":
+        W = _mx_edge_weights(N, K, seed=N + K)
+    else:
+        W = (np.random.default_rng(N).standard_normal((N, K)) * 0.02).astype(np.float32)
+    want = oracle.mx_pack(*oracle.mx_quantize(W))
+    blob = torch.full((q4.q4nx_mx_packed_size(N, K),), 0xAB, dtype=torch.uint8, device="cuda")
+    q4.q4nx_mx_quantize(torch.from_numpy(W).cuda(), N, K, blob)
+    torch.cuda.synchronize()
+    assert np.array_equal(blob.cpu().numpy(), want)
