@@ -84,29 +84,10 @@ __device__ __forceinline__ float group_dot_bf16(u32x4 q, const uint32_t (&xp)[16
   return a + b;
 }
 
-// The 32 codes of one group as float32 values q * 2^-9 (exact), in column
-// order: one conversion turns two code bytes into two float32 values.
+// Two code bytes as two float32 values q * 2^-9 (exact) in one conversion.
 template <bool HI_WORD>
 __device__ __forceinline__ f32x2 codes2_f32(uint32_t bytes) {
   return __builtin_amdgcn_cvt_pk_f32_fp8(bytes, HI_WORD);
-}
-
-__device__ __forceinline__ void codes_to_f32_scaled(u32x4 q, float (&f)[32]) {
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const uint32_t lo = opaque(q[u] & 0x0F0F0F0Fu);          // columns 8u + 0, 2, 4, 6
-    const uint32_t hi = opaque((q[u] >> 4) & 0x0F0F0F0Fu);   // columns 8u + 1, 3, 5, 7
-    const f32x2 a = codes2_f32<false>(lo), b = codes2_f32<true>(lo);
-    const f32x2 e = codes2_f32<false>(hi), g = codes2_f32<true>(hi);
-    f[8 * u + 0] = a[0];
-    f[8 * u + 2] = a[1];
-    f[8 * u + 4] = b[0];
-    f[8 * u + 6] = b[1];
-    f[8 * u + 1] = e[0];
-    f[8 * u + 3] = e[1];
-    f[8 * u + 5] = g[0];
-    f[8 * u + 7] = g[1];
-  }
 }
 
 // Eq. 3 from a scaled code: (q 2^-9) * (d 2^9) is the exact product d*q (both
@@ -114,6 +95,21 @@ __device__ __forceinline__ void codes_to_f32_scaled(u32x4 q, float (&f)[32]) {
 // RN(d*q + m) -- the same bits as the plain definition.
 __device__ __forceinline__ float eq3(float q_scaled, float d_times_512, float m) {
   return fmaf(q_scaled, d_times_512, m);
+}
+
+// Dequantizes 8 consecutive weights (one 32-bit word of codes) of a group to
+// bf16 pairs in column order; d512 = d * 2^9 (see eq3).
+__device__ __forceinline__ u32x4 dequant8_bf16(uint32_t codes, float d512, float m) {
+  const uint32_t lo = opaque(codes & 0x0F0F0F0Fu);          // columns 0, 2, 4, 6
+  const uint32_t hi = opaque((codes >> 4) & 0x0F0F0F0Fu);   // columns 1, 3, 5, 7
+  const f32x2 a = codes2_f32<false>(lo), b = codes2_f32<true>(lo);
+  const f32x2 e = codes2_f32<false>(hi), g = codes2_f32<true>(hi);
+  u32x4 o;
+  o[0] = pack_bf16x2(eq3(a[0], d512, m), eq3(e[0], d512, m));
+  o[1] = pack_bf16x2(eq3(a[1], d512, m), eq3(e[1], d512, m));
+  o[2] = pack_bf16x2(eq3(b[0], d512, m), eq3(g[0], d512, m));
+  o[3] = pack_bf16x2(eq3(b[1], d512, m), eq3(g[1], d512, m));
+  return o;
 }
 
 // ---- MXFP4 variant of the block --------------------------------------------
@@ -171,82 +167,69 @@ constexpr int wblock_bytes() {
 }
 
 // ---------------------------------------------------------------------------
-// q4nx_dequant: Eq. 3 for every weight, written row-major [N][K]
+// q4nx_dequant / q4nx_mx_dequant: every weight, written row-major [N][K]
 // ---------------------------------------------------------------------------
-// One workgroup of 256 threads per block; thread (t, l) handles the group at
-// row 8t + l/8, columns 32(l%8)..+31.  Eight lanes write one row's 256
-// contiguous outputs.
+// One workgroup of 256 threads per block, 32 lanes per block row: lane j of a
+// row handles columns 8j..8j+7 (one 32-bit word of codes, in group j/4), so a
+// row's 32 lanes read 128 contiguous bytes of codes and write 512 (bf16) or
+// 1024 (float32) contiguous bytes -- every store instruction writes whole
+// lines.  Eight rows per pass, four passes per block.  (A lane per group, 64
+// bytes of output per lane, writes a quarter of every line per instruction and
+// ran at a fifth of this speed.)
+template <int F>
 __global__ __launch_bounds__(256) void dequant_kernel(const uint8_t* __restrict__ blob, int64_t N, int64_t K,
                                                       int64_t KB, int64_t nblocks, void* __restrict__ W,
                                                       int w_bf16) {
-  const int t = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int r = 8 * t + (lane >> 3), c = lane & 7;
+  constexpr int kBytes = wblock_bytes<F>();
+  const int lr = threadIdx.x >> 5, j = threadIdx.x & 31;
   for (int64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
-    const int64_t i = b / KB, j = b - i * KB;
-    const int64_t n = i * kBlockRows + r;
-    const int64_t k0 = j * kBlockCols + kGroup * c;
-    if (n >= N || k0 >= K) continue;
-    const uint8_t* blk = blob + b * kBlockBytes;
-    const u32x4 q = load_codes(blk + 1024 * t + 16 * lane);
-    const float d = bf16_to_f32(load_u16(blk + kCodeBytes + 2 * (64 * t + lane)));
-    const float m = bf16_to_f32(load_u16(blk + kCodeBytes + kScaleBytes + 2 * (64 * t + lane)));
-    float f[32];
-    codes_to_f32_scaled(q, f);
-    const float d512 = d * 512.0f;
+    const int64_t i = b / KB, jb = b - i * KB;
+    const int64_t k = jb * kBlockCols + 8 * j;
+    if (k >= K) continue;  // K is a multiple of 32: whole groups lie past K
+    const uint8_t* blk = blob + b * kBytes;
 #pragma unroll
-    for (int e = 0; e < 32; ++e) f[e] = eq3(f[e], d512, m);
-    if (w_bf16) {
-      u32x4* out = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(W) + n * K + k0);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        u32x4 o;
-        o[0] = pack_bf16x2(f[8 * v + 0], f[8 * v + 1]);
-        o[1] = pack_bf16x2(f[8 * v + 2], f[8 * v + 3]);
-        o[2] = pack_bf16x2(f[8 * v + 4], f[8 * v + 5]);
-        o[3] = pack_bf16x2(f[8 * v + 6], f[8 * v + 7]);
-        __builtin_nontemporal_store(o, out + v);
+    for (int pass = 0; pass < 4; ++pass) {
+      const int r = 8 * pass + lr;
+      const int64_t n = i * kBlockRows + r;
+      if (n >= N) break;
+      const uint32_t codes = *reinterpret_cast<const uint32_t*>(blk + 128 * r + 4 * j);
+      const int gi = kGroupsPerRow * r + (j >> 2);
+      u32x4 ob;
+      float of[8];
+      if constexpr (F == kWMX) {
+        const float X = e8m0_f32(blk[kCodeBytes + gi]);
+        if (w_bf16) {
+          ob = mx8_bf16(codes, X);
+        } else {
+          const f32x2 a = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, X, 0);
+          const f32x2 c = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, X, 1);
+          const f32x2 e = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, X, 2);
+          const f32x2 g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(codes, X, 3);
+          of[0] = a[0]; of[1] = a[1]; of[2] = c[0]; of[3] = c[1];
+          of[4] = e[0]; of[5] = e[1]; of[6] = g[0]; of[7] = g[1];
+        }
+      } else {
+        const float d512 = bf16_to_f32(*reinterpret_cast<const uint16_t*>(blk + kCodeBytes + 2 * gi)) * 512.0f;
+        const float m = bf16_to_f32(*reinterpret_cast<const uint16_t*>(blk + kCodeBytes + kScaleBytes + 2 * gi));
+        if (w_bf16) {
+          ob = dequant8_bf16(codes, d512, m);
+        } else {
+          const uint32_t lo = opaque(codes & 0x0F0F0F0Fu);          // columns 0, 2, 4, 6
+          const uint32_t hi = opaque((codes >> 4) & 0x0F0F0F0Fu);   // columns 1, 3, 5, 7
+          const f32x2 a = codes2_f32<false>(lo), c = codes2_f32<true>(lo);
+          const f32x2 e = codes2_f32<false>(hi), g = codes2_f32<true>(hi);
+          of[0] = eq3(a[0], d512, m); of[1] = eq3(e[0], d512, m);
+          of[2] = eq3(a[1], d512, m); of[3] = eq3(e[1], d512, m);
+          of[4] = eq3(c[0], d512, m); of[5] = eq3(g[0], d512, m);
+          of[6] = eq3(c[1], d512, m); of[7] = eq3(g[1], d512, m);
+        }
       }
-    } else {
-      f32x4* out = reinterpret_cast<f32x4*>(static_cast<float*>(W) + n * K + k0);
-#pragma unroll
-      for (int v = 0; v < 8; ++v) {
-        f32x4 o = {f[4 * v + 0], f[4 * v + 1], f[4 * v + 2], f[4 * v + 3]};
-        __builtin_nontemporal_store(o, out + v);
-      }
-    }
-  }
-}
-
-// q4nx_mx_dequant: w = X * fp4(q) for every weight of an MXFP4-variant blob,
-// with the lane mapping of dequant_kernel.
-__global__ __launch_bounds__(256) void mx_dequant_kernel(const uint8_t* __restrict__ blob, int64_t N, int64_t K,
-                                                         int64_t KB, int64_t nblocks, void* __restrict__ W,
-                                                         int w_bf16) {
-  const int t = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int r = 8 * t + (lane >> 3), c = lane & 7;
-  for (int64_t b = blockIdx.x; b < nblocks; b += gridDim.x) {
-    const int64_t i = b / KB, j = b - i * KB;
-    const int64_t n = i * kBlockRows + r;
-    const int64_t k0 = j * kBlockCols + kGroup * c;
-    if (n >= N || k0 >= K) continue;
-    const uint8_t* blk = blob + b * kMxBlockBytes;
-    const u32x4 q = load_codes(blk + 1024 * t + 16 * lane);
-    const float X = e8m0_f32(load_u8(blk + kCodeBytes + 64 * t + lane));
-    if (w_bf16) {
-      u32x4* out = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(W) + n * K + k0);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) __builtin_nontemporal_store(mx8_bf16(q[v], X), out + v);
-    } else {
-      f32x4* out = reinterpret_cast<f32x4*>(static_cast<float*>(W) + n * K + k0);
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const uint32_t w = q[v];
-        const f32x2 a = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, X, 0);
-        const f32x2 b = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, X, 1);
-        const f32x2 e = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, X, 2);
-        const f32x2 g = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, X, 3);
-        __builtin_nontemporal_store((f32x4){a[0], a[1], b[0], b[1]}, out + 2 * v);
-        __builtin_nontemporal_store((f32x4){e[0], e[1], g[0], g[1]}, out + 2 * v + 1);
+      if (w_bf16) {
+        *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(W) + n * K + k) = ob;
+      } else {
+        f32x4* out = reinterpret_cast<f32x4*>(static_cast<float*>(W) + n * K + k);
+        out[0] = (f32x4){of[0], of[1], of[2], of[3]};
+        out[1] = (f32x4){of[4], of[5], of[6], of[7]};
       }
     }
   }
@@ -703,20 +686,6 @@ __device__ __forceinline__ void gemm_tile_of(int wg, int ntiles, int tiles_n, in
   bn = r / rows;
 }
 
-// Dequantizes 8 consecutive weights (one 32-bit word of codes) of a group to
-// bf16 pairs in column order; d512 = d * 2^9 (see eq3).
-__device__ __forceinline__ u32x4 dequant8_bf16(uint32_t codes, float d512, float m) {
-  const uint32_t lo = opaque(codes & 0x0F0F0F0Fu);          // columns 0, 2, 4, 6
-  const uint32_t hi = opaque((codes >> 4) & 0x0F0F0F0Fu);   // columns 1, 3, 5, 7
-  const f32x2 a = codes2_f32<false>(lo), b = codes2_f32<true>(lo);
-  const f32x2 e = codes2_f32<false>(hi), g = codes2_f32<true>(hi);
-  u32x4 o;
-  o[0] = pack_bf16x2(eq3(a[0], d512, m), eq3(e[0], d512, m));
-  o[1] = pack_bf16x2(eq3(a[1], d512, m), eq3(e[1], d512, m));
-  o[2] = pack_bf16x2(eq3(b[0], d512, m), eq3(g[0], d512, m));
-  o[3] = pack_bf16x2(eq3(b[1], d512, m), eq3(g[1], d512, m));
-  return o;
-}
 
 // ---- 256 x 256 tile, one wave per SIMD ------------------------------------
 // Four waves in a 2 x 2 grid, each owning a 128 x 128 sub-tile: 16 MFMA
@@ -1613,12 +1582,8 @@ static q4nx_status dequant_entry(const void* d_blob, int64_t N, int64_t K, void*
   const int64_t grid = std::min<int64_t>(nblocks, int64_t(1) << 20);
   const uint8_t* blob = static_cast<const uint8_t*>(d_blob);
   const int w_bf16 = (w_dtype == Q4NX_BF16);
-  if constexpr (F == kWMX)
-    hipLaunchKernelGGL(mx_dequant_kernel, dim3((unsigned)grid), dim3(256), 0, stream, blob, N, K, KB, nblocks, d_W,
-                       w_bf16);
-  else
-    hipLaunchKernelGGL(dequant_kernel, dim3((unsigned)grid), dim3(256), 0, stream, blob, N, K, KB, nblocks, d_W,
-                       w_bf16);
+  hipLaunchKernelGGL(dequant_kernel<F>, dim3((unsigned)grid), dim3(256), 0, stream, blob, N, K, KB, nblocks, d_W,
+                     w_bf16);
   return check_launch(fn);
 }
 
