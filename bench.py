@@ -11,7 +11,9 @@ One step = one pass of the whole path over one batch of synthetic input:
     out (a stacked Q4NX matrix is the projections' blobs back to back, since
     blocks are stored strip by strip and every N is a multiple of 32); each
     GEMM is q4nx_gemm_ex with a workspace, so shapes with few output tiles
-    over a long K (the down projections) are split along K.
+    over a long K (the down projections) are split along K, and at M = 4096
+    the Q4NX weights are dequantized to bf16 once per product before the
+    bf16 plan runs (same bits as the fused kernel).
 Inputs (packed weights, activations) are resident in HBM before the timed
 region; every (layer, projection) has its own independently seeded weights and
 activations.  Timing uses HIP events on the stream the kernels run on.
@@ -72,6 +74,8 @@ def parse():
     ap.add_argument("--pmc-pass", action="store_true",
                     help="run one eager decode step, one prefill step and a 1 GiB device copy (for rocprofv3 "
                          "counter passes), then exit")
+    ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_JSON"),
+                    help="summarise a rocprofv3 --kernel-trace --stats run of this benchmark as markdown")
     ap.add_argument("--pmc-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "MFMA_DIR"),
                     help="summarise three rocprofv3 --pmc output folders of a --pmc-pass run as markdown")
     return ap.parse_args()
@@ -136,8 +140,8 @@ class Step:
         self.wformat = q4.Q4NX_WEIGHTS_MXFP4 if mx else q4.Q4NX_WEIGHTS_Q4NX
         self.work = None  # GEMM workspace (q4nx_gemm_ex may split K with it), shared by the step's launches
 
-    def _work(self, M, N, K):
-        need = self.q4.q4nx_gemm_workspace_size(M, N, K)
+    def _work(self, fmt, M, N, K):
+        need = self.q4.q4nx_gemm_workspace_size(fmt, M, N, K)
         have = 0 if self.work is None else self.work.numel() * 4
         if need > have:
             raise ValueError(f"GEMM workspace: {have} bytes, {M}x{N}x{K} needs {need}")
@@ -157,7 +161,7 @@ class Step:
         self.q4._need(blob, self.size(N, K), "blob")
         self.q4._need(X, 2 * M * K, "X")
         self.q4._need(Y, M * N * Y.element_size(), "Y")
-        wp, wn = self._work(M, N, K)
+        wp, wn = self._work(self.wformat, M, N, K)
         self.calls.append((self.q4.lib.q4nx_gemm_ex, (self.wformat, M, N, K, X.data_ptr(), blob.data_ptr(),
                                                       Y.data_ptr(), ydt, wp, wn, self.s)))
 
@@ -170,7 +174,7 @@ class Step:
         self.q4._need(W, 2 * N * K, "W")
         self.q4._need(X, 2 * M * K, "X")
         self.q4._need(Y, M * N * Y.element_size(), "Y")
-        wp, wn = self._work(M, N, K)
+        wp, wn = self._work(self.q4.Q4NX_WEIGHTS_BF16, M, N, K)
         self.calls.append((self.q4.lib.q4nx_gemm_ex, (self.q4.Q4NX_WEIGHTS_BF16, M, N, K, X.data_ptr(), W.data_ptr(),
                                                       Y.data_ptr(), ydt, wp, wn, self.s)))
 
@@ -249,11 +253,59 @@ def traffic_file(config):
 
 
 def kernel_family(name):
-    if "gemm256_kernel" in name or "gemm_kernel" in name:
+    if "gemm256_kernel" in name or "gemm_kernel" in name or "splitk_sum_kernel" in name:
         return "gemm"
     if "gemv_kernel" in name:
         return "gemv"
     return None
+
+
+def trace_summary(trace_dir, bench_json):
+    """Markdown summary of a rocprofv3 --kernel-trace --stats run of this
+    benchmark (its *kernel_stats.csv) next to the JSON line the same run
+    printed: per-kernel calls and durations, and the per-step time of the
+    roofline kernels against the benchmark's own HIP-event time."""
+    import csv
+    import glob
+    paths = glob.glob(os.path.join(trace_dir, "**", "*kernel_stats.csv"), recursive=True)
+    if not paths:
+        raise SystemExit(f"no *kernel_stats.csv under {trace_dir}")
+    rows = list(csv.DictReader(open(paths[0])))
+    r = json.loads(open(bench_json).read().strip().splitlines()[-1])
+    runs = r["warmup"] + r["steps"]
+    kern = [(row["Name"], int(row["Calls"]), float(row["TotalDurationNs"]) / 1e6) for row in rows]
+    total = sum(k[2] for k in kern)
+    out = ["| kernel | calls | avg (us) | total (ms) | share |", "|---|---:|---:|---:|---:|"]
+    for n, c, t in sorted(kern, key=lambda k: -k[2])[:14]:
+        short = n.split("(")[0].replace("q4nx::", "")
+        out.append(f"| `{short[:90]}` | {c} | {1e3 * t / c:.1f} | {t:.1f} | {100 * t / total:.2f}% |")
+    lines = ["\n".join(out), ""]
+    # The prefill step's kernels: the products, their partial sums and, where a
+    # Q4NX product dequantizes first, the dequant pass.  Other steps that use
+    # them (the two-phase comparison, the MXFP4 variant) must be off in the
+    # profiled run, or the attribution would mix them in.
+    if r.get("prefill", {}).get("two_phase") or "prefill" in (r.get("mxfp4") or {}):
+        raise SystemExit("profile with --two-phase 0 --mx 0: those steps launch the same kernels")
+    fam = ("gemm256_kernel", "gemm_kernel", "splitk_sum_kernel", "dequant_kernel")
+    gemm = [(n, c, t) for n, c, t in kern if any(f in n.split("(")[0] for f in fam)]
+    gemm_t, gemm_c = sum(k[2] for k in gemm), sum(k[1] for k in gemm)
+    if "prefill" in r:
+        per = gemm_t / runs
+        tflop = r["prefill"]["TFLOP"]
+        lines.append(f"Prefill kernels ({', '.join('`' + f + '`' for f in fam)}): {gemm_c} launches, "
+                     f"{gemm_t:.1f} ms over the {runs} runs of the prefill step (warm-up + timed) = {per:.2f} ms "
+                     f"per step; the benchmark's HIP-event time of the step: {r['prefill']['ms']:.2f} ms.")
+        lines.append(f"Achieved: {tflop:.2f} TFLOP per step / {per:.2f} ms = {tflop / per * 1e3:.0f} TFLOP/s "
+                     f"(benchmark: {r['prefill']['TFLOP_per_s']:.0f} TFLOP/s, "
+                     f"{100 * r['prefill']['frac_mfma']:.1f}% of {BF16_MFMA_PEAK_TFLOPS} TFLOP/s dense bf16).")
+    gv = [(n, c, t) for n, c, t in kern if "gemv_kernel" in n.split("(")[0] and n.split("(")[0].rstrip().endswith("1>")]
+    if gv and "decode" in r:
+        c = sum(k[1] for k in gv)
+        t = sum(k[2] for k in gv)
+        lines.append(f"Q4NX GEMV (`gemv_kernel<.., .., 1>`): {c} launches, average {1e3 * t / c:.1f} us; decode step "
+                     f"({r['decode']['launch']}): {r['decode']['ms']:.3f} ms for {r['decode']['weight_GB']:.3f} GB "
+                     f"= {r['decode']['GB_per_s']:.0f} GB/s ({100 * r['decode']['frac_hbm']:.1f}% of 8 TB/s).")
+    return "\n".join(lines) + "\n"
 
 
 def read_pmc(folder):
@@ -359,6 +411,9 @@ def main():
     if args.pmc_summary:
         print(pmc_summary(args.config, *args.pmc_summary))
         return
+    if args.trace_summary:
+        print(trace_summary(*args.trace_summary), end="")
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: this build measures the single-GPU path "
@@ -428,8 +483,10 @@ def main():
         Xs = {}
         Ys = [torch.empty((M_pre, N), dtype=torch.float32, device="cuda") for N, _ in shapes]
         Wtmp = torch.empty(max(N * K for N, K in shapes), dtype=torch.bfloat16, device="cuda")
-        # One split-K workspace for every GEMM of the step (they run one after another).
-        work_bytes = max(q4.q4nx_gemm_workspace_size(M_pre, N, K) for N, K in shapes)
+        # One workspace for every GEMM of the steps (they run one after another):
+        # split-K partials, and bf16 W where a Q4NX product dequantizes first.
+        work_bytes = max(q4.q4nx_gemm_workspace_size(f, M_pre, N, K) for N, K in shapes
+                         for f in (q4.Q4NX_WEIGHTS_Q4NX, q4.Q4NX_WEIGHTS_MXFP4, q4.Q4NX_WEIGHTS_BF16))
         gemm_work = torch.empty(max(work_bytes // 4, 1), dtype=torch.float32, device="cuda")
         pre.work = two.work = mpre.work = gemm_work
         for l in range(L):
@@ -729,7 +786,7 @@ def main():
             result["value_gemm"] = round(pre_tflops, 2)
     # Dominant kernel by time: the GEMM when the step has a prefill chunk.
     if do_prefill:
-        result["roofline"] = {"kernel": "q4nx_gemm_ex launches (gemm256_kernel, gemm_kernel, splitk_sum_kernel)", "bound": "mfma", "achieved": round(pre_tflops, 2),
+        result["roofline"] = {"kernel": "q4nx_gemm_ex launches (gemm256_kernel, gemm_kernel, splitk_sum_kernel, dequant_kernel)", "bound": "mfma", "achieved": round(pre_tflops, 2),
                               "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                               "frac": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
                               "algorithmic_bytes": round(alg_pre)}

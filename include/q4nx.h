@@ -256,22 +256,26 @@ q4nx_status q4nx_flowkv_decode(const uint16_t* d_q, const uint16_t* d_k, const u
  * w_format:  which of the three weight operands d_W is (a Q4NX blob, an
  *            MXFP4-variant blob, or bf16 [N][K]); other arguments as there.
  * d_work:    NULL, or device memory of at least
- *            q4nx_gemm_workspace_size(M, N, K) bytes (16-byte aligned),
- *            owned by the caller and used only while the call's launches run
- *            on `stream`; calls that overlap on one workspace race.
+ *            q4nx_gemm_workspace_size(w_format, M, N, K) bytes (16-byte
+ *            aligned), owned by the caller and used only while the call's
+ *            launches run on `stream`; calls that overlap on one workspace
+ *            race.
  * With a workspace the launch plan may split K for shapes with few output
  * tiles: each tile is then computed as up to 4 K segments whose float32
  * partial products are added in segment order by a second launch, so results
  * are deterministic but may differ in the last bits from the unsplit
- * product.  With d_work == NULL nothing is split and the result equals the
- * matching entry point's bit for bit.  Errors: as q4nx_gemm;
- * Q4NX_ERR_BUFFER_TOO_SMALL if work_bytes is below the plan's need.
+ * product.  For Q4NX weights and a large M it may also dequantize W to bf16
+ * in the workspace first (each weight once instead of once per row of output
+ * tiles) and run the same plan on those weights, which gives the same bits as
+ * the fused kernel.  With d_work == NULL nothing is split or staged and the
+ * result equals the matching entry point's bit for bit.  Errors: as
+ * q4nx_gemm; Q4NX_ERR_BUFFER_TOO_SMALL if work_bytes is below the need.
  */
 typedef enum { Q4NX_WEIGHTS_Q4NX = 0, Q4NX_WEIGHTS_MXFP4 = 1, Q4NX_WEIGHTS_BF16 = 2 } q4nx_weights;
 
-/* Bytes of workspace q4nx_gemm_ex may use for (M, N, K) on the current device
- * (0 when its plan splits nothing, or if the shape is invalid). */
-size_t q4nx_gemm_workspace_size(int64_t M, int64_t N, int64_t K);
+/* Bytes of workspace q4nx_gemm_ex may use for (w_format, M, N, K) on the
+ * current device (0 when it would use none, or if an argument is invalid). */
+size_t q4nx_gemm_workspace_size(q4nx_weights w_format, int64_t M, int64_t N, int64_t K);
 
 q4nx_status q4nx_gemm_ex(q4nx_weights w_format, int64_t M, int64_t N, int64_t K, const uint16_t* d_X,
                          const void* d_W, void* d_Y, q4nx_dtype y_dtype, void* d_work, size_t work_bytes,

@@ -98,7 +98,7 @@ lib.q4nx_mx_gemv_batched.argtypes = [ctypes.POINTER(q4nx_gemv_desc), _i32, ctype
 lib.q4nx_mx_gemv_batched.restype = ctypes.c_int
 lib.q4nx_mx_gemm.argtypes = [_i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp]
 lib.q4nx_mx_gemm.restype = ctypes.c_int
-lib.q4nx_gemm_workspace_size.argtypes = [_i64, _i64, _i64]
+lib.q4nx_gemm_workspace_size.argtypes = [ctypes.c_int, _i64, _i64, _i64]
 lib.q4nx_gemm_workspace_size.restype = _sz
 lib.q4nx_gemm_ex.argtypes = [ctypes.c_int, _i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp, _sz, _vp]
 lib.q4nx_gemm_ex.restype = ctypes.c_int
@@ -316,13 +316,14 @@ def q4nx_mx_gemm(M: int, N: int, K: int, X, blob, Y, stream=None):
            "q4nx_mx_gemm")
 
 
-def q4nx_gemm_workspace_size(M: int, N: int, K: int) -> int:
-    return int(lib.q4nx_gemm_workspace_size(M, N, K))
+def q4nx_gemm_workspace_size(w_format: int, M: int, N: int, K: int) -> int:
+    return int(lib.q4nx_gemm_workspace_size(w_format, M, N, K))
 
 
 def q4nx_gemm_ex(w_format: int, M: int, N: int, K: int, X, W, Y, work=None, stream=None):
     """Y[M][N] <- X[M][K] W^T for W in the given format (Q4NX_WEIGHTS_*); with a
-    workspace of q4nx_gemm_workspace_size(M, N, K) bytes the plan may split K."""
+    workspace of q4nx_gemm_workspace_size(w_format, M, N, K) bytes the plan may
+    split K and, for Q4NX weights and a large M, dequantize W to bf16 first."""
     wbytes = {Q4NX_WEIGHTS_Q4NX: q4nx_packed_size(N, K), Q4NX_WEIGHTS_MXFP4: q4nx_mx_packed_size(N, K),
               Q4NX_WEIGHTS_BF16: 2 * N * K}.get(w_format, 0)
     _need(W, wbytes, "W")

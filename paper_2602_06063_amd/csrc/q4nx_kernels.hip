@@ -1307,7 +1307,8 @@ static int device_cus() {
 // so a shape with 336 256x256 tiles on 256 CUs is better done as one full
 // round of 256 x 256 tiles and the rest in smaller tiles.  With split_ok, the
 // whole product or the second region may also be split along K.
-static int gemm_plan(int64_t M, int64_t N, int64_t K, int cus, bool split_ok, GemmRegion (&plan)[2]) {
+static int gemm_plan(int64_t M, int64_t N, int64_t K, int cus, bool split_ok, GemmRegion (&plan)[2],
+                     double* est_us = nullptr) {
   const auto rounds = [&](int t, int64_t m, int64_t n) {
     return (double)ceil_div(ceil_div(m, kGemmTiles[t].bm) * ceil_div(n, kGemmTiles[t].bn), cus);
   };
@@ -1367,6 +1368,7 @@ static int gemm_plan(int64_t M, int64_t N, int64_t K, int cus, bool split_ok, Ge
       }
     }
   }
+  if (est_us) *est_us = best * round_us(K);
   return count;
 }
 
@@ -1377,6 +1379,38 @@ static size_t plan_work_bytes(const GemmRegion* plan, int count) {
   for (int i = 0; i < count; ++i)
     if (plan[i].ks > 1) b = std::max(b, (size_t)plan[i].ks * (size_t)plan[i].M * (size_t)plan[i].N * sizeof(float));
   return b;
+}
+
+// Dequantize, then multiply.  The fused kernel dequantizes every weight once
+// per row of output tiles (16 times at M = 4096).  With a workspace that holds
+// W in bf16, a Q4NX product can dequantize each weight once instead (the
+// dequant kernel streams at ~5.5 TB/s) and run the same plan on the bf16
+// weights: the same bf16 values, the same MFMA chains and partial sums, so
+// the same bits.  On MI355X the bf16 product takes 0.85-0.93 of the fused
+// one's time, so the two-phase route is taken when the dequantization pass is
+// estimated below a tenth of the planned fused time -- the Gemma3 27B prefill
+// chunk (M = 4096) qualifies, M <= 2048 does not.  (The MXFP4 variant's
+// conversion is cheap enough that the fused kernel runs at the bf16 speed.)
+constexpr double kDequantLaunchUs = 3.0, kDequantBytesPerUs = 5.5e6, kTwoPhaseMaxShare = 0.10;
+
+struct GemmChoice {
+  GemmRegion plan[2];
+  int count;
+  bool two_phase;
+  size_t w_bytes;     // bf16 W at the start of the workspace (two-phase only)
+  size_t part_bytes;  // split-K partial products after it
+};
+
+static GemmChoice gemm_choose(int wf, int64_t M, int64_t N, int64_t K, bool have_work) {
+  GemmChoice c{};
+  double est_us = 0.0;
+  c.count = gemm_plan(M, N, K, device_cus(), have_work, c.plan, &est_us);
+  c.part_bytes = plan_work_bytes(c.plan, c.count);
+  const double deq_us = kDequantLaunchUs + (kBlockBytes / (double)(kBlockRows * kBlockCols) + 2.0) * (double)N *
+                                               (double)K / kDequantBytesPerUs;
+  c.two_phase = have_work && wf == kWQ4NX && deq_us < kTwoPhaseMaxShare * est_us;
+  c.w_bytes = c.two_phase ? (size_t)ceil_div(N * K * 2, 256) * 256 : 0;
+  return c;
 }
 
 template <int BM, int BN, int WAVES_M, int WAVES_N, int WF>
@@ -1472,13 +1506,22 @@ static q4nx_status gemm_entry(int64_t M, int64_t N, int64_t K, const uint16_t* d
                                                                     : ": X, W and Y need 16-byte alignment"));
   if (M * N > (int64_t(1) << 40)) return fail(Q4NX_ERR_SHAPE, std::string(fn) + ": problem too large for one launch");
   if (d_work && !aligned(d_work, 16)) return fail(Q4NX_ERR_ALIGNMENT, std::string(fn) + ": work needs 16-byte alignment");
-  GemmRegion plan[2];
-  const int count = gemm_plan(M, N, K, device_cus(), d_work != nullptr, plan);
-  if (plan_work_bytes(plan, count) > work_bytes)
-    return fail(Q4NX_ERR_BUFFER_TOO_SMALL, std::string(fn) + ": work_bytes < q4nx_gemm_workspace_size(M, N, K)");
+  const GemmChoice c = gemm_choose(WF, M, N, K, d_work != nullptr);
+  if (c.w_bytes + c.part_bytes > work_bytes)
+    return fail(Q4NX_ERR_BUFFER_TOO_SMALL, std::string(fn) + ": work_bytes < q4nx_gemm_workspace_size(...)");
+  const int y_bf16 = y_dtype == Q4NX_BF16;
+  float* part = reinterpret_cast<float*>(static_cast<uint8_t*>(d_work) + c.w_bytes);
   q4nx_status st = Q4NX_OK;
-  for (int i = 0; i < count && st == Q4NX_OK; ++i)
-    st = launch_region<WF>(plan[i], N, K, d_X, d_W, d_Y, y_dtype == Q4NX_BF16, stream, static_cast<float*>(d_work));
+  if (c.two_phase) {
+    const int64_t KB = ceil_div(K, kBlockCols), nblocks = ceil_div(N, kBlockRows) * KB;
+    hipLaunchKernelGGL(dequant_kernel<kWQ4NX>, dim3((unsigned)std::min<int64_t>(nblocks, int64_t(1) << 20)),
+                       dim3(256), 0, stream, static_cast<const uint8_t*>(d_W), N, K, KB, nblocks, d_work, 1);
+    for (int i = 0; i < c.count && st == Q4NX_OK; ++i)
+      st = launch_region<kWBf16>(c.plan[i], N, K, d_X, d_work, d_Y, y_bf16, stream, part);
+  } else {
+    for (int i = 0; i < c.count && st == Q4NX_OK; ++i)
+      st = launch_region<WF>(c.plan[i], N, K, d_X, d_W, d_Y, y_bf16, stream, part);
+  }
   if (st != Q4NX_OK) return st;
   return check_launch(fn);
 }
@@ -1668,13 +1711,19 @@ q4nx_status q4nx_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* d_X,
   return gemm_entry<kWBf16>(M, N, K, d_X, d_W, d_Y, y_dtype, nullptr, 0, stream, "q4nx_gemm_bf16");
 }
 
-size_t q4nx_gemm_workspace_size(int64_t M, int64_t N, int64_t K) {
+size_t q4nx_gemm_workspace_size(q4nx_weights w_format, int64_t M, int64_t N, int64_t K) {
   if (M <= 0 || N <= 0 || K <= 0 || K % kGroup != 0 || M > Q4NX_MAX_DIM || N > Q4NX_MAX_DIM || K > Q4NX_MAX_DIM ||
       M * N > (int64_t(1) << 40))
     return 0;
-  GemmRegion plan[2];
-  const int count = gemm_plan(M, N, K, device_cus(), true, plan);
-  return plan_work_bytes(plan, count);
+  int wf;
+  switch (w_format) {
+    case Q4NX_WEIGHTS_Q4NX: wf = kWQ4NX; break;
+    case Q4NX_WEIGHTS_MXFP4: wf = kWMX; break;
+    case Q4NX_WEIGHTS_BF16: wf = kWBf16; break;
+    default: return 0;
+  }
+  const GemmChoice c = gemm_choose(wf, M, N, K, true);
+  return c.w_bytes + c.part_bytes;
 }
 
 q4nx_status q4nx_gemm_ex(q4nx_weights w_format, int64_t M, int64_t N, int64_t K, const uint16_t* d_X,

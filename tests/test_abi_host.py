@@ -301,11 +301,18 @@ def test_gemm_ex_workspace_size_and_validation():
     """The split-K plan (device of 256 CUs: the planner's fallback without a
     GPU) and every argument error of q4nx_gemm_ex before any launch."""
     ws = q4.q4nx_gemm_workspace_size
+    Q, MX, BF = q4.Q4NX_WEIGHTS_Q4NX, q4.Q4NX_WEIGHTS_MXFP4, q4.Q4NX_WEIGHTS_BF16
     for M, N, K in [(0, 256, 256), (4, 0, 256), (4, 32, 80), (-1, 32, 256), (4, 32, (1 << 30) + 32)]:
-        assert ws(M, N, K) == 0
-    assert ws(4096, 8192, 5376) == 0      # 512 tiles: two full rounds, nothing to split
-    w = ws(2048, 2560, 10240)             # 80 tiles over a long K: split
+        assert ws(Q, M, N, K) == 0
+    assert ws(7, 2048, 2560, 10240) == 0  # unknown format
+    for f in (MX, BF):
+        assert ws(f, 4096, 8192, 5376) == 0   # 512 tiles: two full rounds, nothing to split
+    # Q4NX at M = 4096: W is dequantized to bf16 in the workspace first
+    assert ws(Q, 4096, 8192, 5376) == 8192 * 5376 * 2
+    assert ws(Q, 2048, 20480, 2560) == 0      # M = 2048: the fused kernel
+    w = ws(BF, 2048, 2560, 10240)             # 80 tiles over a long K: split
     assert w > 0 and w % (4 * 2048 * 2560) == 0 and 2 <= w // (4 * 2048 * 2560) <= 4
+    assert ws(Q, 2048, 2560, 10240) == w and ws(MX, 2048, 2560, 10240) == w
     L = q4.lib
     args = lambda fmt, M, N, K, work, nbytes: (fmt, M, N, K, A16, A16, A16, 0, work, nbytes, None)
     assert L.q4nx_gemm_ex(*args(3, 4, 32, 256, None, 0)) == q4.Q4NX_ERR_INVALID_ARG

@@ -9,7 +9,9 @@ where the launch plan splits K for shapes with few output tiles.
     (same plan, same partial products, same order of the final sum);
   * the workspace starts filled with NaN, so a partial that is read before it
     is written would show; repeated calls are bitwise identical;
-  * without a workspace the result equals q4nx_gemm bit for bit.
+  * without a workspace the result equals q4nx_gemm bit for bit;
+  * Q4NX products with a large M dequantize W to bf16 in the workspace first
+    (each weight once) and give the fused kernel's bits.
 """
 import numpy as np
 import pytest
@@ -46,9 +48,11 @@ def host_f32(t):
     return t.float().cpu().numpy() if t.dtype == torch.bfloat16 else t.cpu().numpy()
 
 
-def work_for(q4, M, N, K):
-    nbytes = q4.q4nx_gemm_workspace_size(M, N, K)
-    assert nbytes > 0, "this shape is meant to take a split-K plan"
+def work_for(q4, M, N, K, fmt=None):
+    """A NaN-filled workspace big enough for every weight format."""
+    fmts = [fmt] if fmt is not None else [q4.Q4NX_WEIGHTS_Q4NX, q4.Q4NX_WEIGHTS_MXFP4, q4.Q4NX_WEIGHTS_BF16]
+    nbytes = max(q4.q4nx_gemm_workspace_size(f, M, N, K) for f in fmts)
+    assert nbytes > 0, "this shape is meant to use a workspace"
     return torch.full((nbytes // 4,), float("nan"), dtype=torch.float32, device="cuda")
 
 
@@ -137,3 +141,34 @@ def test_gemm_ex_repeatable_and_unsplit_without_workspace(q4):
     # split and unsplit differ only by the order of the float32 sums
     d = (Ys[0] - Ys[3]).abs().max().item()
     assert d <= 1e-4 * Ys[3].abs().max().item()
+
+
+@pytest.mark.parametrize("M,N,K,split", [(4096, 1024, 4096, False), (4096, 5376, 21504, True)])
+def test_gemm_ex_dequantize_then_multiply(q4, M, N, K, split):
+    """Shapes whose Q4NX workspace holds bf16 W: the result equals the fused
+    product of the same plan bit for bit (q4nx_gemm when nothing is split,
+    the bf16-weight product of the dequantized W when K is split), and meets
+    the oracle on sampled rows."""
+    _say("gemm_ex two-phase", M, N, K)
+    nbytes = q4.q4nx_gemm_workspace_size(q4.Q4NX_WEIGHTS_Q4NX, M, N, K)
+    assert nbytes >= N * K * 2
+    codes, s, o = gen_weights(N, K, seed=N)
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    Xh = gen_activations((M, K), seed=K)
+    X = dev_bf16(Xh)
+    work = torch.full((nbytes // 4,), float("nan"), dtype=torch.float32, device="cuda")
+    Y1 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    Y2 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, Y1, work=work)
+    if split:
+        W = torch.empty((N, K), dtype=torch.bfloat16, device="cuda")
+        q4.q4nx_dequant(blob, N, K, W)
+        q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_BF16, M, N, K, X, W, Y2, work=work_for(q4, M, N, K, q4.Q4NX_WEIGHTS_BF16))
+    else:
+        q4.q4nx_gemm(M, N, K, X, blob, Y2)
+    torch.cuda.synchronize()
+    assert torch.equal(Y1.view(torch.int32), Y2.view(torch.int32))
+    rows = _rows(M, 24)
+    w32 = oracle.dequant_f32(codes, s, o)
+    ok, worst = oracle.check_close(host_f32(Y1)[rows], oracle.gemm_f64(Xh[rows], w32), oracle.abs_bound(Xh[rows], w32))
+    assert ok, worst
