@@ -253,7 +253,10 @@ def traffic_file(config):
 
 
 def kernel_family(name):
-    if "gemm256_kernel" in name or "gemm_kernel" in name or "splitk_sum_kernel" in name:
+    # The prefill step's launches: the products, their partial sums and the
+    # dequant pass of products that dequantize first (the counter passes run
+    # only the decode and prefill steps, so no other step launches these).
+    if any(k in name for k in ("gemm256_kernel", "gemm_kernel", "splitk_sum_kernel", "dequant_kernel")):
         return "gemm"
     if "gemv_kernel" in name:
         return "gemv"
