@@ -54,7 +54,7 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4])
     ap.add_argument("--seed", type=int, default=0)
@@ -185,9 +185,12 @@ class Step:
                 raise RuntimeError(f"{fn.__name__}: status {st}: {self.q4.lib.q4nx_last_error().decode()}")
 
 
-def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefill):
+def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefill, gpu=None):
     """The oracle, untuned, on a bounded sample: `layers` layer(s) of the
-    workload's projections, timed on this host's cores."""
+    workload's projections, timed on this host's cores.  With `gpu` (outputs
+    the timed GPU steps produced), the same oracle results also check them:
+    layer 0's decode outputs in full, and sampled rows of the last layer's
+    prefill products (untimed)."""
     import numpy as np
     import oracle
     from workloads import gen_weights, gen_activations
@@ -199,6 +202,7 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
     dec_t = dec_bytes = 0.0
     pre_t = pre_flops = 0.0
     rows = 16
+    checks = []
     first = {p: g[0] for g in GROUPS for p in g}   # projections of a group share the prefill input
     for l in range(layers):
         for p, (_, N, K) in enumerate(model["proj"]):
@@ -211,15 +215,31 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
             t_deq = time.perf_counter() - t0
             if do_decode:
                 t0 = time.perf_counter()
-                oracle.gemv_f64(w, x)
+                y_ref = oracle.gemv_f64(w, x)
                 dec_t += t_deq + time.perf_counter() - t0
                 dec_bytes += N * K * WEIGHT_BYTES
+                if gpu and l == 0 and p in gpu.get("decode", {}):
+                    ok, worst = oracle.check_close(gpu["decode"][p], y_ref, oracle.abs_bound(x, w))
+                    checks.append(("decode", p, N, ok, worst))
             if do_prefill:
                 t0 = time.perf_counter()
                 oracle.gemm_f64(X, w)
                 pre_t += t_deq + time.perf_counter() - t0
                 pre_flops += 2.0 * rows * N * K
             log(f"oracle sample: layer {l} projection {p} ({N}x{K}) done")
+    if gpu and "prefill" in gpu:
+        # The last layer's stacked products on the GPU's own input rows.
+        lp = gpu["prefill_layer"]
+        for gi, (Xr, Yr) in gpu["prefill"].items():
+            ws = []
+            for p in GROUPS[gi]:
+                _, N, K = model["proj"][p]
+                codes, s, o = gen_weights(N, K, seed=seed, layer=lp, proj=p, offset_mode=mode)
+                ws.append(oracle.dequant_f32(codes, s, o))
+            w = np.concatenate(ws)
+            ok, worst = oracle.check_close(Yr, oracle.gemm_f64(Xr, w), oracle.abs_bound(Xr, w))
+            checks.append(("prefill", gi, w.shape[0], ok, worst))
+            log(f"oracle check: layer {lp} product {gi} ({w.shape[0]}x{w.shape[1]}) done")
     out = {"cores": int(blas_threads), "kind": "oracle"}
     what = f"{layers} layer(s) x {len(model['proj'])} projections of {cfg['name']}"
     if do_decode:
@@ -234,6 +254,18 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
             out["prefill"] = pf
         else:
             out.update(value=pf["value"], unit=pf["unit"], sample=pf["sample"], seconds=pre_t)
+    if checks:
+        pc = {"tolerance": "|y - y_ref| <= 2e-3 * sum_k |x_k w_k| + 1e-5 per output, float64 oracle"}
+        for kind, what in (("decode", "layer 0, every output of its {} projections"),
+                           ("prefill", "layer {}, {} token rows of each of its {} stacked products")):
+            cs = [c for c in checks if c[0] == kind]
+            if not cs:
+                continue
+            pc[kind] = (what.format(len(cs)) if kind == "decode"
+                        else what.format(gpu["prefill_layer"], gpu["prefill_rows"], len(cs)))
+            pc[f"{kind}_worst_err_over_tol"] = float(f"{max(c[4] for c in cs):.3g}")
+        pc["ok"] = all(c[3] for c in checks)
+        out["parity_check"] = pc
     return out
 
 
@@ -762,6 +794,7 @@ def main():
     }
     if do_decode:
         result["decode"] = {"ms": round(mean(dec_ms), 4), "ms_min": round(min(dec_ms), 4),
+                            "ms_median": round(sorted(dec_ms)[len(dec_ms) // 2], 4),
                             "weight_GB": round(dec_bytes / 1e9, 4), "GB_per_s": round(dec_gbs, 2),
                             "frac_hbm": round(dec_gbs / HBM_PEAK_GBS, 4), "launches": dec_launches,
                             "launch": "hip graph replay" if use_graph else "eager",
@@ -772,7 +805,8 @@ def main():
             result["decode"][f"{key}_ms"] = round(mean(other_dec_ms), 4)
             result["decode"][f"{key}_GB_per_s"] = round(dec_bytes / (mean(other_dec_ms) * 1e-3) / 1e9, 2)
     if do_prefill:
-        result["prefill"] = {"ms": round(mean(pre_ms), 4), "ms_min": round(min(pre_ms), 4), "M": M_pre,
+        result["prefill"] = {"ms": round(mean(pre_ms), 4), "ms_min": round(min(pre_ms), 4),
+                             "ms_median": round(sorted(pre_ms)[len(pre_ms) // 2], 4), "M": M_pre,
                              "TFLOP": round(pre_flops / 1e12, 4), "TFLOP_per_s": round(pre_tflops, 2),
                              "frac_mfma": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4),
                              "launches": len(pre.calls), "dtype": "bf16 MFMA, f32 accumulate",
@@ -801,6 +835,19 @@ def main():
 
     if mx:
         result["mxfp4"] = mx
+    if do_decode:
+        # Read bandwidth a plain streaming kernel reaches on this device (the
+        # library's measurement aid, the GEMV's load pattern over 4 GiB).
+        src = torch.empty(1 << 32, dtype=torch.uint8, device="cuda")
+        sink = torch.empty(2048, dtype=torch.float32, device="cuda")
+        sr = Step(q4, stream.cuda_stream)
+        sr.calls.append((q4.lib.q4nx_stream_read, (src.data_ptr(), src.numel(), sink.data_ptr(), sr.s)))
+        for _ in range(args.warmup):
+            sr.run()
+        _, sr_ms, _ = timed(lambda: None, sr.run, args.steps)
+        t = sorted(sr_ms)[len(sr_ms) // 2]
+        result["roofline_gemv" if do_prefill else "roofline"]["stream_read_GB_per_s"] = round(src.numel() / (t * 1e-3) / 1e9, 1)
+        del src, sink
     if quant:
         result["quantize"] = quant
     if fkv:
@@ -817,9 +864,28 @@ def main():
                 result[key]["mfma_busy_counter"] = round(e["mfma_busy_fraction"], 4)
 
     if not args.no_cpu_baseline:
+        # Outputs of the timed GPU steps for the oracle to check: layer 0's
+        # decode outputs (their own buffers), and the last layer's prefill
+        # products, run once more because later steps reuse the output buffers.
+        gpu = {}
+        if do_decode:
+            for fn, a in dec.calls[:len(GROUPS)]:   # layer 0's launches (the MXFP4 step reuses ys)
+                fn(*a)
+            torch.cuda.synchronize()
+            gpu["decode"] = {p: ys[(0, p)].cpu().numpy() for p in range(len(model["proj"]))}
+        if do_prefill:
+            for fn, a in pre.calls[-len(GROUPS):]:
+                fn(*a)
+            torch.cuda.synchronize()
+            rng = __import__("numpy").random.default_rng(args.seed)
+            rows = sorted(set([0, 1, M_pre // 2, M_pre - 1] + rng.integers(0, M_pre, 12).tolist()))
+            idx = torch.tensor(rows, device="cuda")
+            gpu["prefill_layer"], gpu["prefill_rows"] = L - 1, len(rows)
+            gpu["prefill"] = {gi: (Xs[(L - 1, gi)].index_select(0, idx).view(torch.int16).cpu().numpy().view("uint16"),
+                                   Ys[gi].index_select(0, idx).cpu().numpy()) for gi in range(len(GROUPS))}
         log("timing the CPU oracle sample")
         result["cpu_baseline"] = cpu_baseline(model, cfg, args.seed, args.offset_mode, args.cpu_layers,
-                                              do_decode, do_prefill, M_pre)
+                                              do_decode, do_prefill, M_pre, gpu)
     print(json.dumps(result), flush=True)
 
 

@@ -329,6 +329,13 @@ q4nx_status q4nx_mx_gemv_batched(const q4nx_gemv_desc* descs, int32_t count, q4n
 q4nx_status q4nx_mx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, const void* d_blob, void* d_Y,
                          q4nx_dtype y_dtype, hipStream_t stream);
 
+/* Measurement aid (not part of the projection path): reads `bytes` (a multiple
+ * of 16) of device memory once with the GEMV's load pattern and writes 2048
+ * floats (one per workgroup) to d_sink, which must hold them.  Timing it gives
+ * the read bandwidth a streaming kernel reaches on the device.  Device,
+ * asynchronous; errors as above (d_src 16-byte aligned). */
+q4nx_status q4nx_stream_read(const void* d_src, size_t bytes, float* d_sink, hipStream_t stream);
+
 /* Static description of a status code. */
 const char* q4nx_status_str(q4nx_status status);
 

@@ -35,7 +35,7 @@ Q4NX_WEIGHTS_BF16 = 2
 EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_quantize", "q4nx_dequant", "q4nx_gemv",
             "q4nx_gemv_batched", "q4nx_gemm", "q4nx_gemm_bf16", "q4nx_flowkv_workspace_size",
             "q4nx_flowkv_decode", "q4nx_mx_packed_size", "q4nx_mx_pack", "q4nx_mx_unpack", "q4nx_mx_quantize", "q4nx_mx_dequant",
-            "q4nx_mx_gemv", "q4nx_mx_gemv_batched", "q4nx_mx_gemm", "q4nx_gemm_workspace_size", "q4nx_gemm_ex",
+            "q4nx_mx_gemv", "q4nx_mx_gemv_batched", "q4nx_mx_gemm", "q4nx_gemm_workspace_size", "q4nx_gemm_ex", "q4nx_stream_read",
             "q4nx_status_str", "q4nx_last_error"]
 
 if not os.path.exists(LIB_PATH):
@@ -102,6 +102,8 @@ lib.q4nx_gemm_workspace_size.argtypes = [ctypes.c_int, _i64, _i64, _i64]
 lib.q4nx_gemm_workspace_size.restype = _sz
 lib.q4nx_gemm_ex.argtypes = [ctypes.c_int, _i64, _i64, _i64, _vp, _vp, _vp, ctypes.c_int, _vp, _sz, _vp]
 lib.q4nx_gemm_ex.restype = ctypes.c_int
+lib.q4nx_stream_read.argtypes = [_vp, _sz, _vp, _vp]
+lib.q4nx_stream_read.restype = ctypes.c_int
 lib.q4nx_status_str.argtypes = [ctypes.c_int]
 lib.q4nx_status_str.restype = ctypes.c_char_p
 lib.q4nx_last_error.argtypes = []
@@ -332,6 +334,13 @@ def q4nx_gemm_ex(w_format: int, M: int, N: int, K: int, X, W, Y, work=None, stre
     wp, wn = (None, 0) if work is None else (_dptr(work), work.numel() * work.element_size())
     _check(lib.q4nx_gemm_ex(w_format, M, N, K, _dptr(X), _dptr(W), _dptr(Y), _dtype_code(Y), wp, wn, _stream(stream)),
            "q4nx_gemm_ex")
+
+
+def q4nx_stream_read(src, sink, stream=None):
+    """Measurement aid: read all of `src` once (sink: 2048 float32)."""
+    _need(sink, 4 * 2048, "sink")
+    _check(lib.q4nx_stream_read(_dptr(src), src.numel() * src.element_size(), _dptr(sink), _stream(stream)),
+           "q4nx_stream_read")
 
 
 def q4nx_flowkv_workspace_size(H: int, d: int, n_keys: int) -> int:

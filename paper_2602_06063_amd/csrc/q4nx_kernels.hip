@@ -1630,6 +1630,34 @@ static q4nx_status dequant_entry(const void* d_blob, int64_t N, int64_t K, void*
   return check_launch(fn);
 }
 
+// Measurement aid: read a buffer once with the GEMV's load pattern (16-byte
+// non-temporal loads, a workgroup per contiguous slice) and fold it into one
+// float per workgroup, so that nothing is dead code.  Gives the read bandwidth
+// a streaming kernel reaches on the device, beside the vendor's HBM figure.
+constexpr int kStreamWgs = 2048;
+__global__ __launch_bounds__(256) void stream_read_kernel(const u32x4* __restrict__ src, int64_t n16,
+                                                          float* __restrict__ sink) {
+  const int64_t per = (n16 + gridDim.x - 1) / gridDim.x;
+  const int64_t b = (int64_t)blockIdx.x * per, e = min(n16, b + per);
+  uint32_t acc = 0;
+  for (int64_t i = b + threadIdx.x; i < e; i += 4 * 256) {
+    u32x4 v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      v[u] = i + u * 256 < e ? __builtin_nontemporal_load(src + i + u * 256) : (u32x4){0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  __shared__ uint32_t red[256];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    uint32_t t = 0;
+    for (int k = 0; k < 256; ++k) t ^= red[k];
+    sink[blockIdx.x] = __uint_as_float(t & 0x3FFFFFFFu);
+  }
+}
+
 }  // namespace q4nx
 
 using namespace q4nx;
@@ -1672,6 +1700,16 @@ q4nx_status q4nx_mx_quantize(const float* d_W, int64_t N, int64_t K, void* d_blo
   hipLaunchKernelGGL(mx_quantize_kernel, dim3((unsigned)grid), dim3(256), 0, stream, d_W, N, K, KB, nblocks,
                      static_cast<uint8_t*>(d_blob));
   return check_launch("q4nx_mx_quantize");
+}
+
+q4nx_status q4nx_stream_read(const void* d_src, size_t bytes, float* d_sink, hipStream_t stream) {
+  clear_error();
+  if (!d_src || !d_sink) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_stream_read: NULL pointer");
+  if (bytes == 0 || bytes % 16 != 0) return fail(Q4NX_ERR_SHAPE, "q4nx_stream_read: bytes must be a positive multiple of 16");
+  if (!aligned(d_src, 16) || !aligned(d_sink, 4)) return fail(Q4NX_ERR_ALIGNMENT, "q4nx_stream_read: src needs 16-byte alignment");
+  hipLaunchKernelGGL(stream_read_kernel, dim3(kStreamWgs), dim3(256), 0, stream, static_cast<const u32x4*>(d_src),
+                     (int64_t)(bytes / 16), d_sink);
+  return check_launch("q4nx_stream_read");
 }
 
 q4nx_status q4nx_gemv(const void* d_blob, const uint16_t* d_x, void* d_y, q4nx_dtype y_dtype, int64_t N,

@@ -327,6 +327,15 @@ def test_gemm_ex_workspace_size_and_validation():
         assert L.q4nx_gemm_ex(*args(fmt, 2048, 2560, 10240, A16, 0)) == q4.Q4NX_ERR_BUFFER_TOO_SMALL
 
 
+def test_stream_read_validation():
+    L = q4.lib
+    assert L.q4nx_stream_read(None, 16, A16, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_stream_read(A16, 16, None, None) == q4.Q4NX_ERR_INVALID_ARG
+    assert L.q4nx_stream_read(A16, 0, A16, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_stream_read(A16, 24, A16, None) == q4.Q4NX_ERR_SHAPE
+    assert L.q4nx_stream_read(MIS, 16, A16, None) == q4.Q4NX_ERR_ALIGNMENT
+
+
 def test_status_strings():
     for st in range(6):
         assert q4.lib.q4nx_status_str(st).decode()
