@@ -185,18 +185,23 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
   }
 }
 
-// Phase 2.  grid H, 256 threads: S = 256 / D slices of D threads; slice s
-// takes chunks s, s + S, ...  With M the largest chunk max, Eq. 9's
+// Phase 2.  grid (H, D / DW), 256 threads: workgroup (h, b) produces dims
+// b*DW .. b*DW + DW-1 of head h, with S = 256 / DW slices of DW threads; slice
+// s takes chunks s, s + S, ...  With M the largest chunk max, Eq. 9's
 // correction of chunk c relative to M is exp(m_c - M); the head's output is
 // sum_c exp(m_c - M) Y_c / sum_c exp(m_c - M) l_c (Eq. 10-12), summed over
-// the chunks in increasing order within a slice and then over the slices.
-template <int D>
+// the chunks in increasing order within a slice and then over the slices
+// (every workgroup of a head forms the same denominator in the same order).
+// Splitting the dims keeps many chunks from serialising on a few workgroups
+// when there are few heads (Gemma3 1B: 4 heads, 512 chunks at 32K).
+template <int D, int DW>
 __global__ __launch_bounds__(kFkvThreads) void flowkv_merge_kernel(const float* __restrict__ work, int nchunks,
                                                                    void* __restrict__ out, int out_bf16) {
-  constexpr int kPart = D + 4, S = kFkvThreads / D;
+  constexpr int kPart = D + 4, S = kFkvThreads / DW;
   __shared__ float mx[kFkvThreads / 64];
-  __shared__ float ls[S], yls[S][D];
-  const int h = blockIdx.x, tid = threadIdx.x, dd = tid % D, sl = tid / D;
+  __shared__ float ls[S], yls[S][DW];
+  const int h = blockIdx.x, tid = threadIdx.x, dd = tid % DW, sl = tid / DW;
+  const int dim = blockIdx.y * DW + dd;
   const float* part = work + (size_t)h * nchunks * kPart;
   float mloc = -INFINITY;
   for (int c = tid; c < nchunks; c += kFkvThreads) mloc = fmaxf(mloc, part[(size_t)c * kPart]);
@@ -212,7 +217,7 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_merge_kernel(const float* 
     const float* pc = part + (size_t)c * kPart;
     const float a = expf(pc[0] - M);
     l = fmaf(a, pc[1], l);
-    y = fmaf(a, pc[4 + dd], y);
+    y = fmaf(a, pc[4 + dim], y);
   }
   yls[sl][dd] = y;
   if (dd == 0) ls[sl] = l;
@@ -227,9 +232,9 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_merge_kernel(const float* 
     const float o = yt / lt;
     if (out_bf16) {
       bf16x2f p = __builtin_convertvector((float __attribute__((ext_vector_type(2)))){o, 0.0f}, bf16x2f);
-      static_cast<uint16_t*>(out)[(size_t)h * D + dd] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
+      static_cast<uint16_t*>(out)[(size_t)h * D + dim] = (uint16_t)(__builtin_bit_cast(uint32_t, p) & 0xFFFFu);
     } else {
-      static_cast<float*>(out)[(size_t)h * D + dd] = o;
+      static_cast<float*>(out)[(size_t)h * D + dim] = o;
     }
   }
 }
@@ -240,8 +245,19 @@ static void launch_flowkv(const uint16_t* q, const uint16_t* K, const uint16_t* 
   const int nchunks = (int)ceil_div(j1 - j0, CH);
   hipLaunchKernelGGL((flowkv_chunk_kernel<CH, D, HG>), dim3(nchunks, G), dim3(kFkvThreads), 0, stream, q, K, V, L,
                      j0, j1, scale, work);
-  hipLaunchKernelGGL((flowkv_merge_kernel<D>), dim3(G * HG), dim3(kFkvThreads), 0, stream, work, nchunks, out,
-                     out_bf16);
+  // Dims per merge workgroup: halved (down to 16) until there are at least
+  // 128 workgroups.
+  const int H = G * HG;
+  int dw = D;
+  while (dw > 16 && H * (D / dw) < 128) dw >>= 1;
+  const dim3 mg(H, D / dw);
+  switch (dw) {
+    case 256: hipLaunchKernelGGL((flowkv_merge_kernel<D, (D >= 256 ? 256 : D)>), mg, dim3(kFkvThreads), 0, stream, work, nchunks, out, out_bf16); break;
+    case 128: hipLaunchKernelGGL((flowkv_merge_kernel<D, (D >= 128 ? 128 : D)>), mg, dim3(kFkvThreads), 0, stream, work, nchunks, out, out_bf16); break;
+    case 64: hipLaunchKernelGGL((flowkv_merge_kernel<D, 64>), mg, dim3(kFkvThreads), 0, stream, work, nchunks, out, out_bf16); break;
+    case 32: hipLaunchKernelGGL((flowkv_merge_kernel<D, 32>), mg, dim3(kFkvThreads), 0, stream, work, nchunks, out, out_bf16); break;
+    default: hipLaunchKernelGGL((flowkv_merge_kernel<D, 16>), mg, dim3(kFkvThreads), 0, stream, work, nchunks, out, out_bf16); break;
+  }
 }
 
 // Chunk size: the largest of 256, 128, 64 positions that still gives at

@@ -53,6 +53,10 @@ CASES = [
     (8, 1, 64, 1024, 777, 0),
     (8, 4, 256, 32768, 32767, 0),
     (32, 16, 128, 32768, 20000, 0),
+    # many heads: the merge takes 64, 128 and 256 dims per workgroup
+    (64, 16, 128, 2048, 1999, 0),
+    (128, 16, 128, 1024, 900, 0),
+    (128, 16, 256, 1024, 1000, 0),
 ]
 
 
