@@ -846,8 +846,40 @@ def main():
             sr.run()
         _, sr_ms, _ = timed(lambda: None, sr.run, args.steps)
         t = sorted(sr_ms)[len(sr_ms) // 2]
-        result["roofline_gemv" if do_prefill else "roofline"]["stream_read_GB_per_s"] = round(src.numel() / (t * 1e-3) / 1e9, 1)
-        del src, sink
+        rkey = "roofline_gemv" if do_prefill else "roofline"
+        result[rkey]["stream_read_GB_per_s"] = round(src.numel() / (t * 1e-3) / 1e9, 1)
+        del src
+        # The same weight bytes read by the plain streaming kernel in the
+        # decode step's launch structure: one dependent launch per GEMV launch,
+        # over the very blobs that launch reads.  Each launch pays its ramp and
+        # drain, so this is the ceiling for a step of that many launches.
+        fl = Step(q4, stream.cuda_stream)
+        blobs = [stacked[(l, gi)] for l in range(L) for gi in range(len(GROUPS))]
+        if cfg.get("lm_head"):
+            blobs.append(weights[(L, 7)])
+        for b in blobs:
+            fl.calls.append((q4.lib.q4nx_stream_read, (b.data_ptr(), b.numel(), sink.data_ptr(), fl.s)))
+        fl_fn = fl.run
+        fl.run()
+        torch.cuda.synchronize()
+        fg = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(fg, stream=stream):
+            fl.run()
+        graphs.append(fg)
+        if quick_ms(fg.replay) < quick_ms(fl.run):
+            fl_fn = fg.replay
+        for _ in range(args.warmup):
+            fl_fn()
+        fl_ms, _, _ = timed(fl_fn, lambda: None, args.steps)
+        fl_t = sorted(fl_ms)[len(fl_ms) // 2]
+        dec_t = sorted(dec_ms)[len(dec_ms) // 2]
+        result[rkey]["launch_floor"] = {
+            "what": "q4nx_stream_read over each decode launch's weight blob, one launch per GEMV launch, "
+                    "same launch mode choice (graph or eager, the faster)",
+            "launches": len(fl.calls), "ms_median": round(fl_t, 4),
+            "GB_per_s": round(sum(b.numel() for b in blobs) / (fl_t * 1e-3) / 1e9, 1),
+            "decode_ms_median_over_floor": round(dec_t / fl_t, 4)}
+        del sink
     if quant:
         result["quantize"] = quant
     if fkv:
