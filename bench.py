@@ -25,6 +25,8 @@ in the MXFP4 variant of the block (0.53125 B per weight: the FP4 code plus the
 per-32 E8M0 scale) are timed and reported under "mxfp4".
 
     python bench.py [--config 4] [--steps 5] [--warmup 2] [--gpus 1]
+
+--config 0 times one GEMV launch (1B q_proj) cold and warm instead of a step.
 """
 from __future__ import annotations
 
@@ -56,7 +58,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4])
+    ap.add_argument("--config", type=int, default=4, choices=[0, 1, 2, 3, 4])
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--offset-mode", default="zp", choices=["zp", "literal"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -185,6 +187,14 @@ class Step:
                 raise RuntimeError(f"{fn.__name__}: status {st}: {self.q4.lib.q4nx_last_error().decode()}")
 
 
+def blas_thread_count():
+    try:
+        from threadpoolctl import threadpool_info
+        return max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        return 1
+
+
 def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefill, gpu=None):
     """The oracle, untuned, on a bounded sample: `layers` layer(s) of the
     workload's projections, timed on this host's cores.  With `gpu` (outputs
@@ -194,11 +204,7 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
     import numpy as np
     import oracle
     from workloads import gen_weights, gen_activations
-    try:
-        from threadpoolctl import threadpool_info
-        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    except Exception:  # pragma: no cover
-        blas_threads = 1
+    blas_threads = blas_thread_count()
     dec_t = dec_bytes = 0.0
     pre_t = pre_flops = 0.0
     rows = 16
@@ -441,6 +447,101 @@ def stored_traffic(config):
     return data
 
 
+def run_single(args, cfg, q4, torch):
+    """Config 0: one GEMV launch (1B q_proj, 1024 x 1152, 819,200 stored bytes),
+    launch-latency-bound.  Timed warm (the same weights every launch: they sit
+    in L2) and cold (512 distinct copies, 419 MB, more than the 4 MB L2s and the
+    256 MB memory-side cache together), each as a HIP graph of back-to-back
+    launches; `value` is the cold rate.  The output of every copy is checked
+    against the float64 oracle (full N)."""
+    import numpy as np
+    from workloads import gen_weights, gen_activations
+    _, N, K = cfg["single"]
+    codes, s, o = gen_weights(N, K, seed=args.seed, layer=0, proj=0, offset_mode=args.offset_mode)
+    x_h = gen_activations(K, seed=args.seed, layer=0, proj=0)
+    blob_h = q4.q4nx_pack(codes, s, o)
+    stream = torch.cuda.Stream()
+    torch.cuda.set_stream(stream)
+    st = ctypes.c_void_p(stream.cuda_stream)
+    copies = 512
+    blobs = torch.from_numpy(blob_h).cuda().repeat(copies).view(copies, -1)
+    x = torch.from_numpy(x_h.view("int16")).cuda()
+    ys = torch.empty((copies, N), dtype=torch.float32, device="cuda")
+    gemv = q4.lib.q4nx_gemv
+
+    def launches(which):
+        for i in which:
+            assert gemv(blobs[i].data_ptr(), x.data_ptr(), ys[i].data_ptr(), q4.Q4NX_F32, N, K, st) == 0
+
+    def graph_ms(which, reps):
+        launches(which)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g, stream=stream):
+            launches(which)
+        for _ in range(args.warmup):
+            g.replay()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) / len(which))
+        return sorted(ts)[len(ts) // 2], min(ts)
+
+    cold_ms, cold_min = graph_ms(list(range(copies)), args.steps)
+    warm_ms, warm_min = graph_ms([0] * copies, args.steps)
+    wbytes = N * K * WEIGHT_BYTES
+    cold_gbs, warm_gbs = wbytes / (cold_ms * 1e-3) / 1e9, wbytes / (warm_ms * 1e-3) / 1e9
+    log(f"single GEMV {N}x{K}: cold {cold_ms * 1e3:.2f} us, warm {warm_ms * 1e3:.2f} us per launch")
+    result = {
+        "metric": "Q4NX dequant-GEMV weight GB/s (% HBM peak); dequant-GEMM TFLOP/s (% MFMA)",
+        "value": round(cold_gbs, 2), "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(cold_ms, 6), "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": cfg["name"], "N": N, "K": K, "M": [1], "offset_mode": args.offset_mode,
+                   "seed": args.seed},
+        "single": {"what": "one q4nx_gemv launch per step; per-launch time from a HIP graph of 512 launches",
+                   "cold_us": round(cold_ms * 1e3, 3), "cold_us_min": round(cold_min * 1e3, 3),
+                   "warm_us": round(warm_ms * 1e3, 3), "warm_us_min": round(warm_min * 1e3, 3),
+                   "cold_GB_per_s": round(cold_gbs, 2), "warm_GB_per_s": round(warm_gbs, 2),
+                   "weight_bytes": int(wbytes), "stored_bytes": int(blob_h.nbytes), "copies_cold": copies},
+        "roofline": {"kernel": "gemv_kernel", "bound": "hbm", "achieved": round(cold_gbs, 2), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(cold_gbs / HBM_PEAK_GBS, 4), "traffic": None,
+                     "algorithmic_bytes": int(wbytes + 2 * K + 4 * N),
+                     "note": "launch-latency-bound: 0.1 us of streaming at 8 TB/s against a few us per launch"},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        torch.cuda.synchronize()
+        y_gpu = ys.cpu().numpy()
+        reps, t = 0, 0.0
+        while t < 2.0:
+            t0 = time.perf_counter()
+            w = oracle.dequant_blob_f32(blob_h, N, K)
+            y_ref = oracle.gemv_f64(w, x_h)
+            t += time.perf_counter() - t0
+            reps += 1
+        bound = oracle.abs_bound(x_h, w)
+        worst = 0.0
+        ok = True
+        for i in range(copies):
+            good, wr = oracle.check_close(y_gpu[i], y_ref, bound)
+            ok = ok and good
+            worst = max(worst, wr)
+        result["cpu_baseline"] = {
+            "value": reps * wbytes / t / 1e9, "unit": "GB/s", "cores": int(blas_thread_count()), "kind": "oracle",
+            "sample": f"{reps} runs of the oracle's float32 Eq. 3 dequant (single-threaded) + float64 mat-vec "
+                      f"(BLAS threads) of this GEMV",
+            "seconds": t,
+            "parity_check": {"tolerance": "|y - y_ref| <= 2e-3 * sum_k |x_k w_k| + 1e-5 per output",
+                             "outputs": f"all {N} outputs of every one of the {copies} launches",
+                             "worst_err_over_tol": float(f"{worst:.3g}"), "ok": bool(ok)}}
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -461,6 +562,8 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     cfg = CONFIGS[args.config]
+    if "single" in cfg:
+        return run_single(args, cfg, q4, torch)
     model = MODELS[cfg["model"]]
     L = model["layers"]
     Ms = cfg["M"]
