@@ -409,11 +409,11 @@ def pmc_summary(config, fetch_dir, write_dir, mfma_dir):
     lines = [f"# HBM traffic and MFMA busy counters, bench configuration {config}", "",
              "Three rocprofv3 counter passes over `python3 bench.py --config %d --pmc-pass` (one eager decode "
              "step, one prefill step, then a 1 GiB device-to-device copy used as the calibration):" % config, "",
-             "```", "cd /tmp && export TMPDIR=/tmp; cd $GRAFT_REPO_ROOT",
-             "rocprofv3 --pmc FETCH_SIZE --output-format csv -d gpurun_out/pmc_fetch -o run -- python3 bench.py --config %d --pmc-pass" % config,
-             "rocprofv3 --pmc WRITE_SIZE --output-format csv -d gpurun_out/pmc_write -o run -- python3 bench.py --config %d --pmc-pass" % config,
-             "rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE --output-format csv -d gpurun_out/pmc_mfma -o run -- python3 bench.py --config %d --pmc-pass" % config,
-             "python3 bench.py --config %d --pmc-summary gpurun_out/pmc_fetch gpurun_out/pmc_write gpurun_out/pmc_mfma" % config,
+             "```", "cd /tmp && export TMPDIR=/tmp && cd /root/repo",
+             f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
+             f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
+             f"rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE --output-format csv -d {mfma_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
+             f"python3 bench.py --config {config} --pmc-summary {fetch_dir} {write_dir} {mfma_dir}",
              "```", "",
              "Calibration copy: FETCH_SIZE %.0f KiB and WRITE_SIZE %.0f KiB for %d bytes each way, so counter bytes are "
              "scaled by %.4f (fetch) and %.4f (write)." % (data["calibration"]["fetch_kib"], data["calibration"]["write_kib"],
