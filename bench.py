@@ -187,6 +187,16 @@ class Step:
                 raise RuntimeError(f"{fn.__name__}: status {st}: {self.q4.lib.q4nx_last_error().decode()}")
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:  # pragma: no cover
+        pass
+    return "unknown"
+
+
 def blas_thread_count():
     try:
         from threadpoolctl import threadpool_info
@@ -207,6 +217,7 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
     blas_threads = blas_thread_count()
     dec_t = dec_bytes = 0.0
     pre_t = pre_flops = 0.0
+    deq_total = mv_total = mm_total = 0.0   # the oracle's dequant, mat-vec and matmul separately
     rows = 16
     checks = []
     first = {p: g[0] for g in GROUPS for p in g}   # projections of a group share the prefill input
@@ -219,10 +230,13 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
             t0 = time.perf_counter()
             w = oracle.dequant_blob_f32(blob, N, K)
             t_deq = time.perf_counter() - t0
+            deq_total += t_deq
             if do_decode:
                 t0 = time.perf_counter()
                 y_ref = oracle.gemv_f64(w, x)
-                dec_t += t_deq + time.perf_counter() - t0
+                t_mv = time.perf_counter() - t0
+                mv_total += t_mv
+                dec_t += t_deq + t_mv
                 dec_bytes += N * K * WEIGHT_BYTES
                 if gpu and l == 0 and p in gpu.get("decode", {}):
                     ok, worst = oracle.check_close(gpu["decode"][p], y_ref, oracle.abs_bound(x, w))
@@ -230,7 +244,9 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
             if do_prefill:
                 t0 = time.perf_counter()
                 oracle.gemm_f64(X, w)
-                pre_t += t_deq + time.perf_counter() - t0
+                t_mm = time.perf_counter() - t0
+                mm_total += t_mm
+                pre_t += t_deq + t_mm
                 pre_flops += 2.0 * rows * N * K
             log(f"oracle sample: layer {l} projection {p} ({N}x{K}) done")
     if gpu and "prefill" in gpu:
@@ -246,7 +262,10 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
             ok, worst = oracle.check_close(Yr, oracle.gemm_f64(Xr, w), oracle.abs_bound(Xr, w))
             checks.append(("prefill", gi, w.shape[0], ok, worst))
             log(f"oracle check: layer {lp} product {gi} ({w.shape[0]}x{w.shape[1]}) done")
-    out = {"cores": int(blas_threads), "kind": "oracle"}
+    out = {"cores": int(blas_threads), "kind": "oracle", "cpu_model": cpu_model(),
+           "affinity_cpus": len(os.sched_getaffinity(0)),
+           "seconds_split": {"dequant": round(deq_total, 4), "matvec": round(mv_total, 4),
+                             "matmul": round(mm_total, 4)}}
     what = f"{layers} layer(s) x {len(model['proj'])} projections of {cfg['name']}"
     if do_decode:
         out.update(value=dec_bytes / dec_t / 1e9, unit="GB/s",
