@@ -903,6 +903,49 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
 
   // One K step: MFMAs of step s from stage s&1 while step s+1 (held in Rs) is
   // written to the other stage and step s+3 is loaded into Rs.
+  //
+  // Placement of the LDS accesses.  A slot is one MFMA, 32 clocks, in which
+  // the CU's LDS serves about four 1 KiB wave accesses -- one per wave -- and
+  // every slice reads its 8 fragments of the next slice.  The writes of the
+  // other stage must land before the barrier, so they are spread over the
+  // slices before it instead of being packed into one:
+  //   bf16 W (16 writes: x0..x7, w0..w7), odd slots from 1: slice 0 x0..x5,
+  //     slice 1 x6 x7 w0..w3, slice 2 w4..w7 -- at most 14 accesses in a
+  //     slice; fragment reads on the even slots (slice 2: slots 0, 2, 4, 6,
+  //     8-11, well before the barrier);
+  //   packed W: reads on the even slots of slices 0-1, X at slots 1, 5, 9, 13
+  //     (x0..x3 in slice 0, x4..x7 in slice 1) between the dequantized W
+  //     writes at slots 3, 7, 11, 15.  (With a K tail the X writes stay at
+  //     slots 8-15 of slice 0: the interleaved form costs that instantiation
+  //     a register spill.)
+  // The order of the MFMAs, hence every result bit, does not depend on this.
+  constexpr bool kSpreadPacked = WQ4 && !KTAIL;
+  auto stage_write = [&](WideRegs<WF>& Rs, uint16_t* xsn, int nxt, int slice, int i) {
+    if (!(i & 1)) return;
+    const int o = i >> 1;
+    if constexpr (!WQ4) {
+      if (slice < 2 ? o >= 6 : o >= 4) return;
+      const int k = slice * 6 + o;
+      if (k < 8)
+        *reinterpret_cast<u32x4*>(xsn + 32 * k * kLdsStride) = Rs.x[k];
+      else
+        wchunk(Rs, nxt, k - 8);
+    } else if constexpr (kSpreadPacked) {
+      if (slice < 2 && (o & 1) == 0) {
+        const int k = 4 * slice + (o >> 1);
+        *reinterpret_cast<u32x4*>(xsn + 32 * k * kLdsStride) = Rs.x[k];
+      }
+    }
+  };
+  const auto read_slot = [](int slice, int i) {
+    if (!WQ4 || kSpreadPacked) {
+      if (slice < 2) return (i & 1) ? -1 : i >> 1;
+      if (!WQ4) return i < 8 ? ((i & 1) ? -1 : i >> 1) : (i < 12 ? i - 4 : -1);
+    }
+    return i < 8 ? i : -1;
+  };
+  // Slice 2's global loads of step s + 3 (load i at slot i): a bf16 step's
+  // w4..w7 (loads 12-15) are loaded after their writes at slots 1-7.
   bf16x8 A0[TI], B0[TJ], A1[TI], B1[TJ];
   auto step = [&](int s, WideRegs<WF>& Rs) {
     const int cur = s & 1, nxt = cur ^ 1;
@@ -910,23 +953,28 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       mma1(A0, B0, i);
-      if (i < 8) read1(cur, 1, A1, B1, i);
-      else *reinterpret_cast<u32x4*>(xsn + 32 * (i - 8) * kLdsStride) = Rs.x[i - 8];
+      if (read_slot(0, i) >= 0) read1(cur, 1, A1, B1, read_slot(0, i));
+      if constexpr (WQ4 && !kSpreadPacked) {
+        if (i >= 8) *reinterpret_cast<u32x4*>(xsn + 32 * (i - 8) * kLdsStride) = Rs.x[i - 8];
+      } else {
+        stage_write(Rs, xsn, nxt, 0, i);
+      }
       wpiece(Rs, nxt, 0, i);
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       mma1(A1, B1, i);
-      if (i < 8) read1(cur, 2, A0, B0, i);
-      else if (!WQ4) wchunk(Rs, nxt, i - 8);
+      if (read_slot(1, i) >= 0) read1(cur, 2, A0, B0, read_slot(1, i));
+      stage_write(Rs, xsn, nxt, 1, i);
       wpiece(Rs, nxt, 1, i);
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       mma1(A0, B0, i);
-      if (i < 8) read1(cur, 3, A1, B1, i);
+      if (read_slot(2, i) >= 0) read1(cur, 3, A1, B1, read_slot(2, i));
+      stage_write(Rs, xsn, nxt, 2, i);
       if (i < kLoads) load1(Rs, s + 3, i);
       __builtin_amdgcn_sched_barrier(0);
     }
