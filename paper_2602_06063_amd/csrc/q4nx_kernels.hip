@@ -944,8 +944,37 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
     }
     return i < 8 ? i : -1;
   };
-  // Slice 2's global loads of step s + 3 (load i at slot i): a bf16 step's
-  // w4..w7 (loads 12-15) are loaded after their writes at slots 1-7.
+  // Global loads of step s + 3 go out as soon as their registers are free:
+  // one slot after the write that empties them (bf16 W, and X of packed W),
+  // and a packed W group in the slice after the one that dequantizes it.  So
+  // they spread over slices 0-2 instead of forming one burst in slice 2, and
+  // leave up to two slices earlier.  (With a K tail, packed W keeps the
+  // original order: all loads in slice 2, load i at slot i.)
+  auto early_load = [&](WideRegs<WF>& Rs, int s, int slice, int i) {
+    if constexpr (!WQ4) {
+      // load k one slot after write k (odd slot 2o+1 of its slice; the
+      // per-slice write counts of stage_write)
+      if ((i & 1) || i == 0) return;
+      constexpr int c[3] = {6, 6, 4};
+      const int o = (i >> 1) - 1;
+      if (o >= c[slice]) return;
+      const int k = (slice > 0 ? c[0] : 0) + (slice > 1 ? c[1] : 0) + o;
+      load1(Rs, s + 3, k);
+    } else if constexpr (kSpreadPacked) {
+      if (slice < 2 && (i & 3) == 2) load1(Rs, s + 3, 4 * slice + (i >> 2));  // x after its write at i - 1
+      // W group 0 after slice 0's dequant, group 1 after slice 1's
+      if (slice == 1 && (i & 1) && i < 7) {
+        const int j = i >> 1;  // 0 q, 1 s, 2 m
+        const int idx = 8 + 2 * j;
+        if (idx < kLoads) load1(Rs, s + 3, idx);
+      }
+      if (slice == 2 && !(i & 1) && i < 6) {
+        const int j = i >> 1;
+        const int idx = 9 + 2 * j;
+        if (idx < kLoads) load1(Rs, s + 3, idx);
+      }
+    }
+  };
   bf16x8 A0[TI], B0[TJ], A1[TI], B1[TJ];
   auto step = [&](int s, WideRegs<WF>& Rs) {
     const int cur = s & 1, nxt = cur ^ 1;
@@ -960,6 +989,7 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
         stage_write(Rs, xsn, nxt, 0, i);
       }
       wpiece(Rs, nxt, 0, i);
+      early_load(Rs, s, 0, i);
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
@@ -968,6 +998,7 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
       if (read_slot(1, i) >= 0) read1(cur, 2, A0, B0, read_slot(1, i));
       stage_write(Rs, xsn, nxt, 1, i);
       wpiece(Rs, nxt, 1, i);
+      early_load(Rs, s, 1, i);
       __builtin_amdgcn_sched_barrier(0);
     }
 #pragma unroll
@@ -975,7 +1006,11 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
       mma1(A0, B0, i);
       if (read_slot(2, i) >= 0) read1(cur, 3, A1, B1, read_slot(2, i));
       stage_write(Rs, xsn, nxt, 2, i);
-      if (i < kLoads) load1(Rs, s + 3, i);
+      if constexpr (WQ4 && !kSpreadPacked) {
+        if (i < kLoads) load1(Rs, s + 3, i);
+      } else {
+        early_load(Rs, s, 2, i);
+      }
       __builtin_amdgcn_sched_barrier(0);
     }
     __syncthreads();
