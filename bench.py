@@ -299,10 +299,21 @@ PROFILES = os.path.join(ROOT, "profiles")
 CALIB_BYTES = 1 << 30  # the calibration copy reads and writes this many bytes
 
 
-def kernel_source_sha256():
+def kernel_code_text(text):
+    """The kernel source with comments, trailing blanks and empty lines taken
+    out: what the counters depend on (a comment edit leaves them valid)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    lines = [re.sub(r"//.*$", "", l).rstrip() for l in text.splitlines()]
+    return "\n".join(l for l in lines if l)
+
+
+def kernel_source_sha256(text=None):
     import hashlib
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    if text is None:
+        with open(KERNEL_SOURCE) as f:
+            text = f.read()
+    return hashlib.sha256(kernel_code_text(text).encode()).hexdigest()
 
 
 def traffic_file(config):
@@ -445,7 +456,7 @@ def pmc_summary(config, fetch_dir, write_dir, mfma_dir):
                      f"{e['write_bytes_per_step'] / 1e9:.3f} | {mb} |")
     lines += ["", "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES (summed over the 1024 SIMDs) / (1024 x GRBM_GUI_ACTIVE / 8), "
               "i.e. the fraction of the kernels' busy cycles in which a SIMD's matrix core is working.", "",
-              "bench.py reads the block below while the kernel source still has this SHA-256:", "",
+              "bench.py reads the block below while the kernel source, comments and blank lines aside, still has this SHA-256:", "",
               "```json", json.dumps(data, indent=1), "```", ""]
     return "\n".join(lines)
 

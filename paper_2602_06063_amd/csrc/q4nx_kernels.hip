@@ -695,14 +695,18 @@ __device__ __forceinline__ void gemm_tile_of(int wg, int ntiles, int tiles_n, in
 // a single wave per SIMD nothing hides a stall, so the instruction order is
 // fixed by hand: a K step is four blocks of 16 MFMA slots, each slot one MFMA
 // plus a fixed share of the other work, fenced so the compiler keeps it there:
-//   slots  0-15  MFMAs of K slice 0 | fragment reads of slice 1 | X tile of
-//                the next step into the other LDS stage | weight group 0 of
-//                the next step dequantized (a quarter of 8 columns per slot)
-//   slots 16-31  slice 1 | reads of slice 2 | weight group 1 dequantized
-//   slots 32-47  slice 2 | reads of slice 3 | global loads of step + 3
+//   slots  0-15  MFMAs of K slice 0 | fragment reads of slice 1 | part of
+//                the next step's tiles written to the other LDS stage (X, or
+//                bf16 W) | weight group 0 of the next step dequantized (a
+//                quarter of 8 columns per slot)
+//   slots 16-31  slice 1 | reads of slice 2 | more of the tiles | weight
+//                group 1 dequantized
+//   slots 32-47  slice 2 | reads of slice 3 | the rest of a bf16 W tile
 //   barrier      (the other stage is complete; this stage's reads are done)
 //   slots 48-63  slice 3 | reads of slice 0 of the next step
-// The raw operands of a step are loaded into registers two steps ahead.  X and
+// with the global loads of step + 3 issued as their registers free up (the
+// exact placement is given at the step function below).  The raw operands of
+// a step are loaded into registers two steps ahead.  X and
 // W are read through buffer descriptors limited to the tile's rows and strips;
 // in the last step of a K that is not a multiple of 64 the columns past K are
 // given an offset past the descriptor's end, which reads as zero -- code 0,
