@@ -412,7 +412,8 @@ def pmc_summary(config, fetch_dir, write_dir, mfma_dir):
     for d, (name, c) in fetch.items():
         k = kernel_family(name)
         if k:
-            fam.setdefault(k, {"dispatches": 0, "fetch_kib": 0.0, "write_kib": 0.0, "mfma_busy": 0.0, "gui_active": 0.0})
+            fam.setdefault(k, {"dispatches": 0, "fetch_kib": 0.0, "write_kib": 0.0, "mfma_busy": 0.0, "gui_active": 0.0,
+                               "valu_active": 0.0})
             fam[k]["dispatches"] += 1
             fam[k]["fetch_kib"] += c["FETCH_SIZE"]
     for d, (name, c) in write.items():
@@ -424,6 +425,7 @@ def pmc_summary(config, fetch_dir, write_dir, mfma_dir):
         if k:
             fam[k]["mfma_busy"] += c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
             fam[k]["gui_active"] += c.get("GRBM_GUI_ACTIVE", 0.0)
+            fam[k]["valu_active"] += c.get("SQ_ACTIVE_INST_VALU", 0.0)
     data = {"config": config, "kernel_source_sha256": kernel_source_sha256(),
             "calibration": {"bytes": CALIB_BYTES, "fetch_kib": calib_f, "write_kib": calib_w,
                             "fetch_scale": cf, "write_scale": cw},
@@ -435,27 +437,32 @@ def pmc_summary(config, fetch_dir, write_dir, mfma_dir):
         if v["mfma_busy"] > 0:
             # SQ_VALU_MFMA_BUSY_CYCLES is summed over all SIMDs; GRBM_GUI_ACTIVE over the 8 XCDs.
             e["mfma_busy_fraction"] = v["mfma_busy"] / (1024.0 * v["gui_active"] / 8.0)
+        if v["valu_active"] > 0:
+            # rocprofv3's VALUBusy: sum of SQ_ACTIVE_INST_VALU / CUs / GRBM_GUI_ACTIVE (per XCD).
+            e["valu_busy_fraction"] = v["valu_active"] / (256.0 * v["gui_active"] / 8.0)
         data["families"][k] = e
-    lines = [f"# HBM traffic and MFMA busy counters, bench configuration {config}", "",
+    lines = [f"# HBM traffic, MFMA and VALU busy counters, bench configuration {config}", "",
              "Three rocprofv3 counter passes over `python3 bench.py --config %d --pmc-pass` (one eager decode "
              "step, one prefill step, then a 1 GiB device-to-device copy used as the calibration):" % config, "",
              "```", "cd /tmp && export TMPDIR=/tmp && cd /root/repo",
              f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
              f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
-             f"rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE --output-format csv -d {mfma_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
+             f"rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_ACTIVE_INST_VALU GRBM_GUI_ACTIVE --output-format csv -d {mfma_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
              f"python3 bench.py --config {config} --pmc-summary {fetch_dir} {write_dir} {mfma_dir}",
              "```", "",
              "Calibration copy: FETCH_SIZE %.0f KiB and WRITE_SIZE %.0f KiB for %d bytes each way, so counter bytes are "
              "scaled by %.4f (fetch) and %.4f (write)." % (data["calibration"]["fetch_kib"], data["calibration"]["write_kib"],
                                                         CALIB_BYTES, cf, cw), "",
-             "| kernels | dispatches per step | HBM read (GB/step) | HBM write (GB/step) | MFMA busy |",
-             "|---|---:|---:|---:|---:|"]
+             "| kernels | dispatches per step | HBM read (GB/step) | HBM write (GB/step) | MFMA busy | VALU busy |",
+             "|---|---:|---:|---:|---:|---:|"]
     for k, e in data["families"].items():
         mb = "%.1f%%" % (100 * e["mfma_busy_fraction"]) if "mfma_busy_fraction" in e else "-"
+        vb = "%.1f%%" % (100 * e["valu_busy_fraction"]) if "valu_busy_fraction" in e else "-"
         lines.append(f"| {k} | {e['dispatches_per_step']} | {e['fetch_bytes_per_step'] / 1e9:.3f} | "
-                     f"{e['write_bytes_per_step'] / 1e9:.3f} | {mb} |")
+                     f"{e['write_bytes_per_step'] / 1e9:.3f} | {mb} | {vb} |")
     lines += ["", "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES (summed over the 1024 SIMDs) / (1024 x GRBM_GUI_ACTIVE / 8), "
-              "i.e. the fraction of the kernels' busy cycles in which a SIMD's matrix core is working.", "",
+              "i.e. the fraction of the kernels' busy cycles in which a SIMD's matrix core is working. "
+              "VALU busy = rocprofv3's derived VALUBusy, SQ_ACTIVE_INST_VALU (summed) / (256 CUs x GRBM_GUI_ACTIVE / 8).", "",
               "bench.py reads the block below while the kernel source, comments and blank lines aside, still has this SHA-256:", "",
               "```json", json.dumps(data, indent=1), "```", ""]
     return "\n".join(lines)
