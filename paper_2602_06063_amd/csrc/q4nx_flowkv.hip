@@ -56,6 +56,9 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
                                                                   int j0, int j1, float scale,
                                                                   float* __restrict__ work) {
   constexpr int kPart = D + 4;
+  // K and V rows in flight per lane: 4 for 512-byte rows (d = 256), 2 for
+  // 256-byte rows, where a deeper unroll measured slower.
+  constexpr int kFkvUnroll = D >= 256 ? 4 : 2;
   constexpr int R = D / 8;        // lanes per V row (16 bytes each)
   constexpr int P = 64 / R;       // V rows per wave load
   __shared__ __attribute__((aligned(16))) uint32_t qs[HG][D / 2];   // query bf16 pairs
@@ -78,7 +81,7 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
   // Scores (Eq. 6): 8 lanes per position (8 x 16 B = one 128-byte piece of
   // the row per load); lane u of the 8 takes dims 64i + 8u .. +7.
   const int u = lane & 7, kw = lane >> 3;
-#pragma unroll 2
+#pragma unroll kFkvUnroll
   for (int r = 0; r < CH / 32; ++r) {
     const int pl = (r * 4 + wave) * 8 + kw;
     float acc[HG];
@@ -144,7 +147,7 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
   for (int h = 0; h < HG; ++h)
 #pragma unroll
     for (int e = 0; e < 8; ++e) y[h][e] = 0.0f;
-#pragma unroll 2
+#pragma unroll kFkvUnroll
   for (int pl = wave * P + rs; pl < n; pl += 4 * P) {
     const uint4 w = reinterpret_cast<const uint4*>(Vg + (size_t)pl * D)[db];
     const float v[8] = {bf16lo(w.x), bf16hi(w.x), bf16lo(w.y), bf16hi(w.y),
