@@ -66,6 +66,8 @@ def parse():
     ap.add_argument("--decode-graph", type=int, default=1, help="replay the decode step as a HIP graph")
     ap.add_argument("--two-phase", type=int, default=1,
                     help="also time the two-phase prefill (q4nx_dequant to bf16, then q4nx_gemm_bf16)")
+    ap.add_argument("--bf16-out", type=int, default=1,
+                    help="also time the prefill step with bf16 outputs (the paper keeps every activation in bf16)")
     ap.add_argument("--quantize", type=int, default=1,
                     help="also time q4nx_quantize on the model's largest projection (float32 -> Q4NX)")
     ap.add_argument("--flowkv", type=int, default=1,
@@ -355,8 +357,9 @@ def trace_summary(trace_dir, bench_json):
     # Q4NX product dequantizes first, the dequant pass.  Other steps that use
     # them (the two-phase comparison, the MXFP4 variant) must be off in the
     # profiled run, or the attribution would mix them in.
-    if r.get("prefill", {}).get("two_phase") or "prefill" in (r.get("mxfp4") or {}):
-        raise SystemExit("profile with --two-phase 0 --mx 0: those steps launch the same kernels")
+    if r.get("prefill", {}).get("two_phase") or r.get("prefill", {}).get("bf16_outputs") or \
+            "prefill" in (r.get("mxfp4") or {}):
+        raise SystemExit("profile with --two-phase 0 --mx 0 --bf16-out 0: those steps launch the same kernels")
     fam = ("gemm256_kernel", "gemm_kernel", "splitk_sum_kernel", "dequant_kernel")
     gemm = [(n, c, t) for n, c, t in kern if any(f in n.split("(")[0] for f in fam)]
     gemm_t, gemm_c = sum(k[2] for k in gemm), sum(k[1] for k in gemm)
@@ -648,6 +651,7 @@ def main():
     # ---------------------------------------------------------------- prefill
     pre = Step(q4, stream.cuda_stream)
     two = Step(q4, stream.cuda_stream)   # two-phase: dequant to bf16 W, then the plain bf16 GEMM
+    pre16 = Step(q4, stream.cuda_stream)  # the prefill step with bf16 outputs
     mpre = Step(q4, stream.cuda_stream, mx=True)
     pre_flops = 0.0
     alg_pre = 0.0
@@ -657,17 +661,20 @@ def main():
     if do_prefill:
         Xs = {}
         Ys = [torch.empty((M_pre, N), dtype=torch.float32, device="cuda") for N, _ in shapes]
+        Ys16 = [torch.empty((M_pre, N), dtype=torch.bfloat16, device="cuda") for N, _ in shapes] if args.bf16_out else None
         Wtmp = torch.empty(max(N * K for N, K in shapes), dtype=torch.bfloat16, device="cuda")
         # One workspace for every GEMM of the steps (they run one after another):
         # split-K partials, and bf16 W where a Q4NX product dequantizes first.
         work_bytes = max(q4.q4nx_gemm_workspace_size(f, M_pre, N, K) for N, K in shapes
                          for f in (q4.Q4NX_WEIGHTS_Q4NX, q4.Q4NX_WEIGHTS_MXFP4, q4.Q4NX_WEIGHTS_BF16))
         gemm_work = torch.empty(max(work_bytes // 4, 1), dtype=torch.float32, device="cuda")
-        pre.work = two.work = mpre.work = gemm_work
+        pre.work = two.work = mpre.work = pre16.work = gemm_work
         for l in range(L):
             for gi, (N, K) in enumerate(shapes):
                 Xs[(l, gi)] = gen_activations_device((M_pre, K), seed=args.seed, layer=l, proj=GROUPS[gi][0])
                 pre.gemm(M_pre, N, K, Xs[(l, gi)], stacked[(l, gi)], Ys[gi], F32)
+                if args.bf16_out:
+                    pre16.gemm(M_pre, N, K, Xs[(l, gi)], stacked[(l, gi)], Ys16[gi], q4.Q4NX_BF16)
                 two.dequant_bf16(stacked[(l, gi)], N, K, Wtmp)
                 two.gemm_bf16(M_pre, N, K, Xs[(l, gi)], Wtmp, Ys[gi], F32)
                 pre_flops += 2.0 * M_pre * N * K
@@ -796,6 +803,18 @@ def main():
         for _ in range(args.warmup):
             two.run()
         _, two_ms, _ = timed(lambda: None, two.run, args.steps)
+    b16_ms, b16_equal = None, None
+    if do_prefill and args.bf16_out:
+        for _ in range(args.warmup):
+            pre16.run()
+        _, b16_ms, _ = timed(lambda: None, pre16.run, args.steps)
+        # The same accumulation rounded once: the bf16 outputs of the last
+        # layer's products must equal the float32 outputs rounded to bf16.
+        for fn, a in pre.calls[-len(GROUPS):] + pre16.calls[-len(GROUPS):]:
+            fn(*a)
+        torch.cuda.synchronize()
+        b16_equal = all(torch.equal(y16.view(torch.int16), y32.to(torch.bfloat16).view(torch.int16))
+                        for y16, y32 in zip(Ys16, Ys))
 
     # Bytes the launches must move at least once (operands in, results out).
     alg_dec = sum(N * K * WEIGHT_BYTES + 2 * K + 4 * N for _, N, K in model["proj"]) * L if do_decode else 0
@@ -959,6 +978,15 @@ def main():
                 "TFLOP_per_s": round(pre_flops / (t * 1e-3) / 1e12, 2),
                 "launches": len(two.calls),
                 "what": "per GEMM: q4nx_dequant to a bf16 W buffer, then q4nx_gemm_bf16 (same bits as q4nx_gemm)"}
+        if b16_ms:
+            t = sorted(b16_ms)[len(b16_ms) // 2]
+            result["prefill"]["bf16_outputs"] = {
+                "ms_median": round(t, 4), "ms_min": round(min(b16_ms), 4),
+                "TFLOP_per_s": round(pre_flops / (t * 1e-3) / 1e12, 2),
+                "frac_mfma": round(pre_flops / (t * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+                "equal_to_rounded_f32_outputs": bool(b16_equal),
+                "what": "the same step with bf16 outputs (the paper keeps every activation in bf16); each output "
+                        "is the float32 accumulation rounded once to bf16 by the kernels"}
         if do_decode:
             result["value_gemm"] = round(pre_tflops, 2)
     # Dominant kernel by time: the GEMM when the step has a prefill chunk.
