@@ -66,6 +66,8 @@ def parse():
     ap.add_argument("--decode-graph", type=int, default=1, help="replay the decode step as a HIP graph")
     ap.add_argument("--two-phase", type=int, default=1,
                     help="also time the two-phase prefill (q4nx_dequant to bf16, then q4nx_gemm_bf16)")
+    ap.add_argument("--fused", type=int, default=1,
+                    help="also time the prefill step through q4nx_gemm alone (fused dequant-GEMM, no workspace)")
     ap.add_argument("--bf16-out", type=int, default=1,
                     help="also time the prefill step with bf16 outputs (the paper keeps every activation in bf16)")
     ap.add_argument("--quantize", type=int, default=1,
@@ -168,6 +170,13 @@ class Step:
         wp, wn = self._work(self.wformat, M, N, K)
         self.calls.append((self.q4.lib.q4nx_gemm_ex, (self.wformat, M, N, K, X.data_ptr(), blob.data_ptr(),
                                                       Y.data_ptr(), ydt, wp, wn, self.s)))
+
+    def gemm_fused(self, M, N, K, X, blob, Y, ydt):
+        """q4nx_gemm: the fused dequant-GEMM, no workspace (no split K, no dequantize-once)."""
+        self.q4._need(blob, self.size(N, K), "blob")
+        self.q4._need(X, 2 * M * K, "X")
+        self.q4._need(Y, M * N * Y.element_size(), "Y")
+        self.calls.append((self.q4.lib.q4nx_gemm, (M, N, K, X.data_ptr(), blob.data_ptr(), Y.data_ptr(), ydt, self.s)))
 
     def dequant_bf16(self, blob, N, K, W):
         self.q4._need(blob, self.q4.q4nx_packed_size(N, K), "blob")
@@ -357,9 +366,10 @@ def trace_summary(trace_dir, bench_json):
     # Q4NX product dequantizes first, the dequant pass.  Other steps that use
     # them (the two-phase comparison, the MXFP4 variant) must be off in the
     # profiled run, or the attribution would mix them in.
-    if r.get("prefill", {}).get("two_phase") or r.get("prefill", {}).get("bf16_outputs") or \
-            "prefill" in (r.get("mxfp4") or {}):
-        raise SystemExit("profile with --two-phase 0 --mx 0 --bf16-out 0: those steps launch the same kernels")
+    pf = r.get("prefill", {})
+    if pf.get("two_phase") or pf.get("bf16_outputs") or pf.get("fused_only") or "prefill" in (r.get("mxfp4") or {}):
+        raise SystemExit("profile with --two-phase 0 --mx 0 --bf16-out 0 --fused 0: those steps launch the same "
+                         "kernels")
     fam = ("gemm256_kernel", "gemm_kernel", "splitk_sum_kernel", "dequant_kernel")
     gemm = [(n, c, t) for n, c, t in kern if any(f in n.split("(")[0] for f in fam)]
     gemm_t, gemm_c = sum(k[2] for k in gemm), sum(k[1] for k in gemm)
@@ -652,6 +662,7 @@ def main():
     pre = Step(q4, stream.cuda_stream)
     two = Step(q4, stream.cuda_stream)   # two-phase: dequant to bf16 W, then the plain bf16 GEMM
     pre16 = Step(q4, stream.cuda_stream)  # the prefill step with bf16 outputs
+    fus = Step(q4, stream.cuda_stream)    # the prefill step through q4nx_gemm alone
     mpre = Step(q4, stream.cuda_stream, mx=True)
     pre_flops = 0.0
     alg_pre = 0.0
@@ -675,6 +686,8 @@ def main():
                 pre.gemm(M_pre, N, K, Xs[(l, gi)], stacked[(l, gi)], Ys[gi], F32)
                 if args.bf16_out:
                     pre16.gemm(M_pre, N, K, Xs[(l, gi)], stacked[(l, gi)], Ys16[gi], q4.Q4NX_BF16)
+                if args.fused:
+                    fus.gemm_fused(M_pre, N, K, Xs[(l, gi)], stacked[(l, gi)], Ys[gi], F32)
                 two.dequant_bf16(stacked[(l, gi)], N, K, Wtmp)
                 two.gemm_bf16(M_pre, N, K, Xs[(l, gi)], Wtmp, Ys[gi], F32)
                 pre_flops += 2.0 * M_pre * N * K
@@ -803,6 +816,11 @@ def main():
         for _ in range(args.warmup):
             two.run()
         _, two_ms, _ = timed(lambda: None, two.run, args.steps)
+    fus_ms = None
+    if do_prefill and args.fused:
+        for _ in range(args.warmup):
+            fus.run()
+        _, fus_ms, _ = timed(lambda: None, fus.run, args.steps)
     b16_ms, b16_equal = None, None
     if do_prefill and args.bf16_out:
         for _ in range(args.warmup):
@@ -978,6 +996,13 @@ def main():
                 "TFLOP_per_s": round(pre_flops / (t * 1e-3) / 1e12, 2),
                 "launches": len(two.calls),
                 "what": "per GEMM: q4nx_dequant to a bf16 W buffer, then q4nx_gemm_bf16 (same bits as q4nx_gemm)"}
+        if fus_ms:
+            t = sorted(fus_ms)[len(fus_ms) // 2]
+            result["prefill"]["fused_only"] = {
+                "ms_median": round(t, 4), "ms_min": round(min(fus_ms), 4),
+                "TFLOP_per_s": round(pre_flops / (t * 1e-3) / 1e12, 2),
+                "what": "every product through q4nx_gemm: the fused dequant-GEMM (Eq. 3 in the tile loads), no "
+                        "workspace, so no split K and no dequantize-once"}
         if b16_ms:
             t = sorted(b16_ms)[len(b16_ms) // 2]
             result["prefill"]["bf16_outputs"] = {
