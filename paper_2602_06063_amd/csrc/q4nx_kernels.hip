@@ -687,6 +687,57 @@ __device__ __forceinline__ void gemm_tile_of(int wg, int ntiles, int tiles_n, in
 }
 
 
+// Output of one wave's TI x TJ accumulator blocks when its whole 32TI x 32TJ
+// sub-tile lies inside the matrix.  base (uniform over the wave) is the
+// sub-tile's first element, ldy
+// the row stride in elements (float32, or bf16 when bf16 != 0).  In the MFMA
+// layout, element e of lane l is column l%32 and row 8(e/4) + 4(l/32) + e%4
+// of its block: only the lane's own part of an address varies across the
+// wave, so every element is one buffer store whose block and row offset is a
+// scalar -- no per-element 64-bit address arithmetic and no bounds tests,
+// which made the plain per-element stores several times longer than the
+// memory needs to take them.
+template <int TI, int TJ>
+__device__ __forceinline__ void store_wave_tile(const f32x16 (&acc)[TI][TJ], void* base, int ldy, int bf16) {
+  // The lane index is recomputed here rather than kept live across the K loop.
+  const int lane = (int)__builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u));
+  const unsigned esz = bf16 ? 2u : 4u, rb = (unsigned)ldy * esz;
+  // base is the same in every lane; saying so keeps the descriptor scalar
+  // (otherwise each store may become a loop over distinct descriptors).
+  const uint64_t bp = reinterpret_cast<uint64_t>(base);
+  // (readfirstlane yields an int: each half goes through uint32_t so that the
+  // low word is not sign-extended into the high one.)
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)(bp >> 32));
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)bp);
+  void* const ub = reinterpret_cast<void*>(((uint64_t)hi << 32) | (uint64_t)lo);
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      ub, (short)0, (int)((32 * TI - 1) * rb + 32 * TJ * esz), 0x00020000);
+  const int vo = (int)(4u * (unsigned)(lane >> 5) * rb + (unsigned)(lane & 31) * esz);
+  if (bf16) {
+#pragma unroll
+    for (int a = 0; a < TI; ++a)
+#pragma unroll
+      for (int b = 0; b < TJ; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) {  // rows r and r + 1
+          const uint32_t v = pack_bf16x2(acc[a][b][e], acc[a][b][e + 1]);
+          const int so = (int)((unsigned)(32 * a + 8 * (e >> 2) + (e & 3)) * rb + 64u * b);
+          __builtin_amdgcn_raw_buffer_store_b16((unsigned short)v, rs, vo, so, 0);
+          __builtin_amdgcn_raw_buffer_store_b16((unsigned short)(v >> 16), rs, vo, so + (int)rb, 0);
+        }
+  } else {
+#pragma unroll
+    for (int a = 0; a < TI; ++a)
+#pragma unroll
+      for (int b = 0; b < TJ; ++b)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int so = (int)((unsigned)(32 * a + 8 * (e >> 2) + (e & 3)) * rb + 128u * b);
+          __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(acc[a][b][e]), rs, vo, so, 0);
+        }
+  }
+}
+
 // ---- 256 x 256 tile, one wave per SIMD ------------------------------------
 // Four waves in a 2 x 2 grid, each owning a 128 x 128 sub-tile: 16 MFMA
 // accumulators (256 accumulation registers, which live in the AGPR half of the
@@ -1077,6 +1128,13 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
   // full 64 x 64-bit multiply.)
   void* const Yo = part ? static_cast<void*>(part + (size_t)(blockIdx.y * (unsigned)M) * (unsigned)ldy) : Y;
   const int obf16 = part ? 0 : y_bf16;
+  if (full) {
+    store_wave_tile(acc,
+                    static_cast<char*>(Yo) + ((size_t)(unsigned)(m0 + 128 * wm) * (unsigned)ldy +
+                                              (unsigned)(n0 + 128 * wn)) * (obf16 ? 2u : 4u),
+                    ldy, obf16);
+    return;
+  }
 #pragma unroll
   for (int a = 0; a < TI; ++a)
 #pragma unroll
@@ -1316,6 +1374,13 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
   }
   mma_step(ks & 1);
 
+  if (m0 + BM <= M && n0 + BN <= N) {
+    store_wave_tile(acc,
+                    static_cast<char*>(Y) + ((size_t)(unsigned)(m0 + C::kWTM * wm) * (unsigned)ldy +
+                                             (unsigned)(n0 + C::kWTN * wn)) * (y_bf16 ? 2u : 4u),
+                    ldy, y_bf16);
+    return;
+  }
   // Accumulator element e of lane l: column l%32, row 8(e/4) + 4(l/32) + e%4.
 #pragma unroll
   for (int a = 0; a < C::kTI; ++a)
