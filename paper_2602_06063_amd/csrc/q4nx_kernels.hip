@@ -1538,12 +1538,18 @@ static size_t plan_work_bytes(const GemmRegion* plan, int count) {
 // W in bf16, a Q4NX product can dequantize each weight once instead (the
 // dequant kernel streams at ~5.5 TB/s) and run the same plan on the bf16
 // weights: the same bf16 values, the same MFMA chains and partial sums, so
-// the same bits.  On MI355X the bf16 product takes 0.85-0.93 of the fused
-// one's time, so the two-phase route is taken when the dequantization pass is
-// estimated below a tenth of the planned fused time -- the Gemma3 27B prefill
-// chunk (M = 4096) qualifies, M <= 2048 does not.  (The MXFP4 variant's
-// conversion is cheap enough that the fused kernel runs at the bf16 speed.)
-constexpr double kDequantLaunchUs = 3.0, kDequantBytesPerUs = 5.5e6, kTwoPhaseMaxShare = 0.10;
+// the same bits.  The fused kernel's extra work is Eq. 3 inside the K loop:
+// measured on MI355X it adds about a fifth of the K-loop time of the
+// 256 x 256 kernel (1.19-1.26 x the bf16 product's time on the Gemma3 4B and
+// 27B products) and about a seventh for the smaller tiles of the general
+// kernel, so the two-phase route is taken when the dequantization pass is
+// estimated below that share of the planned K-loop time: every Gemma3 27B
+// product at M = 4096, the 4B gate/up and down products at M = 2048, not the
+// 4B q/k/v and o products (short K, smaller tiles) nor M <= 1024.  (The
+// MXFP4 variant's conversion is cheap enough that the fused kernel runs at
+// the bf16 speed.)
+constexpr double kDequantLaunchUs = 3.0, kDequantBytesPerUs = 5.5e6;
+constexpr double kFusedExtraWide = 0.20, kFusedExtraSmall = 0.14;
 
 struct GemmChoice {
   GemmRegion plan[2];
@@ -1560,7 +1566,9 @@ static GemmChoice gemm_choose(int wf, int64_t M, int64_t N, int64_t K, bool have
   c.part_bytes = plan_work_bytes(c.plan, c.count);
   const double deq_us = kDequantLaunchUs + (kBlockBytes / (double)(kBlockRows * kBlockCols) + 2.0) * (double)N *
                                                (double)K / kDequantBytesPerUs;
-  c.two_phase = have_work && wf == kWQ4NX && deq_us < kTwoPhaseMaxShare * est_us;
+  const double kloop_us = est_us * kRoundPerKUs * (double)K / round_us(K);
+  const double extra = c.plan[0].tile == 0 ? kFusedExtraWide : kFusedExtraSmall;
+  c.two_phase = have_work && wf == kWQ4NX && deq_us < extra * kloop_us;
   c.w_bytes = c.two_phase ? (size_t)ceil_div(N * K * 2, 256) * 256 : 0;
   return c;
 }

@@ -307,12 +307,18 @@ def test_gemm_ex_workspace_size_and_validation():
     assert ws(7, 2048, 2560, 10240) == 0  # unknown format
     for f in (MX, BF):
         assert ws(f, 4096, 8192, 5376) == 0   # 512 tiles: two full rounds, nothing to split
-    # Q4NX at M = 4096: W is dequantized to bf16 in the workspace first
+    # Q4NX: W is dequantized to bf16 in the workspace first where the fused
+    # kernel's Eq. 3 work would cost more than the dequantization pass -- every
+    # product at M = 4096, the large 4B products at M = 2048 -- and not for the
+    # short-K 4B q/k/v and o products or at M = 1024 (the fused kernel).
     assert ws(Q, 4096, 8192, 5376) == 8192 * 5376 * 2
-    assert ws(Q, 2048, 20480, 2560) == 0      # M = 2048: the fused kernel
+    assert ws(Q, 2048, 20480, 2560) == 20480 * 2560 * 2
+    assert ws(Q, 2048, 4096, 2560) == 0 and ws(Q, 2048, 2560, 2048) == 0
+    assert ws(Q, 1024, 43008, 5376) == 0
     w = ws(BF, 2048, 2560, 10240)             # 80 tiles over a long K: split
     assert w > 0 and w % (4 * 2048 * 2560) == 0 and 2 <= w // (4 * 2048 * 2560) <= 4
-    assert ws(Q, 2048, 2560, 10240) == w and ws(MX, 2048, 2560, 10240) == w
+    assert ws(MX, 2048, 2560, 10240) == w
+    assert ws(Q, 2048, 2560, 10240) == 2560 * 10240 * 2 + w   # bf16 W, then the partials
     L = q4.lib
     args = lambda fmt, M, N, K, work, nbytes: (fmt, M, N, K, A16, A16, A16, 0, work, nbytes, None)
     assert L.q4nx_gemm_ex(*args(3, 4, 32, 256, None, 0)) == q4.Q4NX_ERR_INVALID_ARG
@@ -322,8 +328,9 @@ def test_gemm_ex_workspace_size_and_validation():
         assert L.q4nx_gemm_ex(*args(fmt, 4, 32, 80, None, 0)) == q4.Q4NX_ERR_SHAPE
         assert L.q4nx_gemm_ex(fmt, 4, 32, 256, None, A16, A16, 0, None, 0, None) == q4.Q4NX_ERR_INVALID_ARG
         assert L.q4nx_gemm_ex(fmt, 4, 32, 256, A16, MIS, A16, 0, None, 0, None) == q4.Q4NX_ERR_ALIGNMENT
-        assert L.q4nx_gemm_ex(*args(fmt, 2048, 2560, 10240, MIS, w)) == q4.Q4NX_ERR_ALIGNMENT
-        assert L.q4nx_gemm_ex(*args(fmt, 2048, 2560, 10240, A16, w - 1)) == q4.Q4NX_ERR_BUFFER_TOO_SMALL
+        wf = ws(fmt, 2048, 2560, 10240)
+        assert L.q4nx_gemm_ex(*args(fmt, 2048, 2560, 10240, MIS, wf)) == q4.Q4NX_ERR_ALIGNMENT
+        assert L.q4nx_gemm_ex(*args(fmt, 2048, 2560, 10240, A16, wf - 1)) == q4.Q4NX_ERR_BUFFER_TOO_SMALL
         assert L.q4nx_gemm_ex(*args(fmt, 2048, 2560, 10240, A16, 0)) == q4.Q4NX_ERR_BUFFER_TOO_SMALL
 
 
