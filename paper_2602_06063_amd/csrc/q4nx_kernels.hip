@@ -697,6 +697,11 @@ __device__ __forceinline__ void gemm_tile_of(int wg, int ntiles, int tiles_n, in
 // scalar -- no per-element 64-bit address arithmetic and no bounds tests,
 // which made the plain per-element stores several times longer than the
 // memory needs to take them.
+// Offsets inside a wave's sub-tile are 32-bit: its extent is below 2^31 bytes
+// for every row stride below 2^21 elements (at most 256 rows of 4 bytes).
+// Wider rows take the checked per-element stores, which address in 64 bits.
+constexpr int kFastStoreMaxLdy = 1 << 21;
+
 template <int TI, int TJ>
 __device__ __forceinline__ void store_wave_tile(const f32x16 (&acc)[TI][TJ], void* base, int ldy, int bf16) {
   // The lane index is recomputed here rather than kept live across the K loop.
@@ -1128,7 +1133,7 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
   // full 64 x 64-bit multiply.)
   void* const Yo = part ? static_cast<void*>(part + (size_t)(blockIdx.y * (unsigned)M) * (unsigned)ldy) : Y;
   const int obf16 = part ? 0 : y_bf16;
-  if (full) {
+  if (full && ldy < kFastStoreMaxLdy) {
     store_wave_tile(acc,
                     static_cast<char*>(Yo) + ((size_t)(unsigned)(m0 + 128 * wm) * (unsigned)ldy +
                                               (unsigned)(n0 + 128 * wn)) * (obf16 ? 2u : 4u),
@@ -1374,7 +1379,7 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
   }
   mma_step(ks & 1);
 
-  if (m0 + BM <= M && n0 + BN <= N) {
+  if (m0 + BM <= M && n0 + BN <= N && ldy < kFastStoreMaxLdy) {
     store_wave_tile(acc,
                     static_cast<char*>(Y) + ((size_t)(unsigned)(m0 + C::kWTM * wm) * (unsigned)ldy +
                                              (unsigned)(n0 + C::kWTN * wn)) * (y_bf16 ? 2u : 4u),

@@ -307,6 +307,41 @@ def test_gemm_launch_plans_sampled_rows(q4, M, N, K, bf16_out):
     assert tight
 
 
+@pytest.mark.parametrize("N", [(1 << 21) - 256, (1 << 21) + 256])
+def test_gemm_wide_rows_either_side_of_the_fast_store_stride(q4, N):
+    """Tiles inside the output store through 32-bit buffer offsets while the
+    row stride is below 2^21 elements, and element by element with 64-bit
+    addresses beyond it.  All 256 rows are checked at sampled columns around
+    2^21 and at both ends, float32 and bf16 outputs.  K is one group (32) to
+    keep W small; with so few terms one weight's bf16 rounding (up to 2^-8
+    relative) can exceed the projection tolerance, so the reference is the
+    float64 product of the bf16 weights the matrix cores consume, within the
+    tight bound (a misplaced or missing store fails it by orders of
+    magnitude)."""
+    M, K = 256, 32
+    _say("gemm wide rows", M, N, K)
+    codes, s, o = make(N, K, seed=21)
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    Xh = gen_activations((M, K), seed=21)
+    X = dev_bf16(Xh)
+    rng = np.random.default_rng(21)
+    cols = np.unique(np.concatenate([np.arange(64), (1 << 21) - 320 + np.arange(128), N - 64 + np.arange(64),
+                                     rng.integers(0, N, 64)]))
+    cols = cols[cols < N]
+    w16 = oracle.bf16_to_f32(oracle.f32_to_bf16(oracle.dequant_f32(codes[cols], s[cols], o[cols])))
+    ref, bound = oracle.gemm_f64(Xh, w16), oracle.abs_bound(Xh, w16)
+    idx = torch.from_numpy(cols).cuda()
+    for bf16_out in (False, True):
+        Y = torch.full((M, N), float("nan"), dtype=torch.bfloat16 if bf16_out else torch.float32, device="cuda")
+        q4.q4nx_gemm(M, N, K, X, blob, Y)
+        Yh = host_f32(Y.index_select(1, idx)).astype(np.float64)
+        tol = 1e-5 * bound + 1e-6 + (2.0 ** -8 * np.abs(ref) if bf16_out else 0)
+        err = np.abs(Yh - ref)
+        assert (err <= tol).all(), (bf16_out, float(np.nanmax(err / tol)))
+        del Y
+        torch.cuda.empty_cache()
+
+
 # ----------------------------------------------------------------- two-phase prefill
 # q4nx_dequant (bf16) then q4nx_gemm_bf16: the paper's dequantize-then-MM
 # structure.  Same bf16 weights and the same MFMA chain over K as the fused
