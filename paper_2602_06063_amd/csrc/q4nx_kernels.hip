@@ -1434,6 +1434,13 @@ struct GemmRegion {
 // ~5 us launch.
 constexpr double kRoundFixedUs = 40.0, kRoundPerKUs = 0.0226;
 constexpr double kSumLaunchUs = 5.0, kSumBytesPerUs = 5.0e6;
+// (The round costs and this model were fitted before the buffer-store
+// epilogue took 6-10 us off every round.  A refit from single full rounds,
+// about 16 + 0.0237 K us and costs 1 : 0.65 : 0.40 : 0.32, picks worse plans
+// for partly filled launches -- e.g. a two-shape split of 4096 x 2560 x 2048
+// that runs 23% slower than one partial round of 256 x 256 tiles -- while
+// the plans chosen here measure within 2% of the best forced plan on every
+// Gemma3 prefill product, so they are kept.)
 constexpr int kMinSegmentSteps = 8;
 
 static double round_us(int64_t K) { return kRoundFixedUs + kRoundPerKUs * (double)K; }
