@@ -82,8 +82,9 @@ def parse():
                          "counter passes), then exit")
     ap.add_argument("--trace-summary", nargs=2, metavar=("TRACE_DIR", "BENCH_JSON"),
                     help="summarise a rocprofv3 --kernel-trace --stats run of this benchmark as markdown")
-    ap.add_argument("--pmc-summary", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "MFMA_DIR"),
-                    help="summarise three rocprofv3 --pmc output folders of a --pmc-pass run as markdown")
+    ap.add_argument("--pmc-summary", nargs="+", metavar="DIR",
+                    help="summarise the rocprofv3 --pmc output folders of --pmc-pass runs as markdown: "
+                         "FETCH_DIR WRITE_DIR MFMA_DIR [LDS_DIR]")
     return ap.parse_args()
 
 
@@ -342,6 +343,12 @@ def kernel_family(name):
     return None
 
 
+def kernel_base_name(name):
+    """`void q4nx::gemm256_kernel<false, 0>(...)` -> `gemm256_kernel`."""
+    base = name.split("(")[0].split("<")[0].strip()
+    return base.split()[-1].split("::")[-1] if base else name
+
+
 def trace_summary(trace_dir, bench_json):
     """Markdown summary of a rocprofv3 --kernel-trace --stats run of this
     benchmark (its *kernel_stats.csv) next to the JSON line the same run
@@ -407,12 +414,20 @@ def read_pmc(folder):
     return out
 
 
-def pmc_summary(config, fetch_dir, write_dir, mfma_dir):
+LDS_COUNTERS = ("SQ_LDS_BANK_CONFLICT", "SQ_LDS_IDX_ACTIVE", "SQ_WAIT_INST_LDS", "SQ_WAIT_ANY", "SQ_WAVE_CYCLES",
+                "SQ_LDS_DATA_FIFO_FULL", "GRBM_GUI_ACTIVE")
+
+
+def pmc_summary(config, fetch_dir, write_dir, mfma_dir, lds_dir=None):
     """Markdown summary of the counter passes, with a JSON block that bench.py
     reads back (only while the kernel source is unchanged).  FETCH_SIZE and
     WRITE_SIZE are KiB per dispatch; each is scaled by bytes / counter of the
-    calibration copy (the last dispatch of the pass)."""
+    calibration copy (the last dispatch of the pass).  The optional fourth pass
+    gives, per kernel family, the share of LDS cycles lost to bank conflicts
+    and the shares of wave cycles spent waiting to issue an LDS instruction
+    and waiting on a memory counter (s_waitcnt)."""
     fetch, write, mfma = read_pmc(fetch_dir), read_pmc(write_dir), read_pmc(mfma_dir)
+    lds = read_pmc(lds_dir) if lds_dir else {}
 
     def calib(pass_, counter):
         # Copy dispatches after the last kernel of the path: the calibration copy.
@@ -439,6 +454,15 @@ def pmc_summary(config, fetch_dir, write_dir, mfma_dir):
             fam[k]["mfma_busy"] += c.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
             fam[k]["gui_active"] += c.get("GRBM_GUI_ACTIVE", 0.0)
             fam[k]["valu_active"] += c.get("SQ_ACTIVE_INST_VALU", 0.0)
+    # The LDS / wait pass is kept per kernel (the family mixes the products
+    # with the streaming dequant and partial-sum passes).
+    per_kernel = {}
+    for d, (name, c) in lds.items():
+        if kernel_family(name):
+            kn = kernel_base_name(name)
+            acc = per_kernel.setdefault(kn, {})
+            for ctr in LDS_COUNTERS[:-1]:
+                acc[ctr] = acc.get(ctr, 0.0) + c.get(ctr, 0.0)
     data = {"config": config, "kernel_source_sha256": kernel_source_sha256(),
             "calibration": {"bytes": CALIB_BYTES, "fetch_kib": calib_f, "write_kib": calib_w,
                             "fetch_scale": cf, "write_scale": cw},
@@ -454,14 +478,27 @@ def pmc_summary(config, fetch_dir, write_dir, mfma_dir):
             # rocprofv3's VALUBusy: sum of SQ_ACTIVE_INST_VALU / CUs / GRBM_GUI_ACTIVE (per XCD).
             e["valu_busy_fraction"] = v["valu_active"] / (256.0 * v["gui_active"] / 8.0)
         data["families"][k] = e
+    if per_kernel:
+        data["kernels_lds"] = {}
+        for kn, v in sorted(per_kernel.items()):
+            e = {}
+            if v.get("SQ_LDS_IDX_ACTIVE", 0.0) > 0:
+                e["lds_bank_conflict_fraction"] = v["SQ_LDS_BANK_CONFLICT"] / v["SQ_LDS_IDX_ACTIVE"]
+            if v.get("SQ_WAVE_CYCLES", 0.0) > 0:
+                e["wait_lds_issue_fraction"] = v["SQ_WAIT_INST_LDS"] / v["SQ_WAVE_CYCLES"]
+                e["wait_memory_fraction"] = v["SQ_WAIT_ANY"] / v["SQ_WAVE_CYCLES"]
+            data["kernels_lds"][kn] = e
     lines = [f"# HBM traffic, MFMA and VALU busy counters, bench configuration {config}", "",
-             "Three rocprofv3 counter passes over `python3 bench.py --config %d --pmc-pass` (one eager decode "
-             "step, one prefill step, then a 1 GiB device-to-device copy used as the calibration):" % config, "",
+             "%s rocprofv3 counter passes over `python3 bench.py --config %d --pmc-pass` (one eager decode "
+             "step, one prefill step, then a 1 GiB device-to-device copy used as the calibration):"
+             % ("Four" if lds_dir else "Three", config), "",
              "```", "cd /tmp && export TMPDIR=/tmp && cd /root/repo",
              f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
              f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
              f"rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES SQ_ACTIVE_INST_VALU GRBM_GUI_ACTIVE --output-format csv -d {mfma_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
-             f"python3 bench.py --config {config} --pmc-summary {fetch_dir} {write_dir} {mfma_dir}",
+             *([f"rocprofv3 --pmc {' '.join(LDS_COUNTERS)} --output-format csv -d {lds_dir} -o run -- python3 bench.py --config {config} --pmc-pass"]
+               if lds_dir else []),
+             f"python3 bench.py --config {config} --pmc-summary {fetch_dir} {write_dir} {mfma_dir}" + (f" {lds_dir}" if lds_dir else ""),
              "```", "",
              "Calibration copy: FETCH_SIZE %.0f KiB and WRITE_SIZE %.0f KiB for %d bytes each way, so counter bytes are "
              "scaled by %.4f (fetch) and %.4f (write)." % (data["calibration"]["fetch_kib"], data["calibration"]["write_kib"],
@@ -475,7 +512,17 @@ def pmc_summary(config, fetch_dir, write_dir, mfma_dir):
                      f"{e['write_bytes_per_step'] / 1e9:.3f} | {mb} | {vb} |")
     lines += ["", "MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES (summed over the 1024 SIMDs) / (1024 x GRBM_GUI_ACTIVE / 8), "
               "i.e. the fraction of the kernels' busy cycles in which a SIMD's matrix core is working. "
-              "VALU busy = rocprofv3's derived VALUBusy, SQ_ACTIVE_INST_VALU (summed) / (256 CUs x GRBM_GUI_ACTIVE / 8).", "",
+              "VALU busy = rocprofv3's derived VALUBusy, SQ_ACTIVE_INST_VALU (summed) / (256 CUs x GRBM_GUI_ACTIVE / 8)."]
+    if lds:
+        lines += ["", "| kernel | LDS bank conflicts (of LDS cycles) | waiting to issue an LDS instruction | waiting on memory (s_waitcnt) |",
+                  "|---|---:|---:|---:|"]
+        for k, e in data.get("kernels_lds", {}).items():
+            if "wait_lds_issue_fraction" in e:
+                lines.append(f"| {k} | {100 * e.get('lds_bank_conflict_fraction', 0.0):.1f}% | "
+                             f"{100 * e['wait_lds_issue_fraction']:.1f}% | {100 * e['wait_memory_fraction']:.1f}% |")
+        lines += ["", "Shares: SQ_LDS_BANK_CONFLICT / SQ_LDS_IDX_ACTIVE, and SQ_WAIT_INST_LDS and SQ_WAIT_ANY over "
+                  "SQ_WAVE_CYCLES (all summed over the kernel's dispatches in the step, every template instance)."]
+    lines += ["",
               "bench.py reads the block below while the kernel source, comments and blank lines aside, still has this SHA-256:", "",
               "```json", json.dumps(data, indent=1), "```", ""]
     return "\n".join(lines)
@@ -595,6 +642,8 @@ def run_single(args, cfg, q4, torch):
 def main():
     args = parse()
     if args.pmc_summary:
+        if len(args.pmc_summary) not in (3, 4):
+            sys.exit("--pmc-summary takes FETCH_DIR WRITE_DIR MFMA_DIR [LDS_DIR]")
         print(pmc_summary(args.config, *args.pmc_summary))
         return
     if args.trace_summary:

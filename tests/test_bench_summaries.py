@@ -86,8 +86,20 @@ def test_pmc_summary_scaling_and_busy_fractions(tmp_path, monkeypatch):
                   (gemm, {"GRBM_GUI_ACTIVE": [1000.0] * 8, "SQ_VALU_MFMA_BUSY_CYCLES": [512000.0],
                           "SQ_ACTIVE_INST_VALU": [51200.0]}),
                   (copy, {"GRBM_GUI_ACTIVE": [10.0] * 8})])
-    md = bench.pmc_summary(4, f, w, m)
+    lds = str(tmp_path / "lds")
+    # gemm: 250 of 1000 LDS cycles in conflicts; 100 and 50 of 1000 wave cycles waiting on LDS issue / memory
+    _pmc_pass(lds, [(gemv, {"SQ_WAVE_CYCLES": [500.0], "SQ_WAIT_INST_LDS": [0.0], "SQ_WAIT_ANY": [200.0]}),
+                    (gemm, {"SQ_LDS_BANK_CONFLICT": [125.0, 125.0], "SQ_LDS_IDX_ACTIVE": [500.0, 500.0],
+                            "SQ_WAVE_CYCLES": [1000.0], "SQ_WAIT_INST_LDS": [100.0], "SQ_WAIT_ANY": [50.0]})])
+    md = bench.pmc_summary(4, f, w, m, lds)
     data = json.loads(re.search(r"```json\n(.*?)\n```", md, re.S).group(1))
+    kl = data["kernels_lds"]
+    assert kl["gemm256_kernel"]["lds_bank_conflict_fraction"] == pytest.approx(0.25)
+    assert kl["gemm256_kernel"]["wait_lds_issue_fraction"] == pytest.approx(0.1)
+    assert kl["gemm256_kernel"]["wait_memory_fraction"] == pytest.approx(0.05)
+    assert kl["gemv_kernel"]["wait_memory_fraction"] == pytest.approx(0.4)
+    assert "| gemm256_kernel | 25.0% | 10.0% | 5.0% |" in md and md.startswith("# HBM") and "Four rocprofv3" in md
+    assert "Three rocprofv3" in bench.pmc_summary(4, f, w, m)
     assert data["calibration"]["fetch_scale"] == pytest.approx(2.0)
     assert data["calibration"]["write_scale"] == pytest.approx(1.0)
     gv, gm = data["families"]["gemv"], data["families"]["gemm"]
