@@ -651,8 +651,8 @@ def main():
         return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on one GPU only: this build measures the single-GPU path "
-              "(multi-GPU sharding is a design note, not an implementation).", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library implements and measures the single-GPU path "
+              "(how it would shard over several GPUs is described, not implemented).", file=sys.stderr)
         sys.exit(2)
 
     import torch
