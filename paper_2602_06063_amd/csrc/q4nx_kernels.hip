@@ -309,7 +309,9 @@ __global__ __launch_bounds__(256) void quantize_kernel(const float* __restrict__
           q = 0;
         } else {
           const float l_lo = fmaf((float)(cnt - 1), d, m);
-          const int q_lo = levels_below(l_lo, d, m);  // first code with that level
+          // The first code with that level: cnt - 1 unless the level below is
+          // the same value (a d small next to m), then the binary search.
+          const int q_lo = (cnt == 1 || fmaf((float)(cnt - 2), d, m) < l_lo) ? cnt - 1 : levels_below(l_lo, d, m);
           if (cnt == 16) {
             q = q_lo;
           } else {

@@ -393,7 +393,7 @@ def _edge_weights(N, K, seed):
     rng = np.random.default_rng(seed)
     W = (rng.standard_normal((N, K)) * 0.02).astype(np.float32)
     G = K // 32
-    kinds = rng.integers(0, 8, size=(N, G))
+    kinds = rng.integers(0, 9, size=(N, G))
     for n in range(N):
         for g in range(G):
             sl = W[n, 32 * g:32 * g + 32]
@@ -413,6 +413,11 @@ def _edge_weights(N, K, seed):
                 sl[7] = -0.0
             elif k == 6:
                 sl[:] = -np.abs(sl) - np.float32(3.0)                       # offset far from zero
+            elif k == 7:
+                # d far below the float32 spacing at m (0.125 at 2^20): Eq. 3 levels repeat, and
+                # the inputs sit on that spacing, so many are equal to a level or halfway between
+                sl[:] = np.float32(2.0 ** 20) + rng.integers(0, 8, 32).astype(np.float32) * np.float32(0.125)
+                sl[0], sl[1] = np.float32(2.0 ** 20), np.float32(2.0 ** 20 + 0.875)
     return W
 
 
