@@ -4,7 +4,7 @@
 // its sliding-window variant.
 //
 // The sweep is split in two launches.  Phase 1 gives every (KV group, chunk of
-// 64, 128 or 256 positions) to one workgroup, which computes for the H/G query heads
+// 64, 128, 256 or 512 positions) to one workgroup, which computes for the H/G query heads
 // of the group the chunk's own running state: the max score m_c (Eq. 7), the
 // denominator l_c = sum exp(s - m_c) (Eq. 8, 10) and the weighted values
 // Y_c = sum exp(s - m_c) v (Eq. 11), into the caller's workspace.  Phase 2
@@ -114,11 +114,16 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
   __syncthreads();
 
   // Chunk max (Eq. 7), exponentials (Eq. 8) and their sum (Eq. 10);
-  // thread tid < CH owns position tid.
+  // thread tid owns positions tid, tid + 256, ... below CH.
+  constexpr int kOwn = (CH + kFkvThreads - 1) / kFkvThreads;
   float m[HG], l[HG];
 #pragma unroll
   for (int h = 0; h < HG; ++h) {
-    const float v = wave_max(tid < CH ? fs[tid][h] : -INFINITY);
+    float v = -INFINITY;
+#pragma unroll
+    for (int o = 0; o < kOwn; ++o)
+      if (tid + o * kFkvThreads < CH) v = fmaxf(v, fs[tid + o * kFkvThreads][h]);
+    v = wave_max(v);
     if (lane == 0) red[wave][h] = v;
   }
   __syncthreads();
@@ -128,9 +133,14 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
 #pragma unroll
   for (int h = 0; h < HG; ++h) {
     float f = 0.0f;
-    if (tid < CH) {
-      f = expf(fs[tid][h] - m[h]);   // exp(-inf) = 0 past the range
-      fs[tid][h] = f;
+#pragma unroll
+    for (int o = 0; o < kOwn; ++o) {
+      const int p = tid + o * kFkvThreads;
+      if (p < CH) {
+        const float e = expf(fs[p][h] - m[h]);   // exp(-inf) = 0 past the range
+        fs[p][h] = e;
+        f += e;
+      }
     }
     const float sm = wave_sum(f);
     if (lane == 0) red[wave][h] = sm;
@@ -263,13 +273,15 @@ static void launch_flowkv(const uint16_t* q, const uint16_t* K, const uint16_t* 
   }
 }
 
-// Chunk size: the largest of 256, 128, 64 positions that still gives at
+// Chunk size: the largest of 512, 256, 128, 64 positions that still gives at
 // least two workgroups per CU.
 template <int D, int HG>
 static void launch_chunked(const uint16_t* q, const uint16_t* K, const uint16_t* V, int64_t L, int G, int j0, int j1,
                            float scale, float* work, void* out, int out_bf16, hipStream_t stream, int cus) {
   const int64_t n = j1 - j0;
-  if (ceil_div(n, 256) * G >= 2 * cus)
+  if (ceil_div(n, 512) * G >= 2 * cus)
+    launch_flowkv<512, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream);
+  else if (ceil_div(n, 256) * G >= 2 * cus)
     launch_flowkv<256, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream);
   else if (ceil_div(n, 128) * G >= 2 * cus)
     launch_flowkv<128, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream);
