@@ -143,10 +143,12 @@ def test_gemm_ex_repeatable_and_unsplit_without_workspace(q4):
     assert d <= 1e-4 * Ys[3].abs().max().item()
 
 
-@pytest.mark.parametrize("M,N,K,split", [(4096, 1024, 4096, False), (4096, 5376, 21504, True)])
+@pytest.mark.parametrize("M,N,K,split", [(4096, 1024, 4096, False), (4096, 5376, 21504, True),
+                                         (2048, 20480, 2560, False)])
 def test_gemm_ex_dequantize_then_multiply(q4, M, N, K, split):
-    """Shapes whose Q4NX workspace holds bf16 W: the result equals the fused
-    product of the same plan bit for bit (q4nx_gemm when nothing is split,
+    """Shapes whose Q4NX workspace holds bf16 W (M = 4096, and the 4B gate/up
+    product at M = 2048): the result equals the fused product of the same plan
+    bit for bit (q4nx_gemm when nothing is split,
     the bf16-weight product of the dequantized W when K is split), and meets
     the oracle on sampled rows."""
     _say("gemm_ex two-phase", M, N, K)
