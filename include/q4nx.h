@@ -56,18 +56,26 @@ extern "C" {
 struct ihipStream_t;
 typedef struct ihipStream_t* hipStream_t;
 
+/* The two range enumerators of the enums passed into the library make every
+ * 32-bit int a value of the type, so that an unknown value from a caller is
+ * well defined and rejected (Q4NX_ERR_INVALID_ARG, or "unknown status") (without them only the
+ * named values are valid values of the type in C++). */
 typedef enum q4nx_status {
   Q4NX_OK = 0,
   Q4NX_ERR_INVALID_ARG = 1,      /* NULL pointer, unknown dtype, code > 15, scale/offset outside the domain */
   Q4NX_ERR_SHAPE = 2,            /* M, N or K <= 0, K % 32 != 0, or a size beyond the supported range */
   Q4NX_ERR_ALIGNMENT = 3,        /* device pointer not aligned as documented */
   Q4NX_ERR_BUFFER_TOO_SMALL = 4, /* blob_bytes < q4nx_packed_size(N, K) */
-  Q4NX_ERR_HIP = 5               /* a HIP runtime call or kernel launch failed */
+  Q4NX_ERR_HIP = 5,              /* a HIP runtime call or kernel launch failed */
+  Q4NX_STATUS_RANGE_MIN_ = -2147483647 - 1,
+  Q4NX_STATUS_RANGE_MAX_ = 2147483647
 } q4nx_status;
 
 typedef enum q4nx_dtype {
   Q4NX_F32 = 0,  /* float32 */
-  Q4NX_BF16 = 1  /* bfloat16, round to nearest even from the float32 value */
+  Q4NX_BF16 = 1, /* bfloat16, round to nearest even from the float32 value */
+  Q4NX_DTYPE_RANGE_MIN_ = -2147483647 - 1,
+  Q4NX_DTYPE_RANGE_MAX_ = 2147483647
 } q4nx_dtype;
 
 /* Largest N and K accepted by every call (both < 2^31). */
@@ -271,7 +279,13 @@ q4nx_status q4nx_flowkv_decode(const uint16_t* d_q, const uint16_t* d_k, const u
  * result equals the matching entry point's bit for bit.  Errors: as
  * q4nx_gemm; Q4NX_ERR_BUFFER_TOO_SMALL if work_bytes is below the need.
  */
-typedef enum { Q4NX_WEIGHTS_Q4NX = 0, Q4NX_WEIGHTS_MXFP4 = 1, Q4NX_WEIGHTS_BF16 = 2 } q4nx_weights;
+typedef enum q4nx_weights {
+  Q4NX_WEIGHTS_Q4NX = 0,
+  Q4NX_WEIGHTS_MXFP4 = 1,
+  Q4NX_WEIGHTS_BF16 = 2,
+  Q4NX_WEIGHTS_RANGE_MIN_ = -2147483647 - 1, /* see q4nx_status */
+  Q4NX_WEIGHTS_RANGE_MAX_ = 2147483647
+} q4nx_weights;
 
 /* Bytes of workspace q4nx_gemm_ex may use for (w_format, M, N, K) on the
  * current device (0 when it would use none, or if an argument is invalid). */

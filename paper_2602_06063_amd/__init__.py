@@ -7,7 +7,8 @@ enqueue the library's HIP kernels on the current torch stream, or on the
 stream passed explicitly.  Nothing here computes any part of the projection.
 
 If the shared library is missing this module raises at import: there is no
-fallback path.
+fallback path.  Q4NX_LIBRARY, if set, names another build of the same library
+to load instead (the host-sanitized build of build.py --sanitize).
 """
 from __future__ import annotations
 
@@ -17,7 +18,7 @@ import os
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libq4nx.so")
+LIB_PATH = os.environ.get("Q4NX_LIBRARY") or os.path.join(_HERE, "libq4nx.so")
 
 Q4NX_OK = 0
 Q4NX_ERR_INVALID_ARG = 1

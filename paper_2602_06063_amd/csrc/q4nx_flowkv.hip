@@ -17,6 +17,7 @@
 #include <cmath>
 #include <string>
 
+#include "q4nx_device.h"
 #include "q4nx_internal.h"
 
 namespace q4nx {
@@ -301,17 +302,6 @@ static bool dispatch_hg(int hg, const uint16_t* q, const uint16_t* K, const uint
   }
 }
 
-static int fkv_device_cus() {
-  static int cus[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] == 0) {
-    int v = 0;
-    cus[dev] = (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && v > 0) ? v : 256;
-  }
-  return cus[dev];
-}
-
 }  // namespace q4nx
 
 using namespace q4nx;
@@ -348,7 +338,7 @@ q4nx_status q4nx_flowkv_decode(const uint16_t* d_q, const uint16_t* d_k, const u
   const int ob = o_dtype == Q4NX_BF16;
   float* work = static_cast<float*>(d_work);
   bool ok = false;
-  const int cus = fkv_device_cus();
+  const int cus = current_device_cus();
   if (d == 64) ok = dispatch_hg<64>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
   if (d == 128) ok = dispatch_hg<128>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
   if (d == 256) ok = dispatch_hg<256>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);

@@ -15,6 +15,7 @@
 #include <string>
 #include <vector>
 
+#include "q4nx_device.h"
 #include "q4nx_internal.h"
 
 namespace q4nx {
@@ -1455,16 +1456,7 @@ static int split_steps(int64_t K, int ks) {
   return (per >= kMinSegmentSteps && (ks - 1) * per < nsteps) ? (int)per : 0;
 }
 
-static int device_cus() {
-  static int cus[64] = {0};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cus[dev] == 0) {
-    int n = 0;
-    cus[dev] = (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && n > 0) ? n : 256;
-  }
-  return cus[dev];
-}
+static int device_cus() { return current_device_cus(); }
 
 // Chooses one launch, or two launches over a split of the rows or columns,
 // minimising the estimated time: sum over launches of (rounds of tiles on the
@@ -1594,13 +1586,9 @@ static q4nx_status launch_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* 
   const int64_t tiles_n = ceil_div(N, BN), tiles_m = ceil_div(M, BM);
   const size_t lds = sizeof(uint16_t) * Cfg::kLdsElems;
   auto kern = gemm_kernel<BM, BN, WAVES_M, WAVES_N, WF>;
-  static bool attr_set = false;  // LDS above 64 KiB must be requested once per kernel
-  if (!attr_set) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            (int)lds) != hipSuccess)
-      return fail(Q4NX_ERR_HIP, "q4nx_gemm: cannot reserve LDS");
-    attr_set = true;
-  }
+  static LdsReservation lds_res;  // LDS above 64 KiB, requested once per device
+  if (!lds_res.ensure(reinterpret_cast<const void*>(kern), (int)lds))
+    return fail(Q4NX_ERR_HIP, "q4nx_gemm: cannot reserve LDS");
   hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_n * tiles_m)), dim3(Cfg::kThreads), lds, stream, X,
                      static_cast<const uint8_t*>(blob), Y, (int)M, (int)N, (int)K, (int)ldy,
                      (int)ceil_div(K, kBlockCols), (int)ceil_div(N, kBlockRows), (int)tiles_n, y_bf16);
@@ -1611,13 +1599,9 @@ template <bool KTAIL, int WF>
 static q4nx_status launch_gemm256(int64_t M, int64_t N, int64_t K, const uint16_t* X, const void* blob, void* Y,
                                   int64_t ldy, int y_bf16, hipStream_t stream, int ks = 1, float* part = nullptr) {
   auto kern = gemm256_kernel<KTAIL, WF>;
-  static bool attr_set = false;
-  if (!attr_set) {
-    if (hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                            kWideLdsBytes) != hipSuccess)
-      return fail(Q4NX_ERR_HIP, "q4nx_gemm: cannot reserve LDS");
-    attr_set = true;
-  }
+  static LdsReservation lds_res;
+  if (!lds_res.ensure(reinterpret_cast<const void*>(kern), kWideLdsBytes))
+    return fail(Q4NX_ERR_HIP, "q4nx_gemm: cannot reserve LDS");
   const int64_t tiles_n = ceil_div(N, 256), tiles_m = ceil_div(M, 256);
   const int ksteps = ks > 1 ? split_steps(K, ks) : (int)ceil_div(K, kBK);
   hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_n * tiles_m), (unsigned)ks), dim3(kWideThreads), kWideLdsBytes,
