@@ -257,6 +257,30 @@ q4nx_status q4nx_flowkv_decode(const uint16_t* d_q, const uint16_t* d_k, const u
                                q4nx_dtype o_dtype, void* d_work, size_t work_bytes, hipStream_t stream);
 
 /*
+ * Device.  q4nx_flowkv_decode for callers that cannot allocate device memory
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same computation and the same kernels -- so the same
+ * bits -- with the chunk partials kept in the library's own static device
+ * array of Q4NX_FLOWKV_STATIC_BYTES (16 MiB) per device instead of a caller
+ * workspace.  Arguments as q4nx_flowkv_decode, without d_work/work_bytes.
+ * The array is held by every device the library runs on until the process
+ * ends; it is set up on the first call on each device (no allocation, no
+ * synchronization).  Every call on one device shares that device's array:
+ * calls that overlap on one device (concurrent streams, or host threads)
+ * race and give wrong results; calls in one stream order are safe.  Nothing
+ * in the array needs to start at zero (each call writes every partial it
+ * reads).  Errors: as q4nx_flowkv_decode; Q4NX_ERR_BUFFER_TOO_SMALL when the
+ * partials of the attended range, H * ceil(n / chunk) * (d + 4) * 4 bytes
+ * (chunk = the launch's chunk length, 64-512), exceed the array -- e.g. the
+ * Gemma3-27B geometry (H = 32, d = 128) up to about 64K attended positions
+ * at any chunk length; Q4NX_ERR_HIP if the array cannot be located.
+ */
+#define Q4NX_FLOWKV_STATIC_BYTES ((size_t)16 << 20)
+q4nx_status q4nx_flowkv_decode_static(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_v, int64_t H,
+                                      int64_t G, int64_t d, int64_t L, int64_t t, int64_t window, float scale,
+                                      void* d_o, q4nx_dtype o_dtype, hipStream_t stream);
+
+/*
  * The matrix product of q4nx_gemm, q4nx_mx_gemm and q4nx_gemm_bf16, with an
  * optional caller workspace (Sec. 3.1.2's tiled MM; the split along K is this
  * library's scheduling, not the paper's).

@@ -35,7 +35,7 @@ Q4NX_WEIGHTS_BF16 = 2
 
 EXPORTED = ["q4nx_packed_size", "q4nx_pack", "q4nx_unpack", "q4nx_quantize", "q4nx_dequant", "q4nx_gemv",
             "q4nx_gemv_batched", "q4nx_gemm", "q4nx_gemm_bf16", "q4nx_flowkv_workspace_size",
-            "q4nx_flowkv_decode", "q4nx_mx_packed_size", "q4nx_mx_pack", "q4nx_mx_unpack", "q4nx_mx_quantize", "q4nx_mx_dequant",
+            "q4nx_flowkv_decode", "q4nx_flowkv_decode_static", "q4nx_mx_packed_size", "q4nx_mx_pack", "q4nx_mx_unpack", "q4nx_mx_quantize", "q4nx_mx_dequant",
             "q4nx_mx_gemv", "q4nx_mx_gemv_batched", "q4nx_mx_gemm", "q4nx_gemm_workspace_size", "q4nx_gemm_ex", "q4nx_stream_read",
             "q4nx_status_str", "q4nx_last_error"]
 
@@ -83,6 +83,9 @@ lib.q4nx_flowkv_workspace_size.restype = _sz
 lib.q4nx_flowkv_decode.argtypes = [_vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, ctypes.c_float, _vp,
                                    ctypes.c_int, _vp, _sz, _vp]
 lib.q4nx_flowkv_decode.restype = ctypes.c_int
+lib.q4nx_flowkv_decode_static.argtypes = [_vp, _vp, _vp, _i64, _i64, _i64, _i64, _i64, _i64, ctypes.c_float, _vp,
+                                          ctypes.c_int, _vp]
+lib.q4nx_flowkv_decode_static.restype = ctypes.c_int
 lib.q4nx_mx_packed_size.argtypes = [_i64, _i64]
 lib.q4nx_mx_packed_size.restype = _sz
 lib.q4nx_mx_pack.argtypes = [_vp, _vp, _i64, _i64, _vp, _sz]
@@ -359,3 +362,16 @@ def q4nx_flowkv_decode(q, K, V, H: int, G: int, d: int, L: int, t: int, window: 
     _check(lib.q4nx_flowkv_decode(_dptr(q), _dptr(K), _dptr(V), H, G, d, L, t, window, scale, _dptr(o),
                                   _dtype_code(o), _dptr(work), work.numel() * work.element_size(), _stream(stream)),
            "q4nx_flowkv_decode")
+
+
+def q4nx_flowkv_decode_static(q, K, V, H: int, G: int, d: int, L: int, t: int, window: int, scale: float, o,
+                              stream=None):
+    """q4nx_flowkv_decode with the chunk partials in the library's static
+    device scratch (no workspace argument, nothing allocated)."""
+    _need(q, 2 * H * d, "q")
+    _need(K, 2 * G * L * d, "K")
+    _need(V, 2 * G * L * d, "V")
+    _need(o, H * d * o.element_size(), "o")
+    _check(lib.q4nx_flowkv_decode_static(_dptr(q), _dptr(K), _dptr(V), H, G, d, L, t, window, scale, _dptr(o),
+                                         _dtype_code(o), _stream(stream)),
+           "q4nx_flowkv_decode_static")

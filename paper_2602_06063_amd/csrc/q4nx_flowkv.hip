@@ -14,7 +14,9 @@
 // row is read once, by one workgroup, with full 128-byte rows per load.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
+#include <mutex>
 #include <string>
 
 #include "q4nx_device.h"
@@ -276,18 +278,21 @@ static void launch_flowkv(const uint16_t* q, const uint16_t* K, const uint16_t* 
 
 // Chunk size: the largest of 512, 256, 128, 64 positions that still gives at
 // least two workgroups per CU.
+static int flowkv_chunk(int64_t n, int G, int cus) {
+  for (int ch = 512; ch > kMinChunk; ch >>= 1)
+    if (ceil_div(n, ch) * G >= 2 * cus) return ch;
+  return kMinChunk;
+}
+
 template <int D, int HG>
 static void launch_chunked(const uint16_t* q, const uint16_t* K, const uint16_t* V, int64_t L, int G, int j0, int j1,
                            float scale, float* work, void* out, int out_bf16, hipStream_t stream, int cus) {
-  const int64_t n = j1 - j0;
-  if (ceil_div(n, 512) * G >= 2 * cus)
-    launch_flowkv<512, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream);
-  else if (ceil_div(n, 256) * G >= 2 * cus)
-    launch_flowkv<256, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream);
-  else if (ceil_div(n, 128) * G >= 2 * cus)
-    launch_flowkv<128, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream);
-  else
-    launch_flowkv<64, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream);
+  switch (flowkv_chunk(j1 - j0, G, cus)) {
+    case 512: launch_flowkv<512, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
+    case 256: launch_flowkv<256, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
+    case 128: launch_flowkv<128, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
+    default: launch_flowkv<64, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
+  }
 }
 
 template <int D>
@@ -300,6 +305,80 @@ static bool dispatch_hg(int hg, const uint16_t* q, const uint16_t* K, const uint
     case 8: launch_chunked<D, 8>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream, cus); return true;
     default: return false;
   }
+}
+
+// ---- scratch of the entry point that allocates nothing ----------------------
+// q4nx_flowkv_decode_static keeps the chunk partials in this array instead of
+// a caller workspace.  Each device holds its own copy, at its own address,
+// for the life of the process.  Host code never passes the array's name to a
+// kernel (on the host it is only a stand-in for the symbol): the device
+// address comes from hipGetSymbolAddress, taken once per device with that
+// device current.
+constexpr size_t kStaticScratchBytes = Q4NX_FLOWKV_STATIC_BYTES;
+static __device__ __align__(256) float scratch[kStaticScratchBytes / sizeof(float)];
+
+static q4nx_status static_scratch(float** out) {
+  static std::once_flag once[kMaxDevices];
+  static float* ptr[kMaxDevices] = {};
+  static hipError_t err[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+    return fail(Q4NX_ERR_HIP, "q4nx_flowkv_decode_static: no current device");
+  std::call_once(once[dev], [&] {
+    void* p = nullptr;
+    err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    ptr[dev] = static_cast<float*>(p);
+  });
+  if (err[dev] != hipSuccess || ptr[dev] == nullptr)
+    return fail(Q4NX_ERR_HIP, std::string("q4nx_flowkv_decode_static: hipGetSymbolAddress: ") +
+                                  hipGetErrorString(err[dev]));
+  *out = ptr[dev];
+  return Q4NX_OK;
+}
+
+// Validation and launch shared by both entry points.  Every argument is
+// checked before any HIP call.  work == nullptr selects the static scratch,
+// whose need is sized by the chunk length the launch will use; a caller
+// workspace is sized by the smallest chunk (q4nx_flowkv_workspace_size, which
+// callers use to allocate before the chunk length is known).
+static q4nx_status flowkv_entry(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_v, int64_t H, int64_t G,
+                                int64_t d, int64_t L, int64_t t, int64_t window, float scale, void* d_o,
+                                q4nx_dtype o_dtype, float* work, size_t work_bytes, hipStream_t stream,
+                                const char* fn) {
+  const std::string f(fn);
+  if (!d_q || !d_k || !d_v || !d_o) return fail(Q4NX_ERR_INVALID_ARG, f + ": NULL pointer");
+  if (o_dtype != Q4NX_F32 && o_dtype != Q4NX_BF16) return fail(Q4NX_ERR_INVALID_ARG, f + ": unknown o_dtype");
+  if (!std::isfinite(scale)) return fail(Q4NX_ERR_INVALID_ARG, f + ": scale must be finite");
+  if (H <= 0 || G <= 0 || H % G != 0 || G > 65535) return fail(Q4NX_ERR_SHAPE, f + ": H must be a positive multiple of G");
+  const int64_t hg = H / G;
+  if (hg != 1 && hg != 2 && hg != 4 && hg != 8) return fail(Q4NX_ERR_SHAPE, f + ": H/G must be 1, 2, 4 or 8");
+  if (d != 64 && d != 128 && d != 256) return fail(Q4NX_ERR_SHAPE, f + ": d must be 64, 128 or 256");
+  if (L <= 0 || L > (int64_t(1) << 30) || t < 0 || t >= L || window < 0)
+    return fail(Q4NX_ERR_SHAPE, f + ": need 0 <= t < L <= 2^30 and window >= 0");
+  if (!aligned(d_q, 16) || !aligned(d_k, 16) || !aligned(d_v, 16) || !aligned(d_o, 4))
+    return fail(Q4NX_ERR_ALIGNMENT, f + ": q, K and V need 16-byte alignment, o 4-byte");
+  const int64_t j1 = t + 1, j0 = window == 0 ? 0 : std::max<int64_t>(0, j1 - window);
+  if (work && work_bytes < q4nx_flowkv_workspace_size(H, d, j1 - j0))
+    return fail(Q4NX_ERR_BUFFER_TOO_SMALL, f + ": workspace smaller than q4nx_flowkv_workspace_size");
+  const int cus = current_device_cus();
+  if (!work) {
+    const size_t need = (size_t)H * (size_t)ceil_div(j1 - j0, flowkv_chunk(j1 - j0, (int)G, cus)) *
+                        (size_t)(d + 4) * sizeof(float);
+    if (need > kStaticScratchBytes)
+      return fail(Q4NX_ERR_BUFFER_TOO_SMALL, f + ": the chunk partials (" + std::to_string(need) +
+                                                 " bytes) exceed the static scratch (" +
+                                                 std::to_string(kStaticScratchBytes) + " bytes)");
+    if (q4nx_status st = static_scratch(&work)) return st;
+  }
+  const int ob = o_dtype == Q4NX_BF16;
+  bool ok = false;
+  if (d == 64) ok = dispatch_hg<64>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
+  if (d == 128) ok = dispatch_hg<128>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
+  if (d == 256) ok = dispatch_hg<256>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
+  if (!ok) return fail(Q4NX_ERR_SHAPE, f + ": unsupported shape");
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(Q4NX_ERR_HIP, f + ": " + hipGetErrorString(e));
+  return Q4NX_OK;
 }
 
 }  // namespace q4nx
@@ -317,35 +396,18 @@ q4nx_status q4nx_flowkv_decode(const uint16_t* d_q, const uint16_t* d_k, const u
                                int64_t d, int64_t L, int64_t t, int64_t window, float scale, void* d_o,
                                q4nx_dtype o_dtype, void* d_work, size_t work_bytes, hipStream_t stream) {
   clear_error();
-  if (!d_q || !d_k || !d_v || !d_o || !d_work) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_flowkv_decode: NULL pointer");
-  if (o_dtype != Q4NX_F32 && o_dtype != Q4NX_BF16)
-    return fail(Q4NX_ERR_INVALID_ARG, "q4nx_flowkv_decode: unknown o_dtype");
-  if (!std::isfinite(scale)) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_flowkv_decode: scale must be finite");
-  if (H <= 0 || G <= 0 || H % G != 0 || G > 65535)
-    return fail(Q4NX_ERR_SHAPE, "q4nx_flowkv_decode: H must be a positive multiple of G");
-  const int64_t hg = H / G;
-  if (hg != 1 && hg != 2 && hg != 4 && hg != 8)
-    return fail(Q4NX_ERR_SHAPE, "q4nx_flowkv_decode: H/G must be 1, 2, 4 or 8");
-  if (d != 64 && d != 128 && d != 256) return fail(Q4NX_ERR_SHAPE, "q4nx_flowkv_decode: d must be 64, 128 or 256");
-  if (L <= 0 || L > (int64_t(1) << 30) || t < 0 || t >= L || window < 0)
-    return fail(Q4NX_ERR_SHAPE, "q4nx_flowkv_decode: need 0 <= t < L <= 2^30 and window >= 0");
-  if (!aligned(d_q, 16) || !aligned(d_k, 16) || !aligned(d_v, 16) || !aligned(d_o, 4) || !aligned(d_work, 16))
-    return fail(Q4NX_ERR_ALIGNMENT, "q4nx_flowkv_decode: q, K, V and workspace need 16-byte alignment, o 4-byte");
-  const int64_t j1 = t + 1, j0 = window == 0 ? 0 : std::max<int64_t>(0, j1 - window);
-  const size_t need = q4nx_flowkv_workspace_size(H, d, j1 - j0);
-  if (work_bytes < need)
-    return fail(Q4NX_ERR_BUFFER_TOO_SMALL, "q4nx_flowkv_decode: workspace smaller than q4nx_flowkv_workspace_size");
-  const int ob = o_dtype == Q4NX_BF16;
-  float* work = static_cast<float*>(d_work);
-  bool ok = false;
-  const int cus = current_device_cus();
-  if (d == 64) ok = dispatch_hg<64>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
-  if (d == 128) ok = dispatch_hg<128>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
-  if (d == 256) ok = dispatch_hg<256>((int)hg, d_q, d_k, d_v, L, (int)G, (int)j0, (int)j1, scale, work, d_o, ob, stream, cus);
-  if (!ok) return fail(Q4NX_ERR_SHAPE, "q4nx_flowkv_decode: unsupported shape");
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return fail(Q4NX_ERR_HIP, std::string("q4nx_flowkv_decode: ") + hipGetErrorString(e));
-  return Q4NX_OK;
+  if (!d_work) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_flowkv_decode: NULL pointer");
+  if (!aligned(d_work, 16)) return fail(Q4NX_ERR_ALIGNMENT, "q4nx_flowkv_decode: workspace needs 16-byte alignment");
+  return flowkv_entry(d_q, d_k, d_v, H, G, d, L, t, window, scale, d_o, o_dtype, static_cast<float*>(d_work),
+                      work_bytes, stream, "q4nx_flowkv_decode");
+}
+
+q4nx_status q4nx_flowkv_decode_static(const uint16_t* d_q, const uint16_t* d_k, const uint16_t* d_v, int64_t H,
+                                      int64_t G, int64_t d, int64_t L, int64_t t, int64_t window, float scale,
+                                      void* d_o, q4nx_dtype o_dtype, hipStream_t stream) {
+  clear_error();
+  return flowkv_entry(d_q, d_k, d_v, H, G, d, L, t, window, scale, d_o, o_dtype, nullptr, 0, stream,
+                      "q4nx_flowkv_decode_static");
 }
 
 }  // extern "C"

@@ -385,3 +385,25 @@ def test_flowkv_workspace_size_and_validation():
     assert call(k=MIS) == q4.Q4NX_ERR_ALIGNMENT
     assert call(work=MIS) == q4.Q4NX_ERR_ALIGNMENT
     assert call(wb=8 * 260 * 4 - 1) == q4.Q4NX_ERR_BUFFER_TOO_SMALL
+
+
+def test_flowkv_static_validates_before_hip():
+    """The entry point that allocates nothing checks every argument before any
+    HIP call (these run without a GPU: each call fails validation)."""
+    import paper_2602_06063_amd as q4
+    L = q4.lib
+    A = ctypes.c_void_p(1 << 20)
+    MIS = ctypes.c_void_p((1 << 20) + 2)
+
+    def call(q=A, k=A, v=A, H=8, G=4, d=256, Lc=1024, t=10, win=0, scale=0.0625, o=A, odt=0):
+        return L.q4nx_flowkv_decode_static(q, k, v, H, G, d, Lc, t, win, scale, o, odt, None)
+    assert call(q=None) == q4.Q4NX_ERR_INVALID_ARG
+    assert call(o=None) == q4.Q4NX_ERR_INVALID_ARG
+    assert call(odt=7) == q4.Q4NX_ERR_INVALID_ARG
+    assert call(scale=float("nan")) == q4.Q4NX_ERR_INVALID_ARG
+    assert call(H=6, G=4) == q4.Q4NX_ERR_SHAPE
+    assert call(d=96) == q4.Q4NX_ERR_SHAPE
+    assert call(t=1024) == q4.Q4NX_ERR_SHAPE
+    assert call(win=-1) == q4.Q4NX_ERR_SHAPE
+    assert call(v=MIS) == q4.Q4NX_ERR_ALIGNMENT
+    assert "q4nx_flowkv_decode_static" in L.q4nx_last_error().decode()
