@@ -264,6 +264,7 @@ const char* q4nx_status_str(q4nx_status s) {
     case Q4NX_ERR_ALIGNMENT: return "misaligned pointer";
     case Q4NX_ERR_BUFFER_TOO_SMALL: return "buffer too small";
     case Q4NX_ERR_HIP: return "HIP error";
+    default: break;
   }
   return "unknown status";
 }

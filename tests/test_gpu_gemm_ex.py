@@ -174,3 +174,91 @@ def test_gemm_ex_dequantize_then_multiply(q4, M, N, K, split):
     w32 = oracle.dequant_f32(codes, s, o)
     ok, worst = oracle.check_close(host_f32(Y1)[rows], oracle.gemm_f64(Xh[rows], w32), oracle.abs_bound(Xh[rows], w32))
     assert ok, worst
+
+
+# Shapes whose tiles do not fill whole rounds of the 256 CUs, where the plan
+# mixes tile shapes or splits K: a round and a few tiles (4352 x 4096), two
+# rounds and a part (4352 x 8448), the Gemma3-4B o shape (80 tiles), few tiles
+# over a long K with M and N ragged (2000 x 1100 x 6912), and a K tail with a
+# ragged M (1999 x 2500 x 2016).
+ROUND_SHAPES = [(4352, 4096, 2560, 32), (4352, 8448, 2560, 32), (2048, 2560, 2048, 48), (2000, 1100, 6912, 48),
+                (1999, 2500, 2016, 48)]
+
+
+@pytest.mark.parametrize("M,N,K,nrows", ROUND_SHAPES)
+@pytest.mark.parametrize("bf16_out", [False, True])
+def test_gemm_ex_partial_round_parity(q4, M, N, K, nrows, bf16_out):
+    """The planned launches against the oracle on sampled rows, against the
+    bf16-weight product within the tight bound, and against the launch without
+    a workspace (no split) within the order of float32 sums."""
+    _say("gemm_ex partial round", M, N, K, "bf16" if bf16_out else "f32")
+    codes, s, o = gen_weights(N, K, seed=M + 3 * K)
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    Xh = gen_activations((M, K), seed=N + 5)
+    X = dev_bf16(Xh)
+    odt = torch.bfloat16 if bf16_out else torch.float32
+    Y = torch.empty((M, N), dtype=odt, device="cuda")
+    Y0 = torch.empty((M, N), dtype=odt, device="cuda")
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, Y, work=work_for(q4, M, N, K, q4.Q4NX_WEIGHTS_Q4NX))
+    q4.q4nx_gemm(M, N, K, X, blob, Y0)
+    Yh, Y0h = host_f32(Y), host_f32(Y0)
+    assert np.isfinite(Yh).all()
+    rows = _rows(M, nrows)
+    w32 = oracle.dequant_f32(codes, s, o)
+    ok, worst = oracle.check_close(Yh[rows], oracle.gemm_f64(Xh[rows], w32), oracle.abs_bound(Xh[rows], w32),
+                                   bf16_out=bf16_out)
+    assert ok, worst
+    w16 = oracle.bf16_to_f32(oracle.f32_to_bf16(w32))
+    ref16 = oracle.gemm_f64(Xh[rows], w16)
+    tight = np.abs(Yh[rows].astype(np.float64) - ref16) <= (
+        1e-5 * oracle.abs_bound(Xh[rows], w16) + 1e-6 + (2.0 ** -8 * np.abs(ref16) if bf16_out else 0))
+    assert tight.all()
+    # Every element, split or not, against the unsplit launch: the same
+    # products summed in another order (float32), or equal after bf16 rounding.
+    scale = np.abs(Y0h).max()
+    assert np.abs(Yh - Y0h).max() <= (1e-4 if not bf16_out else 2.0 ** -7) * scale
+
+
+@pytest.mark.parametrize("M,N,K", [(2048, 4096, 2560), (2048, 2560, 2048), (2048, 20480, 2560), (2048, 2560, 10240)])
+def test_gemm_ex_gemma3_4b_products(q4, M, N, K):
+    """The four stacked Gemma3-4B prefill products at M = 2048 (q/k/v, o,
+    gate/up, down) through the plans the benchmark runs, against the oracle on
+    sampled rows."""
+    _say("gemm_ex 4B", M, N, K)
+    codes, s, o = gen_weights(N, K, seed=N + K)
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    Xh = gen_activations((M, K), seed=K + 1)
+    Y = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, dev_bf16(Xh), blob, Y, work=work_for(q4, M, N, K, q4.Q4NX_WEIGHTS_Q4NX))
+    rows = _rows(M, 24)
+    w32 = oracle.dequant_f32(codes, s, o)
+    ok, worst = oracle.check_close(host_f32(Y)[rows], oracle.gemm_f64(Xh[rows], w32), oracle.abs_bound(Xh[rows], w32))
+    assert ok, worst
+
+
+def test_gemm_ex_split_repeats_with_workspace_cleared(q4):
+    """Ten calls in a row, the workspace refilled with NaN before each: a
+    partial read before its writer finished, or a tile counter taken over from
+    the previous call, would show as a NaN or a changed bit."""
+    M, N, K = 2048, 2560, 2048
+    _say("gemm_ex split repeats", M, N, K)
+    codes, s, o = gen_weights(N, K, seed=77)
+    blob = dev_u8(q4.q4nx_pack(codes, s, o))
+    X = dev_bf16(gen_activations((M, K), seed=78))
+    work = work_for(q4, M, N, K, q4.Q4NX_WEIGHTS_Q4NX)
+    ref = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, ref, work=work)
+    Y = torch.empty_like(ref)
+    for _ in range(10):
+        work.fill_(float("nan"))
+        Y.fill_(float("nan"))
+        q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, Y, work=work)
+        torch.cuda.synchronize()
+        assert torch.equal(Y.view(torch.int32), ref.view(torch.int32))
+    # And ten back to back without clearing (counters left by the previous
+    # call in place).
+    outs = [torch.empty_like(ref) for _ in range(10)]
+    for y in outs:
+        q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, y, work=work)
+    torch.cuda.synchronize()
+    assert all(torch.equal(y.view(torch.int32), ref.view(torch.int32)) for y in outs)
