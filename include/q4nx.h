@@ -368,10 +368,14 @@ q4nx_status q4nx_mx_gemm(int64_t M, int64_t N, int64_t K, const uint16_t* d_X, c
                          q4nx_dtype y_dtype, hipStream_t stream);
 
 /* Measurement aid (not part of the projection path): reads `bytes` (a multiple
- * of 16) of device memory once with the GEMV's load pattern and writes 2048
- * floats (one per workgroup) to d_sink, which must hold them.  Timing it gives
- * the read bandwidth a streaming kernel reaches on the device.  Device,
- * asynchronous; errors as above (d_src 16-byte aligned). */
+ * of 16, below 2^42) of device memory once with the GEMV's load pattern -- 2048
+ * workgroups of 4 waves, workgroup b reading the b-th of 2048 equal contiguous
+ * slices -- and writes 8192 floats to d_sink, which must hold them: float
+ * 4b + w is the XOR of every 32-bit word wave w of workgroup b read (the
+ * slice's 16-byte pieces p with p % 256 in [64w, 64w + 64)), masked to its low
+ * 30 bits.  Timing it gives the read bandwidth, and the per-launch floor, of a
+ * plain streaming kernel.  Device, asynchronous; errors as above (d_src
+ * 16-byte aligned). */
 q4nx_status q4nx_stream_read(const void* d_src, size_t bytes, float* d_sink, hipStream_t stream);
 
 /* Static description of a status code. */

@@ -341,8 +341,8 @@ def q4nx_gemm_ex(w_format: int, M: int, N: int, K: int, X, W, Y, work=None, stre
 
 
 def q4nx_stream_read(src, sink, stream=None):
-    """Measurement aid: read all of `src` once (sink: 2048 float32)."""
-    _need(sink, 4 * 2048, "sink")
+    """Measurement aid: read all of `src` once (sink: 8192 float32, one fold per wave)."""
+    _need(sink, 4 * 8192, "sink")
     _check(lib.q4nx_stream_read(_dptr(src), src.numel() * src.element_size(), _dptr(sink), _stream(stream)),
            "q4nx_stream_read")
 

@@ -420,6 +420,8 @@ constexpr int kGroupPadDw = 20;  // dwords per staged group (16 bf16 pairs + 4 p
 constexpr int kRedFloats = kGemvMaxWaves * 32;
 // Blocks in flight per wave (register slots), by row octets per wave.
 constexpr int kGemvDepth4 = 1, kGemvDepth2 = 3, kGemvDepth1 = 4;
+// Workgroups per CU of the streaming form (gemv_stream_kernel), LDS permitting.
+constexpr int kGemvStreamPerCu = 4;
 // 16-byte pieces of x per thread requested before the first weight blocks.
 template <int TQ>
 constexpr int gemv_xpre() {
@@ -650,6 +652,161 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
       }
     }
     __syncthreads();  // red[] is rewritten by the next row group
+  }
+}
+
+// Persistent streaming form of gemv_kernel, for launches whose K fits one
+// staged piece of x (every Gemma3 K).  A job's row groups are dealt to a
+// bounded number of workgroups, rg = r0, r0 + nwg, ...; a workgroup stages x
+// once and each wave streams its blocks of all its row groups (w, w + W, ...
+// of each) through one ring of D register slots that runs on across row
+// groups, so the next row group's loads are in flight while the current one's
+// rows are added up and stored.  The arithmetic and the order of every sum
+// are those of gemv_kernel (same waves per row group), hence the same bits.
+// Every wave meets the same barriers: two to stage x, two per row group.
+template <int TQ, int D, int F>
+__global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_stream_kernel(const GemvArgs args) {
+  constexpr int kBytes = wblock_bytes<F>();
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  float* red = lds;
+  float* ssum = lds + kRedFloats;
+  uint32_t* xs = reinterpret_cast<uint32_t*>(ssum + args.chunk_blocks * kGroupsPerRow);
+
+  const int wg = blockIdx.x;
+  int jb = 0;
+#pragma unroll
+  for (int t = 1; t < Q4NX_MAX_BATCH; ++t)
+    if (t < args.njobs && wg >= args.job[t].wg_begin) jb = t;
+  const GemvJob& J = args.job[jb];
+
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int c = lane & 7;
+  const int W = J.waves, nb = J.KB;
+  const int nthreads = blockDim.x;
+  const bool wave_on = w < W;  // wave-uniform
+  const int r0 = wg - J.wg_begin;
+  const int nrg = r0 < J.nrg ? (J.nrg - 1 - r0) / J.nwg + 1 : 0;  // row groups of this workgroup
+  if (nrg == 0) return;                                           // the whole workgroup
+  const int nbw = wave_on ? (nb - w + W - 1) / W : 0;              // this wave's blocks per row group
+  const int Q = nbw * nrg;
+  const int kvalid = J.K;
+  const int sbytes = nb * kBytes;  // bytes of one strip
+
+  // Load cursor: row group lk of this workgroup, this wave's block ljq of it.
+  int lk = 0, ljq = 0;
+  auto load_next = [&](GemvSlot<TQ>& R, int& jj) {
+    const int row0 = (r0 + lk * J.nwg) * 8 * TQ;
+    jj = w + ljq * W;
+    gemv_load<TQ, F>(chunk_rsrc(J.blob + (size_t)(row0 >> 5) * sbytes, sbytes), jj, (row0 & 31) >> 3, lane, R);
+    if (++ljq == nbw) {
+      ljq = 0;
+      ++lk;
+    }
+  };
+
+  // The first pieces of x are requested before the weight blocks (every
+  // workgroup waits for x before it computes anything), then the wave's
+  // first D blocks, then x is staged as in gemv_kernel.
+  constexpr int kXPre = gemv_xpre<TQ>();
+  u32x4 xpre[kXPre];
+#pragma unroll
+  for (int i = 0; i < kXPre; ++i) {
+    const int e = threadIdx.x + i * nthreads;
+    const int k = 8 * e;
+    xpre[i] = (u32x4){0u, 0u, 0u, 0u};
+    if (e < nb * (kBlockCols / 8) && k < J.K) xpre[i] = *reinterpret_cast<const u32x4*>(J.x + k);
+  }
+  GemvSlot<TQ> buf[D];
+  int jjs[D];
+#pragma unroll
+  for (int d = 0; d < D; ++d) {
+    jjs[d] = 0;
+    if (d < Q) load_next(buf[d], jjs[d]);
+  }
+  {
+    int it = 0;
+    for (int e = threadIdx.x; e < nb * (kBlockCols / 8); e += nthreads, ++it) {
+      const int k = 8 * e;
+      u32x4 v = (u32x4){0u, 0u, 0u, 0u};
+      if (it < kXPre) {
+#pragma unroll
+        for (int i = 0; i < kXPre; ++i)
+          if (i == it) v = xpre[i];
+      } else if (k < J.K) {
+        v = *reinterpret_cast<const u32x4*>(J.x + k);
+      }
+      if constexpr (F == kWMX) {
+        *reinterpret_cast<u32x4*>(xs + (e >> 2) * kGroupPadDw + 4 * (e & 3)) = v;
+        continue;
+      }
+      const uint32_t p02 = (v[0] & 0xFFFFu) | (v[1] << 16), p46 = (v[2] & 0xFFFFu) | (v[3] << 16);
+      const uint32_t p13 = (v[0] >> 16) | (v[1] & 0xFFFF0000u), p57 = (v[2] >> 16) | (v[3] & 0xFFFF0000u);
+      const int g = e >> 2;
+      *reinterpret_cast<u32x4*>(xs + g * kGroupPadDw + 4 * (e & 3)) = (u32x4){p02, p46, p13, p57};
+      float sm = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sm += __uint_as_float(v[i] << 16) + __uint_as_float(v[i] & 0xFFFF0000u);
+      sm += __shfl_xor(sm, 1);
+      sm += __shfl_xor(sm, 2);
+      if ((threadIdx.x & 3) == 0) ssum[g] = sm;
+    }
+  }
+  __syncthreads();
+
+  // Row group k of this workgroup is complete in every wave: add the 8 groups
+  // of each row, then the W waves' sums in wave order, and store.
+  float acc[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+  auto finish = [&](int k) {
+#pragma unroll
+    for (int t = 0; t < TQ; ++t) {
+      acc[t] += __shfl_xor(acc[t], 1);
+      acc[t] += __shfl_xor(acc[t], 2);
+      acc[t] += __shfl_xor(acc[t], 4);
+    }
+    if (wave_on && c < TQ) {
+      const float v = (c == 0) ? acc[0] : (c == 1) ? acc[1] : (c == 2) ? acc[2] : acc[3];
+      red[w * 32 + 8 * c + (lane >> 3)] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < 8 * TQ) {
+      float sum = 0.0f;
+      for (int q = 0; q < W; ++q) sum += red[q * 32 + threadIdx.x];
+      const int64_t n = (int64_t)(r0 + k * J.nwg) * 8 * TQ + threadIdx.x;
+      if (n < J.N) {
+        if (args.y_bf16)
+          static_cast<uint16_t*>(J.y)[n] = f32_to_bf16_bits(sum);
+        else
+          static_cast<float*>(J.y)[n] = sum;
+      }
+    }
+    __syncthreads();  // red[] is rewritten for the next row group
+#pragma unroll
+    for (int t = 0; t < 4; ++t) acc[t] = 0.0f;
+  };
+
+  if (Q == 0) {  // a wave without blocks still meets every barrier
+    for (int k = 0; k < nrg; ++k) finish(k);
+    return;
+  }
+  // Ring of D slots: block q of the wave's stream lives in slot q % D and the
+  // slot is refilled with block q + D right after it is consumed.
+  int ck = 0, cjq = 0;
+  for (int q0 = 0; q0 < Q; q0 += D) {
+#pragma unroll
+    for (int d = 0; d < D; ++d) {
+      const int q = q0 + d;
+      if (q < Q) {
+        const int jj = jjs[d];
+        gemv_compute<TQ, F>(buf[d], jj * kBlockCols + kGroup * c < kvalid, xs + (jj * kGroupsPerRow + c) * kGroupPadDw,
+                            F == kWMX ? 0.0f : ssum[jj * kGroupsPerRow + c], acc);
+        if (q + D < Q) load_next(buf[d], jjs[d]);
+        if (++cjq == nbw) {
+          finish(ck);
+          cjq = 0;
+          ++ck;
+        }
+      }
+    }
   }
 }
 
@@ -1728,10 +1885,21 @@ static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtyp
       return fail(Q4NX_ERR_ALIGNMENT, std::string(fn) + ": blob/x need 16-byte, y 4-byte alignment");
     strips += ceil_div(d.N, kBlockRows);
   }
-  const int tq = gemv_tq(strips);
-  int min_kb = 1 << 30;
-  for (int i = 0; i < count; ++i) min_kb = std::min<int>(min_kb, (int)ceil_div(descs[i].K, kBlockCols));
-  const int waves = gemv_waves(strips * (4 / tq), min_kb);
+  int min_kb = 1 << 30, max_kb = 0;
+  for (int i = 0; i < count; ++i) {
+    min_kb = std::min<int>(min_kb, (int)ceil_div(descs[i].K, kBlockCols));
+    max_kb = std::max<int>(max_kb, (int)ceil_div(descs[i].K, kBlockCols));
+  }
+  // Launches of 80-159 strips take the streaming form with half-strip row
+  // groups, 8 waves each.  Measured on MI355X in whole Gemma3 decode steps:
+  // the 4B step 3% faster (its q/k/v, o and down launches); with quarter-strip
+  // groups at 160-256 strips the 27B step was 2% slower (although each of
+  // those launch types alone, repeated, ran 2-5% faster), so those launches
+  // keep gemv_kernel.
+  const bool streaming = max_kb <= kGemvChunkBlocks && strips >= 80 && strips < 160;
+  const int tq = streaming ? 2 : gemv_tq(strips);
+  int waves = streaming ? 8 : gemv_waves(strips * (4 / tq), min_kb);
+  while (waves > 1 && waves > min_kb) waves >>= 1;
   GemvArgs args = {};
   args.njobs = count;
   args.y_bf16 = (y_dtype == Q4NX_BF16);
@@ -1759,7 +1927,24 @@ static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtyp
     args.chunk_blocks = std::max(args.chunk_blocks, std::min(J.KB, kGemvChunkBlocks));
   }
   const size_t lds = sizeof(float) * ((size_t)kRedFloats + (size_t)args.chunk_blocks * kGroupsPerRow * (1 + kGroupPadDw));
-  const dim3 grid((unsigned)wg), block(64 * max_waves);
+  const dim3 block(64 * max_waves);
+  if (streaming) {
+    // Streaming form: a bounded grid (workgroups per CU as the LDS allows, at
+    // most kGemvStreamPerCu), dealt to the jobs in proportion to their row
+    // groups; each workgroup walks its job's row groups r0, r0 + nwg, ...
+    const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(kGemvStreamPerCu, (160 * 1024) / (int64_t)lds));
+    const int64_t total_rg = strips * (4 / tq), budget = (int64_t)device_cus() * per_cu;
+    int64_t sw = 0;
+    for (int i = 0; i < count; ++i) {
+      GemvJob& J = args.job[i];
+      J.nwg = (int)std::max<int64_t>(1, std::min<int64_t>(J.nrg, (budget * J.nrg + total_rg - 1) / total_rg));
+      J.wg_begin = (int)sw;
+      sw += J.nwg;
+    }
+    hipLaunchKernelGGL((gemv_stream_kernel<2, kGemvDepth2, F>), dim3((unsigned)sw), block, lds, stream, args);
+    return check_launch(fn);
+  }
+  const dim3 grid((unsigned)wg);
   switch (tq) {
     case 4: hipLaunchKernelGGL((gemv_kernel<4, kGemvDepth4, F>), grid, block, lds, stream, args); break;
     case 2: hipLaunchKernelGGL((gemv_kernel<2, kGemvDepth2, F>), grid, block, lds, stream, args); break;
@@ -1789,31 +1974,31 @@ static q4nx_status dequant_entry(const void* d_blob, int64_t N, int64_t K, void*
 }
 
 // Measurement aid: read a buffer once with the GEMV's load pattern (16-byte
-// non-temporal loads, a workgroup per contiguous slice) and fold it into one
-// float per workgroup, so that nothing is dead code.  Gives the read bandwidth
-// a streaming kernel reaches on the device, beside the vendor's HBM figure.
+// non-temporal loads, a workgroup per contiguous slice, through a buffer
+// descriptor limited to the slice, so no load needs a bounds test) and fold it
+// into one value per wave (lane shuffles, no LDS and no barrier), so that
+// nothing is dead code and the kernel has no tail beyond the loads.  Gives the
+// read bandwidth, and the per-launch floor, of a plain streaming kernel.
 constexpr int kStreamWgs = 2048;
-__global__ __launch_bounds__(256) void stream_read_kernel(const u32x4* __restrict__ src, int64_t n16,
+__global__ __launch_bounds__(256) void stream_read_kernel(const uint8_t* __restrict__ src, int64_t n16,
                                                           float* __restrict__ sink) {
   const int64_t per = (n16 + gridDim.x - 1) / gridDim.x;
   const int64_t b = (int64_t)blockIdx.x * per, e = min(n16, b + per);
+  const int cnt = (int)max<int64_t>(0, e - b);  // 16-byte pieces of this slice
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(src) + (e > b ? b * 16 : 0), (short)0, cnt * 16, 0x00020000);
   uint32_t acc = 0;
-  for (int64_t i = b + threadIdx.x; i < e; i += 4 * 256) {
+  for (int i = threadIdx.x; i < cnt; i += 4 * 256) {
     u32x4 v[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u)
-      v[u] = i + u * 256 < e ? __builtin_nontemporal_load(src + i + u * 256) : (u32x4){0u, 0u, 0u, 0u};
+      v[u] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs, (i + u * 256) * 16, 0, kNtLoad));
 #pragma unroll
     for (int u = 0; u < 4; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
   }
-  __shared__ uint32_t red[256];
-  red[threadIdx.x] = acc;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    uint32_t t = 0;
-    for (int k = 0; k < 256; ++k) t ^= red[k];
-    sink[blockIdx.x] = __uint_as_float(t & 0x3FFFFFFFu);
-  }
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) acc ^= (uint32_t)__shfl_xor((int)acc, o);
+  if ((threadIdx.x & 63) == 0) sink[blockIdx.x * 4 + (threadIdx.x >> 6)] = __uint_as_float(acc & 0x3FFFFFFFu);
 }
 
 }  // namespace q4nx
@@ -1863,9 +2048,10 @@ q4nx_status q4nx_mx_quantize(const float* d_W, int64_t N, int64_t K, void* d_blo
 q4nx_status q4nx_stream_read(const void* d_src, size_t bytes, float* d_sink, hipStream_t stream) {
   clear_error();
   if (!d_src || !d_sink) return fail(Q4NX_ERR_INVALID_ARG, "q4nx_stream_read: NULL pointer");
-  if (bytes == 0 || bytes % 16 != 0) return fail(Q4NX_ERR_SHAPE, "q4nx_stream_read: bytes must be a positive multiple of 16");
+  if (bytes == 0 || bytes % 16 != 0 || bytes / kStreamWgs >= (size_t(1) << 31))
+    return fail(Q4NX_ERR_SHAPE, "q4nx_stream_read: bytes must be a positive multiple of 16, below 2^42");
   if (!aligned(d_src, 16) || !aligned(d_sink, 4)) return fail(Q4NX_ERR_ALIGNMENT, "q4nx_stream_read: src needs 16-byte alignment");
-  hipLaunchKernelGGL(stream_read_kernel, dim3(kStreamWgs), dim3(256), 0, stream, static_cast<const u32x4*>(d_src),
+  hipLaunchKernelGGL(stream_read_kernel, dim3(kStreamWgs), dim3(256), 0, stream, static_cast<const uint8_t*>(d_src),
                      (int64_t)(bytes / 16), d_sink);
   return check_launch("q4nx_stream_read");
 }

@@ -56,6 +56,13 @@ def work_for(q4, M, N, K, fmt=None):
     return torch.full((nbytes // 4,), float("nan"), dtype=torch.float32, device="cuda")
 
 
+def work_if_any(q4, M, N, K, fmt):
+    """The workspace the planner asks for (NaN-filled), or None when its plan
+    takes none."""
+    nbytes = q4.q4nx_gemm_workspace_size(fmt, M, N, K)
+    return torch.full((nbytes // 4,), float("nan"), dtype=torch.float32, device="cuda") if nbytes else None
+
+
 # (M, N, K, rows checked by the oracle: None = all)
 SPLIT_SHAPES = [(512, 512, 16384, None), (512, 512, 16352, None), (300, 520, 20000, None), (260, 257, 12000, None),
                 (1, 256, 20480, None), (2048, 2560, 10240, 64), (2048, 2560, 10208, 64), (4096, 5376, 21504, 48)]
@@ -181,17 +188,20 @@ def test_gemm_ex_dequantize_then_multiply(q4, M, N, K, split):
 # rounds and a part (4352 x 8448), the Gemma3-4B o shape (80 tiles), few tiles
 # over a long K with M and N ragged (2000 x 1100 x 6912), and a K tail with a
 # ragged M (1999 x 2500 x 2016).
-ROUND_SHAPES = [(4352, 4096, 2560, 32), (4352, 8448, 2560, 32), (2048, 2560, 2048, 48), (2000, 1100, 6912, 48),
-                (1999, 2500, 2016, 48)]
+# Ragged prefill-sized shapes; the planner takes a different plan for each:
+# dequantize-once with a partial last wave of tiles (the first two), the
+# direct fused launch (the third and fifth), split K (the fourth).
+PLANNED_SHAPES = [(4352, 4096, 2560, 32), (4352, 8448, 2560, 32), (2048, 2560, 2048, 48), (2000, 1100, 6912, 48),
+                  (1999, 2500, 2016, 48)]
 
 
-@pytest.mark.parametrize("M,N,K,nrows", ROUND_SHAPES)
+@pytest.mark.parametrize("M,N,K,nrows", PLANNED_SHAPES)
 @pytest.mark.parametrize("bf16_out", [False, True])
-def test_gemm_ex_partial_round_parity(q4, M, N, K, nrows, bf16_out):
+def test_gemm_ex_planned_parity(q4, M, N, K, nrows, bf16_out):
     """The planned launches against the oracle on sampled rows, against the
     bf16-weight product within the tight bound, and against the launch without
     a workspace (no split) within the order of float32 sums."""
-    _say("gemm_ex partial round", M, N, K, "bf16" if bf16_out else "f32")
+    _say("gemm_ex planned", M, N, K, "bf16" if bf16_out else "f32")
     codes, s, o = gen_weights(N, K, seed=M + 3 * K)
     blob = dev_u8(q4.q4nx_pack(codes, s, o))
     Xh = gen_activations((M, K), seed=N + 5)
@@ -199,7 +209,7 @@ def test_gemm_ex_partial_round_parity(q4, M, N, K, nrows, bf16_out):
     odt = torch.bfloat16 if bf16_out else torch.float32
     Y = torch.empty((M, N), dtype=odt, device="cuda")
     Y0 = torch.empty((M, N), dtype=odt, device="cuda")
-    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, Y, work=work_for(q4, M, N, K, q4.Q4NX_WEIGHTS_Q4NX))
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, Y, work=work_if_any(q4, M, N, K, q4.Q4NX_WEIGHTS_Q4NX))
     q4.q4nx_gemm(M, N, K, X, blob, Y0)
     Yh, Y0h = host_f32(Y), host_f32(Y0)
     assert np.isfinite(Yh).all()
@@ -229,7 +239,8 @@ def test_gemm_ex_gemma3_4b_products(q4, M, N, K):
     blob = dev_u8(q4.q4nx_pack(codes, s, o))
     Xh = gen_activations((M, K), seed=K + 1)
     Y = torch.empty((M, N), dtype=torch.float32, device="cuda")
-    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, dev_bf16(Xh), blob, Y, work=work_for(q4, M, N, K, q4.Q4NX_WEIGHTS_Q4NX))
+    q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, dev_bf16(Xh), blob, Y,
+                    work=work_if_any(q4, M, N, K, q4.Q4NX_WEIGHTS_Q4NX))
     rows = _rows(M, 24)
     w32 = oracle.dequant_f32(codes, s, o)
     ok, worst = oracle.check_close(host_f32(Y)[rows], oracle.gemm_f64(Xh[rows], w32), oracle.abs_bound(Xh[rows], w32))
@@ -237,10 +248,10 @@ def test_gemm_ex_gemma3_4b_products(q4, M, N, K):
 
 
 def test_gemm_ex_split_repeats_with_workspace_cleared(q4):
-    """Ten calls in a row, the workspace refilled with NaN before each: a
-    partial read before its writer finished, or a tile counter taken over from
-    the previous call, would show as a NaN or a changed bit."""
-    M, N, K = 2048, 2560, 2048
+    """Ten calls of a split-K plan in a row, the workspace refilled with NaN
+    before each: a partial read before its writer finished, or one left over
+    from the previous call, would show as a NaN or a changed bit."""
+    M, N, K = 2000, 1100, 6912
     _say("gemm_ex split repeats", M, N, K)
     codes, s, o = gen_weights(N, K, seed=77)
     blob = dev_u8(q4.q4nx_pack(codes, s, o))
@@ -255,7 +266,7 @@ def test_gemm_ex_split_repeats_with_workspace_cleared(q4):
         q4.q4nx_gemm_ex(q4.Q4NX_WEIGHTS_Q4NX, M, N, K, X, blob, Y, work=work)
         torch.cuda.synchronize()
         assert torch.equal(Y.view(torch.int32), ref.view(torch.int32))
-    # And ten back to back without clearing (counters left by the previous
+    # And ten back to back without clearing (the partials of the previous
     # call in place).
     outs = [torch.empty_like(ref) for _ in range(10)]
     for y in outs:

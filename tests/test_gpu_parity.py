@@ -439,18 +439,20 @@ def test_quantize_bit_exact(q4, N, K, kind):
 
 # ----------------------------------------------------------------- measurement aid
 def test_stream_read_folds_every_word(q4):
-    """q4nx_stream_read reads every 16-byte piece exactly once: its per-
-    workgroup XOR fold equals the fold computed on the host."""
+    """q4nx_stream_read reads every 16-byte piece exactly once: its per-wave
+    XOR fold equals the fold computed on the host."""
     n16 = 2048 * 37 + 5            # slices of unequal length, some workgroups past the end
     data = np.random.default_rng(8).integers(0, 2 ** 32, size=4 * n16, dtype=np.uint32)
     src = torch.from_numpy(data.view(np.uint8)).cuda()
-    sink = torch.empty(2048, dtype=torch.float32, device="cuda")
+    sink = torch.empty(8192, dtype=torch.float32, device="cuda")
     q4.q4nx_stream_read(src, sink)
     got = sink.cpu().numpy().view(np.uint32)
     per = -(-n16 // 2048)
     words = data.reshape(n16, 4)
-    want = np.zeros(2048, np.uint32)
+    want = np.zeros(8192, np.uint32)
     for b in range(2048):
-        sl = words[b * per:min(n16, (b + 1) * per)]
-        want[b] = np.bitwise_xor.reduce(sl.reshape(-1)) if sl.size else 0
+        lo, hi = b * per, min(n16, (b + 1) * per)
+        for w in range(4):
+            idx = [p for p in range(lo, hi) if (p - lo) % 256 // 64 == w]
+            want[4 * b + w] = np.bitwise_xor.reduce(words[idx].reshape(-1)) if idx else 0
     assert np.array_equal(got, want & np.uint32(0x3FFFFFFF))
