@@ -35,6 +35,7 @@ from __future__ import annotations
 import argparse
 import ctypes
 import json
+import re
 import os
 import sys
 import time
@@ -79,6 +80,9 @@ def parse():
     ap.add_argument("--context", type=int, default=32768, help="decode position + 1 for the FlowKV timing")
     ap.add_argument("--mx", type=int, default=1,
                     help="also time the decode and prefill steps over MXFP4-variant weights")
+    ap.add_argument("--with-4b", type=int, default=1,
+                    help="with the default 27B configuration, also run the 4B decode step and prefill chunk "
+                         "(configurations 2 and 3) and report them beside it")
     ap.add_argument("--pmc-pass", action="store_true",
                     help="run one eager decode step, one prefill step and a 1 GiB device copy (for rocprofv3 "
                          "counter passes), then exit")
@@ -201,6 +205,207 @@ class Step:
                 raise RuntimeError(f"{fn.__name__}: status {st}: {self.q4.lib.q4nx_last_error().decode()}")
 
 
+def time_steps(torch, stream, fn, steps):
+    """Runs fn `steps` times back to back, each between an event pair on
+    `stream`; returns (median ms, min ms)."""
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    ts = sorted(a.elapsed_time(b) for a, b in evs)
+    return ts[len(ts) // 2], ts[0]
+
+
+def capture(torch, stream, fn):
+    """fn captured as a HIP graph on `stream` (run once eagerly first)."""
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=stream):
+        fn()
+    return g
+
+
+def faster_launch_mode(torch, stream, run, outputs, warmup):
+    """The decode step as a HIP graph, checked bit for bit against eager
+    launches on three replays (outputs cleared in between), and the faster
+    of graph and eager by a short timing; returns (fn, info)."""
+    run()
+    torch.cuda.synchronize()
+    ref = [y.clone() for y in outputs]
+    g = capture(torch, stream, run)
+    ok = True
+    for _ in range(3):
+        for y in outputs:
+            y.fill_(float("nan"))
+        g.replay()
+        torch.cuda.synchronize()
+        ok = ok and all(torch.equal(a.view(torch.int32), b.view(torch.int32)) for a, b in zip(outputs, ref))
+        run()
+        torch.cuda.synchronize()
+    info = {"replays_checked": 3, "bitwise_equal_to_eager": bool(ok)}
+    if not ok:
+        return run, dict(info, launch="eager")
+    for _ in range(warmup):
+        g.replay()
+        run()
+    gm, _ = time_steps(torch, stream, g.replay, 3)
+    em, _ = time_steps(torch, stream, run, 3)
+    info["calibration_ms"] = {"graph": round(gm, 4), "eager": round(em, 4)}
+    if gm <= em:
+        return g.replay, dict(info, launch="hip graph replay", graph=g)
+    return run, dict(info, launch="eager", graph=g)
+
+
+def launch_floor(q4, torch, stream, blobs, steps, warmup):
+    """q4nx_stream_read over each decode launch's weight bytes, one launch per
+    GEMV launch (the faster of graph and eager): the time a plain streaming
+    kernel needs for the same bytes in the same launch structure."""
+    sink = torch.empty(8192, dtype=torch.float32, device="cuda")
+    fl = Step(q4, stream.cuda_stream)
+    for b in blobs:
+        fl.calls.append((q4.lib.q4nx_stream_read, (b.data_ptr(), b.numel(), sink.data_ptr(), fl.s)))
+    g = capture(torch, stream, fl.run)
+    fn = g.replay if time_steps(torch, stream, g.replay, 3)[0] < time_steps(torch, stream, fl.run, 3)[0] else fl.run
+    for _ in range(warmup):
+        fn()
+    ms, _ = time_steps(torch, stream, fn, steps)
+    nbytes = sum(b.numel() for b in blobs)
+    return {"what": "q4nx_stream_read (a plain streaming read with the GEMV's load pattern) over each decode "
+                    "launch's weight bytes, one launch per GEMV launch, graph or eager (the faster)",
+            "launches": len(blobs), "ms_median": round(ms, 4), "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1)}
+
+
+def run_4b(args, q4, torch, stream):
+    """The Gemma3-4B workloads beside the default 27B line: the decode step
+    (34 layers + lm_head 262144 x 2560, M = 1) and the prefill chunk (34
+    layers, M = 2048), timed like the 27B steps, each with its roofline
+    fraction, and checked in the same run against the oracle: every output of
+    layers 0 and 33 and 4096 sampled lm_head rows at decode, every element of
+    layer 0's four prefill products and 256 sampled token rows of layer 33's."""
+    import numpy as np
+    import oracle
+    from workloads import MODELS, CONFIGS, gen_weights, gen_activations, gen_activations_device
+    cfg = CONFIGS[2]
+    model = MODELS[cfg["model"]]
+    L = model["layers"]
+    F32 = q4.Q4NX_F32
+    log(f"gemma3-4b: {L} layers, decode step with lm_head and prefill chunk at M = 2048")
+    weights, stacked = build_weights(model, cfg, args.seed, args.offset_mode, q4, torch)
+    out = {}
+    # ---- decode step
+    xs, ys, dec_bytes = {}, {}, 0.0
+    keys = [(l, p) for l in range(L) for p in range(len(model["proj"]))] + [(L, 7)]
+    for (l, p) in keys:
+        _, N, K = model["lm_head"] if p == 7 else model["proj"][p]
+        xs[(l, p)] = torch.from_numpy(gen_activations(K, seed=args.seed, layer=l, proj=p).view("int16")).cuda()
+        ys[(l, p)] = torch.empty(N, dtype=torch.float32, device="cuda")
+        dec_bytes += N * K * WEIGHT_BYTES
+    dec = Step(q4, stream.cuda_stream)
+    for l in range(L):
+        it = lambda p: (weights[(l, p)], xs[(l, p)], ys[(l, p)], model["proj"][p][1], model["proj"][p][2])
+        for g in GROUPS:
+            dec.gemv_batched([it(p) for p in g], F32)
+    _, Nh, Kh = model["lm_head"]
+    dec.gemv_batched([(weights[(L, 7)], xs[(L, 7)], ys[(L, 7)], Nh, Kh)], F32)
+    for _ in range(args.warmup):
+        dec.run()
+    fn, info = faster_launch_mode(torch, stream, dec.run, list(ys.values()), args.warmup)
+    info.pop("graph", None)
+    ms, ms_min = time_steps(torch, stream, fn, args.steps)
+    gbs = dec_bytes / (ms * 1e-3) / 1e9
+    floor = launch_floor(q4, torch, stream, [stacked[(l, gi)] for l in range(L) for gi in range(len(GROUPS))]
+                         + [weights[(L, 7)]], args.steps, args.warmup)
+    floor["decode_ms_median_over_floor"] = round(ms / floor["ms_median"], 4)
+    out["decode"] = {"workload": cfg["name"], "ms_median": round(ms, 4), "ms_min": round(ms_min, 4),
+                     "weight_GB": round(dec_bytes / 1e9, 4), "GB_per_s": round(gbs, 2),
+                     "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "launches": len(dec.calls), "launch": info["launch"],
+                     "graph_check": info, "launch_floor": floor,
+                     "target": "70% of 8 TB/s = 0.433 ms"}
+    log(f"4b decode {ms:.3f} ms ({gbs:.0f} GB/s), floor {floor['ms_median']:.3f} ms")
+    # ---- prefill chunk
+    M = 2048
+    shapes = [(sum(model["proj"][p][1] for p in g), model["proj"][g[0]][2]) for g in GROUPS]
+    Xs = {(l, gi): gen_activations_device((M, K), seed=args.seed, layer=l, proj=GROUPS[gi][0])
+          for l in range(L) for gi, (N, K) in enumerate(shapes)}
+    Ys = [torch.empty((M, N), dtype=torch.float32, device="cuda") for N, _ in shapes]
+    wb = max(q4.q4nx_gemm_workspace_size(q4.Q4NX_WEIGHTS_Q4NX, M, N, K) for N, K in shapes)
+    pre = Step(q4, stream.cuda_stream)
+    pre.work = torch.empty(max(wb // 4, 1), dtype=torch.float32, device="cuda")
+    flops = 0.0
+    for l in range(L):
+        for gi, (N, K) in enumerate(shapes):
+            pre.gemm(M, N, K, Xs[(l, gi)], stacked[(l, gi)], Ys[gi], F32)
+            flops += 2.0 * M * N * K
+    for _ in range(args.warmup):
+        pre.run()
+    pms, pms_min = time_steps(torch, stream, pre.run, args.steps)
+    tf = flops / (pms * 1e-3) / 1e12
+    out["prefill"] = {"workload": CONFIGS[3]["name"], "ms_median": round(pms, 4), "ms_min": round(pms_min, 4),
+                      "M": M, "TFLOP": round(flops / 1e12, 4), "TFLOP_per_s": round(tf, 2),
+                      "frac_mfma": round(tf / BF16_MFMA_PEAK_TFLOPS, 4), "launches": len(pre.calls),
+                      "gemms": ", ".join(f"{N}x{K}" for N, K in shapes), "target": "50% of 2516.6 TFLOP/s = 10.45 ms"}
+    log(f"4b prefill {pms:.3f} ms ({tf:.0f} TFLOP/s)")
+    if args.no_cpu_baseline:
+        return out
+    # ---- parity against the oracle, same run
+    checks = []
+    for l in (0, L - 1):
+        for c in dec.calls[4 * l:4 * l + 4]:
+            c[0](*c[1])
+    dec.calls[-1][0](*dec.calls[-1][1])
+    for gi in range(len(GROUPS)):
+        pre.calls[gi][0](*pre.calls[gi][1])
+    torch.cuda.synchronize()
+    y0 = {k: ys[k].cpu().numpy() for k in ys if k[0] in (0, L - 1, L)}
+    Yl0 = [Y.cpu().numpy() for Y in Ys]
+    rng = np.random.default_rng(args.seed)
+    rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, 254)]))
+    for gi in range(len(GROUPS)):   # last layer's products on sampled rows (run after layer 0's are copied)
+        pre.calls[4 * (L - 1) + gi][0](*pre.calls[4 * (L - 1) + gi][1])
+    torch.cuda.synchronize()
+    idx = torch.tensor(rows, device="cuda")
+    Ylast = [Y.index_select(0, idx).cpu().numpy() for Y in Ys]
+    for l in (0, L - 1):
+        wl = []
+        for p, (_, N, K) in enumerate(model["proj"]):
+            codes, sc, of = gen_weights(N, K, seed=args.seed, layer=l, proj=p, offset_mode=args.offset_mode)
+            w = oracle.dequant_f32(codes, sc, of)
+            x = gen_activations(K, seed=args.seed, layer=l, proj=p)
+            ok, worst = oracle.check_close(y0[(l, p)], oracle.gemv_f64(w, x), oracle.abs_bound(x, w))
+            checks.append(("decode", ok, worst))
+            wl.append(w)
+        for gi, g in enumerate(GROUPS):
+            w = np.concatenate([wl[p] for p in g])
+            X = Xs[(l, gi)].view(torch.int16).cpu().numpy().view("uint16")
+            if l == 0:
+                ok, worst = oracle.check_close(Yl0[gi], oracle.gemm_f64(X, w), oracle.abs_bound(X, w))
+            else:
+                ok, worst = oracle.check_close(Ylast[gi], oracle.gemm_f64(X[rows], w), oracle.abs_bound(X[rows], w))
+            checks.append(("prefill", ok, worst))
+        log(f"4b oracle check: layer {l} done")
+        del wl
+    codes, sc, of = gen_weights(Nh, Kh, seed=args.seed, layer=L, proj=7, offset_mode=args.offset_mode)
+    hr = np.unique(np.concatenate([[0, Nh - 1], rng.integers(0, Nh, 4094)]))
+    w = oracle.dequant_f32(codes[hr], sc[hr], of[hr])
+    x = gen_activations(Kh, seed=args.seed, layer=L, proj=7)
+    ok, worst = oracle.check_close(y0[(L, 7)][hr], oracle.gemv_f64(w, x), oracle.abs_bound(x, w))
+    checks.append(("decode", ok, worst))
+    out["parity_check"] = {
+        "tolerance": "|y - y_ref| <= 2e-3 * sum_k |x_k w_k| + 1e-5 per output, float64 oracle",
+        "decode": f"every output of layers 0 and {L - 1} (7 projections each) and {len(hr)} sampled lm_head rows",
+        "prefill": f"every element of layer 0's 4 products, {len(rows)} sampled token rows of layer {L - 1}'s",
+        "decode_worst_err_over_tol": float(f"{max(c[2] for c in checks if c[0] == 'decode'):.3g}"),
+        "prefill_worst_err_over_tol": float(f"{max(c[2] for c in checks if c[0] == 'prefill'):.3g}"),
+        "ok": all(c[1] for c in checks)}
+    del weights, stacked, Xs, Ys, pre, dec
+    torch.cuda.empty_cache()
+    return out
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -219,13 +424,10 @@ def blas_thread_count():
         return 1
 
 
-def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefill, gpu=None):
+def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefill):
     """The oracle, untuned, on a bounded sample: `layers` layer(s) of the
-    workload's projections, timed on this host's cores.  With `gpu` (outputs
-    the timed GPU steps produced), the same oracle results also check them:
-    layer 0's decode outputs in full, and sampled rows of the last layer's
-    prefill products (untimed)."""
-    import numpy as np
+    workload's projections, timed on this host's cores (16 token rows of the
+    prefill chunk)."""
     import oracle
     from workloads import gen_weights, gen_activations
     blas_threads = blas_thread_count()
@@ -233,7 +435,6 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
     pre_t = pre_flops = 0.0
     deq_total = mv_total = mm_total = 0.0   # the oracle's dequant, mat-vec and matmul separately
     rows = 16
-    checks = []
     first = {p: g[0] for g in GROUPS for p in g}   # projections of a group share the prefill input
     for l in range(layers):
         for p, (_, N, K) in enumerate(model["proj"]):
@@ -247,14 +448,11 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
             deq_total += t_deq
             if do_decode:
                 t0 = time.perf_counter()
-                y_ref = oracle.gemv_f64(w, x)
+                oracle.gemv_f64(w, x)
                 t_mv = time.perf_counter() - t0
                 mv_total += t_mv
                 dec_t += t_deq + t_mv
                 dec_bytes += N * K * WEIGHT_BYTES
-                if gpu and l == 0 and p in gpu.get("decode", {}):
-                    ok, worst = oracle.check_close(gpu["decode"][p], y_ref, oracle.abs_bound(x, w))
-                    checks.append(("decode", p, N, ok, worst))
             if do_prefill:
                 t0 = time.perf_counter()
                 oracle.gemm_f64(X, w)
@@ -263,19 +461,6 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
                 pre_t += t_deq + t_mm
                 pre_flops += 2.0 * rows * N * K
             log(f"oracle sample: layer {l} projection {p} ({N}x{K}) done")
-    if gpu and "prefill" in gpu:
-        # The last layer's stacked products on the GPU's own input rows.
-        lp = gpu["prefill_layer"]
-        for gi, (Xr, Yr) in gpu["prefill"].items():
-            ws = []
-            for p in GROUPS[gi]:
-                _, N, K = model["proj"][p]
-                codes, s, o = gen_weights(N, K, seed=seed, layer=lp, proj=p, offset_mode=mode)
-                ws.append(oracle.dequant_f32(codes, s, o))
-            w = np.concatenate(ws)
-            ok, worst = oracle.check_close(Yr, oracle.gemm_f64(Xr, w), oracle.abs_bound(Xr, w))
-            checks.append(("prefill", gi, w.shape[0], ok, worst))
-            log(f"oracle check: layer {lp} product {gi} ({w.shape[0]}x{w.shape[1]}) done")
     out = {"cores": int(blas_threads), "kind": "oracle", "cpu_model": cpu_model(),
            "affinity_cpus": len(os.sched_getaffinity(0)),
            "seconds_split": {"dequant": round(deq_total, 4), "matvec": round(mv_total, 4),
@@ -293,19 +478,61 @@ def cpu_baseline(model, cfg, seed, mode, layers, do_decode, do_prefill, M_prefil
             out["prefill"] = pf
         else:
             out.update(value=pf["value"], unit=pf["unit"], sample=pf["sample"], seconds=pre_t)
-    if checks:
-        pc = {"tolerance": "|y - y_ref| <= 2e-3 * sum_k |x_k w_k| + 1e-5 per output, float64 oracle"}
-        for kind, what in (("decode", "layer 0, every output of its {} projections"),
-                           ("prefill", "layer {}, {} token rows of each of its {} stacked products")):
-            cs = [c for c in checks if c[0] == kind]
-            if not cs:
-                continue
-            pc[kind] = (what.format(len(cs)) if kind == "decode"
-                        else what.format(gpu["prefill_layer"], gpu["prefill_rows"], len(cs)))
-            pc[f"{kind}_worst_err_over_tol"] = float(f"{max(c[4] for c in cs):.3g}")
-        pc["ok"] = all(c[3] for c in checks)
-        out["parity_check"] = pc
     return out
+
+
+def parity_check(model, seed, mode, gpu):
+    """The timed steps' outputs against the oracle (untimed): at decode every
+    output of the layers in gpu["decode"]; at prefill every element of the
+    product in gpu["prefill_full"] and the sampled token rows of the last
+    layer's products in gpu["prefill"]."""
+    import numpy as np
+    import oracle
+    from workloads import gen_weights, gen_activations
+    checks = []
+    layers = sorted(set([l for l, _ in gpu.get("decode", {})] + ([gpu["prefill_layer"]] if "prefill" in gpu else [])
+                        + ([gpu["prefill_full"][0]] if "prefill_full" in gpu else [])))
+    for l in layers:
+        ws = {}
+        for p, (_, N, K) in enumerate(model["proj"]):
+            codes, sc, of = gen_weights(N, K, seed=seed, layer=l, proj=p, offset_mode=mode)
+            ws[p] = oracle.dequant_f32(codes, sc, of)
+            if (l, p) in gpu.get("decode", {}):
+                x = gen_activations(K, seed=seed, layer=l, proj=p)
+                ok, worst = oracle.check_close(gpu["decode"][(l, p)], oracle.gemv_f64(ws[p], x),
+                                               oracle.abs_bound(x, ws[p]))
+                checks.append(("decode", ok, worst))
+        if "prefill_full" in gpu and gpu["prefill_full"][0] == l:
+            _, gi, X, Y = gpu["prefill_full"]
+            w = np.concatenate([ws[p] for p in GROUPS[gi]])
+            ok, worst = oracle.check_close(Y, oracle.gemm_f64(X, w), oracle.abs_bound(X, w))
+            checks.append(("prefill", ok, worst))
+        if "prefill" in gpu and gpu["prefill_layer"] == l:
+            for gi, (Xr, Yr) in gpu["prefill"].items():
+                w = np.concatenate([ws[p] for p in GROUPS[gi]])
+                ok, worst = oracle.check_close(Yr, oracle.gemm_f64(Xr, w), oracle.abs_bound(Xr, w))
+                checks.append(("prefill", ok, worst))
+        log(f"oracle check: layer {l} done")
+        del ws
+    pc = {"tolerance": "|y - y_ref| <= 2e-3 * sum_k |x_k w_k| + 1e-5 per output, float64 oracle"}
+    if "decode" in gpu:
+        dl = sorted(set(l for l, _ in gpu["decode"]))
+        pc["decode"] = f"every output of layers {dl} ({len(gpu['decode'])} projections)"
+    if "prefill_full" in gpu or "prefill" in gpu:
+        parts = []
+        if "prefill_full" in gpu:
+            l, gi, X, _ = gpu["prefill_full"]
+            parts.append(f"every element of layer {l}'s product {gi} ({X.shape[0]} x {gpu['prefill_full'][3].shape[1]})")
+        if "prefill" in gpu:
+            parts.append(f"{gpu['prefill_rows']} sampled token rows of each of layer {gpu['prefill_layer']}'s "
+                         f"{len(gpu['prefill'])} stacked products")
+        pc["prefill"] = "; ".join(parts)
+    for kind in ("decode", "prefill"):
+        cs = [c for c in checks if c[0] == kind]
+        if cs:
+            pc[f"{kind}_worst_err_over_tol"] = float(f"{max(c[2] for c in cs):.3g}")
+    pc["ok"] = all(c[1] for c in checks)
+    return pc
 
 
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2602_06063_amd", "csrc", "q4nx_kernels.hip")
@@ -387,16 +614,20 @@ def trace_summary(trace_dir, bench_json):
         tflop = r["prefill"]["TFLOP"]
         lines.append(f"Prefill kernels ({', '.join('`' + f + '`' for f in fam)}): {gemm_c} launches, "
                      f"{gemm_t:.1f} ms over the {runs} runs of the prefill step (warm-up + timed) = {per:.2f} ms "
-                     f"per step; the benchmark's HIP-event time of the step: {r['prefill']['ms']:.2f} ms.")
+                     f"per step; the benchmark's HIP-event time of the step (median): {r['prefill']['ms_median']:.2f} ms.")
         lines.append(f"Achieved: {tflop:.2f} TFLOP per step / {per:.2f} ms = {tflop / per * 1e3:.0f} TFLOP/s "
                      f"(benchmark: {r['prefill']['TFLOP_per_s']:.0f} TFLOP/s, "
                      f"{100 * r['prefill']['frac_mfma']:.1f}% of {BF16_MFMA_PEAK_TFLOPS} TFLOP/s dense bf16).")
-    gv = [(n, c, t) for n, c, t in kern if "gemv_kernel" in n.split("(")[0] and n.split("(")[0].rstrip().endswith("1>")]
+    # Q4NX GEMV launches: gemv_kernel and gemv_stream_kernel with the Q4NX
+    # format (last template argument 1; 2 is the MXFP4 variant).
+    gv = [(n, c, t) for n, c, t in kern if re.search(r"gemv(_stream)?_kernel<", n.split("(")[0])
+          and n.split("(")[0].rstrip().endswith("1>")]
     if gv and "decode" in r:
         c = sum(k[1] for k in gv)
         t = sum(k[2] for k in gv)
-        lines.append(f"Q4NX GEMV (`gemv_kernel<.., .., 1>`): {c} launches, average {1e3 * t / c:.1f} us; decode step "
-                     f"({r['decode']['launch']}): {r['decode']['ms']:.3f} ms for {r['decode']['weight_GB']:.3f} GB "
+        lines.append(f"Q4NX GEMV (`gemv_kernel`, `gemv_stream_kernel`): {c} launches, average {1e3 * t / c:.1f} us; "
+                     f"decode step ({r['decode']['launch']}, median): {r['decode']['ms_median']:.3f} ms for "
+                     f"{r['decode']['weight_GB']:.3f} GB "
                      f"= {r['decode']['GB_per_s']:.0f} GB/s ({100 * r['decode']['frac_hbm']:.1f}% of 8 TB/s).")
     return "\n".join(lines) + "\n"
 
@@ -866,16 +1097,36 @@ def main():
     dec_ms, pre_ms, wall = timed(decode_fn, pre.run, args.steps)
     step_ms = [d + p for d, p in zip(dec_ms, pre_ms)]
     mean = lambda v: sum(v) / len(v)
+    med = lambda v: sorted(v)[len(v) // 2]
     log(f"timed {args.steps} steps in {wall:.2f}s wall; decode {mean(dec_ms):.3f} ms, prefill {mean(pre_ms):.3f} ms")
     other_dec_ms = None   # the launch mode not used in the timed steps
     if do_decode and graph_info and "calibration_ms" in graph_info:
         other = dec.run if use_graph else graphs[0].replay
         other_dec_ms, _, _ = timed(other, lambda: None, args.steps)
     two_ms = None
+    gemm_only_ms = None
     if do_prefill and args.two_phase:
         for _ in range(args.warmup):
             two.run()
         _, two_ms, _ = timed(lambda: None, two.run, args.steps)
+        # The bf16 GEMM launches alone: an event pair around every
+        # q4nx_gemm_bf16 call of the two-phase step (the dequantization
+        # passes run between them, outside the pairs).
+        per_step = []
+        for _ in range(args.steps):
+            pairs = []
+            for fn, a in two.calls:
+                if fn is q4.lib.q4nx_gemm_ex:
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    fn(*a)
+                    e1.record(stream)
+                    pairs.append((e0, e1))
+                else:
+                    fn(*a)
+            torch.cuda.synchronize()
+            per_step.append(sum(x.elapsed_time(y) for x, y in pairs))
+        gemm_only_ms = sorted(per_step)[len(per_step) // 2]
     fus_ms = None
     if do_prefill and args.fused:
         for _ in range(args.warmup):
@@ -908,12 +1159,12 @@ def main():
             mdec_ms, _, _ = timed(mdec_fn, lambda: None, args.steps)
             if minfo and minfo["graph_usable"]:   # keep the faster launch mode, as for the Q4NX step
                 eager_ms, _, _ = timed(mdec.run, lambda: None, args.steps)
-                minfo.update(graph_ms=round(mean(mdec_ms), 4), eager_ms=round(mean(eager_ms), 4))
-                if mean(eager_ms) < mean(mdec_ms):
+                minfo.update(graph_ms=round(med(mdec_ms), 4), eager_ms=round(med(eager_ms), 4))
+                if med(eager_ms) < med(mdec_ms):
                     mdec_ms = eager_ms
             mbytes = dec_bytes / WEIGHT_BYTES * MX_WEIGHT_BYTES
-            t = mean(mdec_ms)
-            mx["decode"] = {"ms": round(t, 4), "ms_min": round(min(mdec_ms), 4), "weight_GB": round(mbytes / 1e9, 4),
+            t = med(mdec_ms)
+            mx["decode"] = {"ms_median": round(t, 4), "ms_min": round(min(mdec_ms), 4), "weight_GB": round(mbytes / 1e9, 4),
                             "GB_per_s": round(mbytes / (t * 1e-3) / 1e9, 2),
                             "frac_hbm": round(mbytes / (t * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                             "launches": len(mdec.calls), "graph_check": minfo,
@@ -922,8 +1173,8 @@ def main():
             for _ in range(args.warmup):
                 mpre.run()
             _, mpre_ms, _ = timed(lambda: None, mpre.run, args.steps)
-            t = mean(mpre_ms)
-            mx["prefill"] = {"ms": round(t, 4), "ms_min": round(min(mpre_ms), 4), "M": M_pre,
+            t = med(mpre_ms)
+            mx["prefill"] = {"ms_median": round(t, 4), "ms_min": round(min(mpre_ms), 4), "M": M_pre,
                              "TFLOP_per_s": round(pre_flops / (t * 1e-3) / 1e12, 2),
                              "frac_mfma": round(pre_flops / (t * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
                              "launches": len(mpre.calls)}
@@ -943,9 +1194,9 @@ def main():
         for _ in range(args.warmup):
             sq.run()
         _, q_ms, _ = timed(lambda: None, sq.run, args.steps)
-        tq = mean(q_ms)
+        tq = med(q_ms)
         qbytes = Nq * Kq * (4 + WEIGHT_BYTES)
-        quant = {"shape": [Nq, Kq], "ms": round(tq, 4), "ms_min": round(min(q_ms), 4),
+        quant = {"shape": [Nq, Kq], "ms_median": round(tq, 4), "ms_min": round(min(q_ms), 4),
                  "Gweights_per_s": round(Nq * Kq / (tq * 1e-3) / 1e9, 2),
                  "GB_per_s": round(qbytes / (tq * 1e-3) / 1e9, 2),
                  "frac_hbm": round(qbytes / (tq * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
@@ -957,9 +1208,9 @@ def main():
         for _ in range(args.warmup):
             sm.run()
         _, m_ms, _ = timed(lambda: None, sm.run, args.steps)
-        tm = mean(m_ms)
+        tm = med(m_ms)
         mbytes = Nq * Kq * (4 + MX_WEIGHT_BYTES)
-        quant["mxfp4"] = {"ms": round(tm, 4), "Gweights_per_s": round(Nq * Kq / (tm * 1e-3) / 1e9, 2),
+        quant["mxfp4"] = {"ms_median": round(tm, 4), "Gweights_per_s": round(Nq * Kq / (tm * 1e-3) / 1e9, 2),
                           "GB_per_s": round(mbytes / (tm * 1e-3) / 1e9, 2),
                           "frac_hbm": round(mbytes / (tm * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                           "bytes": "4 B read + 0.53125 B written per weight"}
@@ -995,17 +1246,17 @@ def main():
         for _ in range(args.warmup):
             sk.run()
         _, k_ms, _ = timed(lambda: None, sk.run, args.steps)
-        tk = mean(k_ms)
+        tk = med(k_ms)
         fkv = {"context": T, "layers": L, "global_layers": sum(is_global_layer(l) for l in range(L)),
                "window": SWA_WINDOW, "heads": H, "kv_groups": G, "head_dim": d,
-               "ms": round(tk, 4), "ms_min": round(min(k_ms), 4), "kv_GB": round(kv_bytes / 1e9, 4),
+               "ms_median": round(tk, 4), "ms_min": round(min(k_ms), 4), "kv_GB": round(kv_bytes / 1e9, 4),
                "GB_per_s": round(kv_bytes / (tk * 1e-3) / 1e9, 2),
                "frac_hbm": round(kv_bytes / (tk * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                "launches": 2 * L, "bytes": "K and V rows of the attended positions, bf16"}
         del bufs, work
 
-    dec_gbs = dec_bytes / (mean(dec_ms) * 1e-3) / 1e9 if do_decode else None
-    pre_tflops = pre_flops / (mean(pre_ms) * 1e-3) / 1e12 if do_prefill else None
+    dec_gbs = dec_bytes / (med(dec_ms) * 1e-3) / 1e9 if do_decode else None
+    pre_tflops = pre_flops / (med(pre_ms) * 1e-3) / 1e12 if do_prefill else None
 
     result = {
         "metric": "Q4NX dequant-GEMV weight GB/s (% HBM peak); dequant-GEMM TFLOP/s (% MFMA)",
@@ -1014,11 +1265,11 @@ def main():
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": round(mean(step_ms), 4),
+        "ms_per_step": round(med(step_ms), 4),
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if do_decode else "bf16",
+        "dtype": "bf16",
         "data": "synthetic",
         "config": {
             "workload": cfg["name"],
@@ -1030,8 +1281,8 @@ def main():
         },
     }
     if do_decode:
-        result["decode"] = {"ms": round(mean(dec_ms), 4), "ms_min": round(min(dec_ms), 4),
-                            "ms_median": round(sorted(dec_ms)[len(dec_ms) // 2], 4),
+        result["decode"] = {"ms_median": round(med(dec_ms), 4), "ms_min": round(min(dec_ms), 4),
+                            "ms_mean": round(mean(dec_ms), 4),
                             "weight_GB": round(dec_bytes / 1e9, 4), "GB_per_s": round(dec_gbs, 2),
                             "frac_hbm": round(dec_gbs / HBM_PEAK_GBS, 4), "launches": dec_launches,
                             "launch": "hip graph replay" if use_graph else "eager",
@@ -1039,20 +1290,20 @@ def main():
                             "dtype": "exact bf16 codes times bf16 x (v_dot2), float32 accumulation"}
         if other_dec_ms:
             key = "eager" if use_graph else "graph"
-            result["decode"][f"{key}_ms"] = round(mean(other_dec_ms), 4)
-            result["decode"][f"{key}_GB_per_s"] = round(dec_bytes / (mean(other_dec_ms) * 1e-3) / 1e9, 2)
+            result["decode"][f"{key}_ms_median"] = round(med(other_dec_ms), 4)
+            result["decode"][f"{key}_GB_per_s"] = round(dec_bytes / (med(other_dec_ms) * 1e-3) / 1e9, 2)
     if do_prefill:
-        result["prefill"] = {"ms": round(mean(pre_ms), 4), "ms_min": round(min(pre_ms), 4),
-                             "ms_median": round(sorted(pre_ms)[len(pre_ms) // 2], 4), "M": M_pre,
+        result["prefill"] = {"ms_median": round(med(pre_ms), 4), "ms_min": round(min(pre_ms), 4),
+                             "ms_mean": round(mean(pre_ms), 4), "M": M_pre,
                              "TFLOP": round(pre_flops / 1e12, 4), "TFLOP_per_s": round(pre_tflops, 2),
                              "frac_mfma": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4),
                              "launches": len(pre.calls), "dtype": "bf16 MFMA, f32 accumulate",
                              "gemms": "per layer: q/k/v stacked, o, gate/up stacked, down ("
                                       + ", ".join(f"{N}x{K}" for N, K in shapes) + ")"}
         if two_ms:
-            t = mean(two_ms)
+            t = med(two_ms)
             result["prefill"]["two_phase"] = {
-                "ms": round(t, 4), "ms_min": round(min(two_ms), 4),
+                "ms_median": round(t, 4), "ms_min": round(min(two_ms), 4),
                 "TFLOP_per_s": round(pre_flops / (t * 1e-3) / 1e12, 2),
                 "launches": len(two.calls),
                 "what": "per GEMM: q4nx_dequant to a bf16 W buffer, then q4nx_gemm_bf16 (same bits as q4nx_gemm)"}
@@ -1076,10 +1327,19 @@ def main():
             result["value_gemm"] = round(pre_tflops, 2)
     # Dominant kernel by time: the GEMM when the step has a prefill chunk.
     if do_prefill:
-        result["roofline"] = {"kernel": "q4nx_gemm_ex launches (gemm256_kernel, gemm_kernel, splitk_sum_kernel, dequant_kernel)", "bound": "mfma", "achieved": round(pre_tflops, 2),
-                              "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+        result["roofline"] = {"kernel": "the prefill step's q4nx_gemm_ex launches (gemm256_kernel, gemm_kernel, "
+                                        "splitk_sum_kernel, dequant_kernel)", "bound": "mfma",
+                              "achieved": round(pre_tflops, 2), "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                               "frac": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
                               "algorithmic_bytes": round(alg_pre)}
+        if gemm_only_ms:
+            t = gemm_only_ms
+            result["roofline"]["dominant_kernel"] = {
+                "what": "the same products' bf16 MFMA launches alone (gemm256_kernel, gemm_kernel and the split-K "
+                        "sum, the dequantization pass excluded): HIP events around every q4nx_gemm_bf16 call of "
+                        "the two-phase step, summed per step, median over the steps",
+                "ms_median": round(t, 4), "achieved": round(pre_flops / (t * 1e-3) / 1e12, 2),
+                "frac": round(pre_flops / (t * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4)}
     if do_decode:
         r = {"kernel": "gemv_kernel", "bound": "hbm", "achieved": round(dec_gbs, 2), "peak": HBM_PEAK_GBS,
              "unit": "GB/s", "frac": round(dec_gbs / HBM_PEAK_GBS, 4), "traffic": None,
@@ -1092,7 +1352,7 @@ def main():
         # Read bandwidth a plain streaming kernel reaches on this device (the
         # library's measurement aid, the GEMV's load pattern over 4 GiB).
         src = torch.empty(1 << 32, dtype=torch.uint8, device="cuda")
-        sink = torch.empty(2048, dtype=torch.float32, device="cuda")
+        sink = torch.empty(8192, dtype=torch.float32, device="cuda")
         sr = Step(q4, stream.cuda_stream)
         sr.calls.append((q4.lib.q4nx_stream_read, (src.data_ptr(), src.numel(), sink.data_ptr(), sr.s)))
         for _ in range(args.warmup):
@@ -1106,32 +1366,12 @@ def main():
         # decode step's launch structure: one dependent launch per GEMV launch,
         # over the very blobs that launch reads.  Each launch pays its ramp and
         # drain, so this is the ceiling for a step of that many launches.
-        fl = Step(q4, stream.cuda_stream)
         blobs = [stacked[(l, gi)] for l in range(L) for gi in range(len(GROUPS))]
         if cfg.get("lm_head"):
             blobs.append(weights[(L, 7)])
-        for b in blobs:
-            fl.calls.append((q4.lib.q4nx_stream_read, (b.data_ptr(), b.numel(), sink.data_ptr(), fl.s)))
-        fl_fn = fl.run
-        fl.run()
-        torch.cuda.synchronize()
-        fg = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(fg, stream=stream):
-            fl.run()
-        graphs.append(fg)
-        if quick_ms(fg.replay) < quick_ms(fl.run):
-            fl_fn = fg.replay
-        for _ in range(args.warmup):
-            fl_fn()
-        fl_ms, _, _ = timed(fl_fn, lambda: None, args.steps)
-        fl_t = sorted(fl_ms)[len(fl_ms) // 2]
-        dec_t = sorted(dec_ms)[len(dec_ms) // 2]
-        result[rkey]["launch_floor"] = {
-            "what": "q4nx_stream_read over each decode launch's weight blob, one launch per GEMV launch, "
-                    "same launch mode choice (graph or eager, the faster)",
-            "launches": len(fl.calls), "ms_median": round(fl_t, 4),
-            "GB_per_s": round(sum(b.numel() for b in blobs) / (fl_t * 1e-3) / 1e9, 1),
-            "decode_ms_median_over_floor": round(dec_t / fl_t, 4)}
+        floor = launch_floor(q4, torch, stream, blobs, args.steps, args.warmup)
+        floor["decode_ms_median_over_floor"] = round(med(dec_ms) / floor["ms_median"], 4)
+        result[rkey]["launch_floor"] = floor
         del sink
     if quant:
         result["quantize"] = quant
@@ -1148,30 +1388,56 @@ def main():
             if "mfma_busy_fraction" in e:
                 result[key]["mfma_busy_counter"] = round(e["mfma_busy_fraction"], 4)
 
+    parity_ok = True
     if not args.no_cpu_baseline:
-        # Outputs of the timed GPU steps for the oracle to check: layer 0's
-        # decode outputs (their own buffers), and the last layer's prefill
-        # products, run once more because later steps reuse the output buffers.
+        # Outputs of the timed GPU steps for the oracle to check, each launch
+        # run once more because later steps reuse the output buffers: every
+        # decode output of the first and last layers, every element of the
+        # first layer's o product, and sampled rows of the last layer's
+        # prefill products.
+        import numpy as np
         gpu = {}
         if do_decode:
-            for fn, a in dec.calls[:len(GROUPS)]:   # layer 0's launches (the MXFP4 step reuses ys)
-                fn(*a)
+            for l in (0, L - 1):
+                for fn, a in dec.calls[len(GROUPS) * l:len(GROUPS) * (l + 1)]:
+                    fn(*a)
             torch.cuda.synchronize()
-            gpu["decode"] = {p: ys[(0, p)].cpu().numpy() for p in range(len(model["proj"]))}
+            gpu["decode"] = {(l, p): ys[(l, p)].cpu().numpy() for l in (0, L - 1) for p in range(len(model["proj"]))}
         if do_prefill:
+            fn, a = pre.calls[1]                  # layer 0, the o product (group 1)
+            fn(*a)
+            torch.cuda.synchronize()
+            gpu["prefill_full"] = (0, 1, Xs[(0, 1)].view(torch.int16).cpu().numpy().view("uint16"),
+                                   Ys[1].cpu().numpy())
             for fn, a in pre.calls[-len(GROUPS):]:
                 fn(*a)
             torch.cuda.synchronize()
-            rng = __import__("numpy").random.default_rng(args.seed)
-            rows = sorted(set([0, 1, M_pre // 2, M_pre - 1] + rng.integers(0, M_pre, 12).tolist()))
+            rng = np.random.default_rng(args.seed)
+            rows = np.unique(np.concatenate([[0, 1, M_pre // 2, M_pre - 1], rng.integers(0, M_pre, 252)]))
             idx = torch.tensor(rows, device="cuda")
             gpu["prefill_layer"], gpu["prefill_rows"] = L - 1, len(rows)
             gpu["prefill"] = {gi: (Xs[(L - 1, gi)].index_select(0, idx).view(torch.int16).cpu().numpy().view("uint16"),
                                    Ys[gi].index_select(0, idx).cpu().numpy()) for gi in range(len(GROUPS))}
         log("timing the CPU oracle sample")
         result["cpu_baseline"] = cpu_baseline(model, cfg, args.seed, args.offset_mode, args.cpu_layers,
-                                              do_decode, do_prefill, M_pre, gpu)
+                                              do_decode, do_prefill, M_pre)
+        result["cpu_baseline"]["parity_check"] = parity_check(model, args.seed, args.offset_mode, gpu)
+        parity_ok = result["cpu_baseline"]["parity_check"]["ok"]
+    if args.config == 4 and args.with_4b:
+        del weights, stacked
+        if mweights is not None:
+            del mweights, mstacked
+        if do_prefill:
+            del Xs, Ys, gemm_work
+        torch.cuda.empty_cache()
+        result["gemma3_4b"] = run_4b(args, q4, torch, stream)
+        if "parity_check" in result["gemma3_4b"]:
+            parity_ok = parity_ok and result["gemma3_4b"]["parity_check"]["ok"]
+    result["parity_ok"] = bool(parity_ok)
     print(json.dumps(result), flush=True)
+    if not parity_ok:
+        log("parity check FAILED: the numbers above are not valid")
+        sys.exit(1)
 
 
 if __name__ == "__main__":

@@ -33,8 +33,8 @@ def _write_csv(path, fields, rows):
 
 def _bench_json(path, **extra):
     r = {"warmup": 2, "steps": 5,
-         "prefill": {"TFLOP": 209.7, "ms": 180.0, "TFLOP_per_s": 1165.0, "frac_mfma": 0.463},
-         "decode": {"launch": "eager", "ms": 3.6, "weight_GB": 16.0, "GB_per_s": 4444.0, "frac_hbm": 0.555}}
+         "prefill": {"TFLOP": 209.7, "ms_median": 180.0, "TFLOP_per_s": 1165.0, "frac_mfma": 0.463},
+         "decode": {"launch": "eager", "ms_median": 3.6, "weight_GB": 16.0, "GB_per_s": 4444.0, "frac_hbm": 0.555}}
     for k, v in extra.items():
         r["prefill"][k] = v
     with open(path, "w") as f:
@@ -50,13 +50,14 @@ def test_trace_summary_per_step_prefill_time(tmp_path):
         {"Name": "void q4nx::dequant_kernel<1>(unsigned char const*)", "Calls": 28, "TotalDurationNs": 63e6},
         {"Name": "void q4nx::gemv_kernel<4, 1, 1>(q4nx::GemvArgs)", "Calls": 1736, "TotalDurationNs": 24.304e6},
         {"Name": "void q4nx::gemv_kernel<4, 1, 2>(q4nx::GemvArgs)", "Calls": 100, "TotalDurationNs": 5e6},
+        {"Name": "void q4nx::gemv_stream_kernel<4, 1, 1>(q4nx::GemvArgs)", "Calls": 264, "TotalDurationNs": 3.696e6},
     ])
     js = tmp_path / "b.json"
     _bench_json(str(js))
     md = bench.trace_summary(str(tmp_path / "trace"), str(js))
     assert "770.0 ms over the 7 runs" in md and "110.00 ms per step" in md
     assert "= 1906 TFLOP/s" in md                        # 209.7 TFLOP / 110 ms
-    assert "1736 launches, average 14.0 us" in md        # the Q4NX GEMV only, not the MXFP4 one
+    assert "2000 launches, average 14.0 us" in md        # the Q4NX GEMVs (both kernels), not the MXFP4 one
     _bench_json(str(js), bf16_outputs={"ms_median": 1.0})
     with pytest.raises(SystemExit):
         bench.trace_summary(str(tmp_path / "trace"), str(js))
