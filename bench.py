@@ -65,7 +65,7 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--offset-mode", default="zp", choices=["zp", "literal"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-layers", type=int, default=1, help="layers of the oracle CPU sample")
+    ap.add_argument("--cpu-layers", type=int, default=6, help="layers of the oracle CPU sample")
     ap.add_argument("--decode-graph", type=int, default=1, help="replay the decode step as a HIP graph")
     ap.add_argument("--two-phase", type=int, default=1,
                     help="also time the two-phase prefill (q4nx_dequant to bf16, then q4nx_gemm_bf16)")
@@ -325,6 +325,12 @@ def run_4b(args, q4, torch, stream):
                      "frac_hbm": round(gbs / HBM_PEAK_GBS, 4), "launches": len(dec.calls), "launch": info["launch"],
                      "graph_check": info, "launch_floor": floor,
                      "target": "70% of 8 TB/s = 0.433 ms"}
+    st = stored_traffic(2)
+    if st and "gemv" in st["families"]:
+        out["decode"]["traffic"] = round(st["families"]["gemv"]["hbm_bytes_per_step"])
+        out["decode"]["traffic_note"] = ("HBM bytes per step of the GEMV launches from rocprofv3 FETCH_SIZE/WRITE_SIZE "
+                                         "scaled by a copy-kernel calibration: "
+                                         + os.path.relpath(traffic_file(2), ROOT))
     log(f"4b decode {ms:.3f} ms ({gbs:.0f} GB/s), floor {floor['ms_median']:.3f} ms")
     # ---- prefill chunk
     M = 2048
@@ -348,6 +354,14 @@ def run_4b(args, q4, torch, stream):
                       "M": M, "TFLOP": round(flops / 1e12, 4), "TFLOP_per_s": round(tf, 2),
                       "frac_mfma": round(tf / BF16_MFMA_PEAK_TFLOPS, 4), "launches": len(pre.calls),
                       "gemms": ", ".join(f"{N}x{K}" for N, K in shapes), "target": "50% of 2516.6 TFLOP/s = 10.45 ms"}
+    st = stored_traffic(3)
+    if st and "gemm" in st["families"]:
+        e = st["families"]["gemm"]
+        out["prefill"]["traffic"] = round(e["hbm_bytes_per_step"])
+        out["prefill"]["traffic_note"] = ("HBM bytes per step of the GEMM launches from rocprofv3 FETCH_SIZE/WRITE_SIZE "
+                                          "scaled by a copy-kernel calibration: " + os.path.relpath(traffic_file(3), ROOT))
+        if "mfma_busy_fraction" in e:
+            out["prefill"]["mfma_busy_counter"] = round(e["mfma_busy_fraction"], 4)
     log(f"4b prefill {pms:.3f} ms ({tf:.0f} TFLOP/s)")
     if args.no_cpu_baseline:
         return out
@@ -557,8 +571,13 @@ def kernel_source_sha256(text=None):
     return hashlib.sha256(kernel_code_text(text).encode()).hexdigest()
 
 
+# Counter summaries, named for the workload of each configuration.
+WORKLOAD_SLUG = {1: "gemma3-1b_decode-M1", 2: "gemma3-4b_decode-M1", 3: "gemma3-4b_prefill-M2048",
+                 4: "gemma3-27b_decode-M1_prefill-M4096"}
+
+
 def traffic_file(config):
-    return os.path.join(PROFILES, f"hbm-traffic_config{config}.md")
+    return os.path.join(PROFILES, f"hbm-traffic_{WORKLOAD_SLUG.get(config, f'config{config}')}.md")
 
 
 def kernel_family(name):
@@ -567,7 +586,7 @@ def kernel_family(name):
     # only the decode and prefill steps, so no other step launches these).
     if any(k in name for k in ("gemm256_kernel", "gemm_kernel", "splitk_sum_kernel", "dequant_kernel")):
         return "gemm"
-    if "gemv_kernel" in name:
+    if re.search(r"gemv(_stream)?_kernel<", name):
         return "gemv"
     return None
 
@@ -625,10 +644,13 @@ def trace_summary(trace_dir, bench_json):
     if gv and "decode" in r:
         c = sum(k[1] for k in gv)
         t = sum(k[2] for k in gv)
-        lines.append(f"Q4NX GEMV (`gemv_kernel`, `gemv_stream_kernel`): {c} launches, average {1e3 * t / c:.1f} us; "
-                     f"decode step ({r['decode']['launch']}, median): {r['decode']['ms_median']:.3f} ms for "
-                     f"{r['decode']['weight_GB']:.3f} GB "
-                     f"= {r['decode']['GB_per_s']:.0f} GB/s ({100 * r['decode']['frac_hbm']:.1f}% of 8 TB/s).")
+        d = r["decode"]
+        per = 1e3 * t / c * d["launches"] / 1e3
+        lines.append(f"Q4NX GEMV (`gemv_kernel`, `gemv_stream_kernel`): {c} launches, average {1e3 * t / c:.2f} us; "
+                     f"x {d['launches']} launches per decode step = {per:.3f} ms of kernel time per step = "
+                     f"{d['weight_GB'] / per * 1e3:.0f} GB/s ({d['weight_GB'] / per * 1e3 / HBM_PEAK_GBS * 100:.1f}% of "
+                     f"8 TB/s) for {d['weight_GB']:.3f} GB. The benchmark's own step time in this profiled run "
+                     f"({d['launch']}, median): {d['ms_median']:.3f} ms (the tracer adds time between dispatches).")
     return "\n".join(lines) + "\n"
 
 
@@ -721,10 +743,10 @@ def pmc_summary(config, fetch_dir, write_dir, mfma_dir, lds_dir=None):
                 e["wait_lds_issue_fraction"] = v["SQ_WAIT_INST_LDS"] / v["SQ_WAVE_CYCLES"]
                 e["wait_memory_fraction"] = v["SQ_WAIT_ANY"] / v["SQ_WAVE_CYCLES"]
             data["kernels_lds"][kn] = e
-    lines = [f"# HBM traffic, MFMA and VALU busy counters, bench configuration {config}", "",
-             "%s rocprofv3 counter passes over `python3 bench.py --config %d --pmc-pass` (one eager decode "
-             "step, one prefill step, then a 1 GiB device-to-device copy used as the calibration):"
-             % ("Four" if lds_dir else "Three", config), "",
+    lines = [f"# HBM traffic, MFMA and VALU busy counters: {WORKLOAD_SLUG.get(config, config)}", "",
+             "%s rocprofv3 counter passes over `python3 bench.py --config %d --pmc-pass` (one eager step of "
+             "each kind the configuration has, decode and/or prefill, then a 1 GiB device-to-device copy used "
+             "as the calibration):" % ("Four" if lds_dir else "Three", config), "",
              "```", "cd /tmp && export TMPDIR=/tmp && cd /root/repo",
              f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {fetch_dir} -o run -- python3 bench.py --config {config} --pmc-pass",
              f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {write_dir} -o run -- python3 bench.py --config {config} --pmc-pass",

@@ -34,7 +34,7 @@ def _write_csv(path, fields, rows):
 def _bench_json(path, **extra):
     r = {"warmup": 2, "steps": 5,
          "prefill": {"TFLOP": 209.7, "ms_median": 180.0, "TFLOP_per_s": 1165.0, "frac_mfma": 0.463},
-         "decode": {"launch": "eager", "ms_median": 3.6, "weight_GB": 16.0, "GB_per_s": 4444.0, "frac_hbm": 0.555}}
+         "decode": {"launch": "eager", "launches": 248, "ms_median": 3.6, "weight_GB": 16.0, "GB_per_s": 4444.0, "frac_hbm": 0.555}}
     for k, v in extra.items():
         r["prefill"][k] = v
     with open(path, "w") as f:
@@ -57,7 +57,8 @@ def test_trace_summary_per_step_prefill_time(tmp_path):
     md = bench.trace_summary(str(tmp_path / "trace"), str(js))
     assert "770.0 ms over the 7 runs" in md and "110.00 ms per step" in md
     assert "= 1906 TFLOP/s" in md                        # 209.7 TFLOP / 110 ms
-    assert "2000 launches, average 14.0 us" in md        # the Q4NX GEMVs (both kernels), not the MXFP4 one
+    assert "2000 launches, average 14.00 us" in md       # the Q4NX GEMVs (both kernels), not the MXFP4 one
+    assert "= 3.472 ms of kernel time per step" in md    # 14 us x 248 launches
     _bench_json(str(js), bf16_outputs={"ms_median": 1.0})
     with pytest.raises(SystemExit):
         bench.trace_summary(str(tmp_path / "trace"), str(js))
@@ -76,20 +77,23 @@ def _pmc_pass(folder, counter_rows):
 def test_pmc_summary_scaling_and_busy_fractions(tmp_path, monkeypatch):
     gemv, gemm = "void q4nx::gemv_kernel<4, 1, 1>(q4nx::GemvArgs)", "void q4nx::gemm256_kernel<false, 0>(x)"
     copy = "__amd_rocclr_copyBuffer"
+    gvs = "void q4nx::gemv_stream_kernel<2, 3, 1>(q4nx::GemvArgs)"   # counted with the GEMV launches
     f, w, m = (str(tmp_path / n) for n in ("fetch", "write", "mfma"))
     # Calibration copy of 1 GiB each way: FETCH_SIZE reads half (512 MiB in KiB), WRITE_SIZE all of it.
-    _pmc_pass(f, [(gemv, {"FETCH_SIZE": [1000.0, 1000.0]}), (gemm, {"FETCH_SIZE": [3000.0]}),
+    _pmc_pass(f, [(gemv, {"FETCH_SIZE": [1000.0, 500.0]}), (gvs, {"FETCH_SIZE": [500.0]}), (gemm, {"FETCH_SIZE": [3000.0]}),
                   (copy, {"FETCH_SIZE": [262144.0, 262144.0]})])
-    _pmc_pass(w, [(gemv, {"WRITE_SIZE": [4.0]}), (gemm, {"WRITE_SIZE": [500.0]}),
+    _pmc_pass(w, [(gemv, {"WRITE_SIZE": [3.0]}), (gvs, {"WRITE_SIZE": [1.0]}), (gemm, {"WRITE_SIZE": [500.0]}),
                   (copy, {"WRITE_SIZE": [1048576.0]})])
     # 8 XCDs each report GRBM_GUI_ACTIVE = 1000 cycles -> 8000 summed
-    _pmc_pass(m, [(gemv, {"GRBM_GUI_ACTIVE": [1000.0] * 8, "SQ_ACTIVE_INST_VALU": [25600.0]}),
+    _pmc_pass(m, [(gemv, {"GRBM_GUI_ACTIVE": [600.0] * 8, "SQ_ACTIVE_INST_VALU": [15360.0]}),
+                  (gvs, {"GRBM_GUI_ACTIVE": [400.0] * 8, "SQ_ACTIVE_INST_VALU": [10240.0]}),
                   (gemm, {"GRBM_GUI_ACTIVE": [1000.0] * 8, "SQ_VALU_MFMA_BUSY_CYCLES": [512000.0],
                           "SQ_ACTIVE_INST_VALU": [51200.0]}),
                   (copy, {"GRBM_GUI_ACTIVE": [10.0] * 8})])
     lds = str(tmp_path / "lds")
     # gemm: 250 of 1000 LDS cycles in conflicts; 100 and 50 of 1000 wave cycles waiting on LDS issue / memory
     _pmc_pass(lds, [(gemv, {"SQ_WAVE_CYCLES": [500.0], "SQ_WAIT_INST_LDS": [0.0], "SQ_WAIT_ANY": [200.0]}),
+                    (gvs, {"SQ_WAVE_CYCLES": [100.0], "SQ_WAIT_INST_LDS": [0.0], "SQ_WAIT_ANY": [10.0]}),
                     (gemm, {"SQ_LDS_BANK_CONFLICT": [125.0, 125.0], "SQ_LDS_IDX_ACTIVE": [500.0, 500.0],
                             "SQ_WAVE_CYCLES": [1000.0], "SQ_WAIT_INST_LDS": [100.0], "SQ_WAIT_ANY": [50.0]})])
     md = bench.pmc_summary(4, f, w, m, lds)
@@ -99,6 +103,8 @@ def test_pmc_summary_scaling_and_busy_fractions(tmp_path, monkeypatch):
     assert kl["gemm256_kernel"]["wait_lds_issue_fraction"] == pytest.approx(0.1)
     assert kl["gemm256_kernel"]["wait_memory_fraction"] == pytest.approx(0.05)
     assert kl["gemv_kernel"]["wait_memory_fraction"] == pytest.approx(0.4)
+    assert kl["gemv_stream_kernel"]["wait_memory_fraction"] == pytest.approx(0.1)
+    assert data["families"]["gemv"]["dispatches_per_step"] == 2
     assert "| gemm256_kernel | 25.0% | 10.0% | 5.0% |" in md and md.startswith("# HBM") and "Four rocprofv3" in md
     assert "Three rocprofv3" in bench.pmc_summary(4, f, w, m)
     assert data["calibration"]["fetch_scale"] == pytest.approx(2.0)
