@@ -399,10 +399,13 @@ __global__ __launch_bounds__(256) void mx_quantize_kernel(const float* __restric
 // l%8 as
 //     acc += d_g * (sum_{k in g} q_k x_k) + m_g * S_g ,  S_g = sum_{k in g} x_k
 // (Eq. 3 folded into Eq. 15), so the per-weight work is the exact code ->
-// bf16 conversion and one v_dot2 per two weights.  x is staged in LDS as bf16
-// pairs in the order the nibble split produces, with its group sums, a chunk
-// of K at a time; groups are padded to 20 dwords so the eight groups a wave
-// reads at once fall in distinct banks.  At the end a 3-step
+// bf16 conversion and one v_dot2 per two weights.  A wave loads each block's
+// x (512 bytes) together with the block's weights, in the same register slot,
+// and stages it in its own LDS slot as bf16 pairs in the order the nibble
+// split produces, forming the group sums with lane shuffles; groups are
+// padded to 20 dwords so the eight groups a wave reads at once fall in
+// distinct banks.  No wave waits for x beyond its own block, and there is no
+// workgroup-wide staging phase or barrier before the first block.  At the end a 3-step
 // butterfly adds the 8 groups of a row and the W waves' partial sums are added
 // in wave order through LDS.  No workgroup talks to another, so there is no
 // cross-XCD traffic and no device-wide fence.  The summation order is fixed
@@ -412,9 +415,8 @@ __global__ __launch_bounds__(256) void mx_quantize_kernel(const float* __restric
 // For the MXFP4 variant the per-group term is X_g * (sum_{k in g} fp4(q_k) x_k)
 // (no offset), with x staged in natural column order.
 constexpr int kGemvMaxWaves = 16;
-// x is staged up to 88 x 256 columns at a time (at most 61 KiB of LDS with the
-// padding and group sums): every Gemma3 K in one piece, so no workgroup drains
-// its waves to restage x in the middle of a row group.
+// A strip's weights are read 88 blocks at a time through one buffer
+// descriptor (every Gemma3 K in one piece).
 constexpr int kGemvChunkBlocks = 88;
 constexpr int kGroupPadDw = 20;  // dwords per staged group (16 bf16 pairs + 4 pad: conflict-free reads)
 constexpr int kRedFloats = kGemvMaxWaves * 32;
@@ -422,11 +424,6 @@ constexpr int kRedFloats = kGemvMaxWaves * 32;
 constexpr int kGemvDepth4 = 1, kGemvDepth2 = 3, kGemvDepth1 = 4;
 // Workgroups per CU of the streaming form (gemv_stream_kernel), LDS permitting.
 constexpr int kGemvStreamPerCu = 4;
-// 16-byte pieces of x per thread requested before the first weight blocks.
-template <int TQ>
-constexpr int gemv_xpre() {
-  return TQ == 2 ? 2 : 4;
-}
 
 struct GemvJob {
   const uint8_t* blob;
@@ -445,7 +442,7 @@ struct GemvArgs {
   GemvJob job[Q4NX_MAX_BATCH];
   int njobs;
   int y_bf16;
-  int chunk_blocks;  // blocks of x staged at once (sizes the dynamic LDS)
+  int chunk_blocks;  // blocks per chunk: a strip's weights are read through one descriptor per chunk
   int pad;
 };
 
@@ -455,6 +452,7 @@ template <int TQ>
 struct GemvSlot {
   u32x4 q[TQ];
   uint32_t s[TQ], m[TQ];
+  uint32_t xv[2];  // gemv_kernel: this lane's 4 bf16 of x for the block
 };
 
 // Buffer descriptor over one chunk of one strip (at most 88 blocks <= 440 KiB,
@@ -485,17 +483,77 @@ __device__ __forceinline__ void gemv_load(__amdgpu_buffer_rsrc_t rs, int jj, int
   }
 }
 
+// x for one block, per wave: lane l = c + 8r (group c, r = 0..7) reads
+// columns 32c + 4r .. 32c + 4r + 3 of the block (8 bytes; 512 contiguous
+// bytes per wave), in the same ring slot as the block's weights.  The
+// descriptor covers the chunk's columns inside K, so columns past K read 0.
+__device__ __forceinline__ void gemv_load_x(__amdgpu_buffer_rsrc_t xr, int jj, int lane, uint32_t (&xv)[2]) {
+  typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+  const u32x2 v = __builtin_bit_cast(
+      u32x2, __builtin_amdgcn_raw_buffer_load_b64(xr, 2 * (kBlockCols * jj + 32 * (lane & 7) + 4 * (lane >> 3)), 0, 0));
+  xv[0] = v[0];
+  xv[1] = v[1];
+}
+
+// Stages one block's x in the wave's own LDS slot and returns the group sum
+// S_g of this lane's group.  Q4NX: lane c + 8r writes the bf16 pairs of its 4
+// columns, (x0,x2),(x1,x3) for even r, (x4,x6),(x5,x7) for odd r, so that each
+// 8-column run u of a group holds (x0,x2),(x1,x3),(x4,x6),(x5,x7) at dwords
+// 4u..4u+3 (slot of group c at dword c * kGroupPadDw).  S_g is formed in the
+// same order as the workgroup-wide staging: per 8-column run
+// ((x0+x1) + (x2+x3)) + (x4+x5) + (x6+x7), then (run0 + run1) + (run2 + run3).
+// MXFP4 variant: the pairs in natural order, no sum.  The wave reads the slot
+// right after writing it: a wave's LDS instructions are carried out in order,
+// and the fence keeps the compiler from moving the reads above the writes.
+template <int F>
+__device__ __forceinline__ float gemv_stage_x(const uint32_t (&xv)[2], uint32_t* __restrict__ xw, int lane) {
+  typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+  const int c = lane & 7, r = lane >> 3;
+  uint32_t* dst = xw + c * kGroupPadDw + 2 * r;
+  if constexpr (F == kWMX) {
+    *reinterpret_cast<u32x2*>(dst) = (u32x2){xv[0], xv[1]};
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    return 0.0f;
+  }
+  const uint32_t pa = (xv[0] & 0xFFFFu) | (xv[1] << 16);           // (x0,x2) or (x4,x6)
+  const uint32_t pb = (xv[0] >> 16) | (xv[1] & 0xFFFF0000u);       // (x1,x3) or (x5,x7)
+  *reinterpret_cast<u32x2*>(dst) = (u32x2){pa, pb};
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  const float s01 = __uint_as_float(xv[0] << 16) + __uint_as_float(xv[0] & 0xFFFF0000u);
+  const float s23 = __uint_as_float(xv[1] << 16) + __uint_as_float(xv[1] & 0xFFFF0000u);
+  const float o01 = __shfl_xor(s01, 8), o23 = __shfl_xor(s23, 8);  // the odd lane's (x4+x5), (x6+x7)
+  float sm = 0.0f;
+  sm += s01;
+  sm += s23;
+  sm += o01;
+  sm += o23;                       // the run's sum, on the even lanes
+  sm += __shfl_xor(sm, 16);
+  sm += __shfl_xor(sm, 32);
+  const float se = __shfl_xor(sm, 8);
+  return (r & 1) ? se : sm;
+}
+
+// One block's contribution to the lane's row sums: Eq. 15 with Eq. 3 folded
+// in, x from the wave's slot (see gemv_stage_x).  Groups past K (block
+// padding) contribute nothing whatever the padding holds.
 template <int TQ, int F>
 __device__ __forceinline__ void gemv_compute(const GemvSlot<TQ>& R, bool gvalid, const uint32_t* __restrict__ xg,
-                                             float S, float (&acc)[4]) {
+                                               float S, float (&acc)[4]) {
   uint32_t xp[16];
 #pragma unroll
   for (int v = 0; v < 4; ++v) {
     const u32x4 xv = *reinterpret_cast<const u32x4*>(xg + 4 * v);
-    xp[4 * v + 0] = xv[0];
-    xp[4 * v + 1] = xv[1];
-    xp[4 * v + 2] = xv[2];
-    xp[4 * v + 3] = xv[3];
+    if constexpr (F == kWMX) {
+      xp[4 * v + 0] = xv[0];
+      xp[4 * v + 1] = xv[1];
+      xp[4 * v + 2] = xv[2];
+      xp[4 * v + 3] = xv[3];
+    } else {  // slot order (x0,x2),(x1,x3),(x4,x6),(x5,x7) -> the nibble split's order
+      xp[4 * v + 0] = xv[0];
+      xp[4 * v + 1] = xv[2];
+      xp[4 * v + 2] = xv[1];
+      xp[4 * v + 3] = xv[3];
+    }
   }
   if constexpr (F == kWMX) {
 #pragma unroll
@@ -508,7 +566,6 @@ __device__ __forceinline__ void gemv_compute(const GemvSlot<TQ>& R, bool gvalid,
 #pragma unroll
   for (int t = 0; t < TQ; ++t) {
     const float dot = group_dot_bf16(R.q[t], xp);
-    // Groups past K (block padding) contribute nothing whatever the padding holds.
     const float d = gvalid ? bf16_to_f32(R.s[t]) : 0.0f;
     const float m = gvalid ? bf16_to_f32(R.m[t]) : 0.0f;
     acc[t] = fmaf(d, dot, acc[t]);
@@ -519,12 +576,9 @@ __device__ __forceinline__ void gemv_compute(const GemvSlot<TQ>& R, bool gvalid,
 template <int TQ, int D, int F>
 __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs args) {
   constexpr int kBytes = wblock_bytes<F>();
-  // Dynamic LDS: red[16*32] | ssum[chunk*8] | xs[chunk*8*20], chunk = the
-  // launch's largest staged block count (at most kGemvChunkBlocks).
-  extern __shared__ __attribute__((aligned(16))) float lds[];
-  float* red = lds;
-  float* ssum = lds + kRedFloats;
-  uint32_t* xs = reinterpret_cast<uint32_t*>(ssum + args.chunk_blocks * kGroupsPerRow);
+  // red: the waves' row sums; xw: each wave's x slot (one block of x).
+  __shared__ float red[kRedFloats];
+  __shared__ __attribute__((aligned(16))) uint32_t xw_all[kGemvMaxWaves][kGroupsPerRow * kGroupPadDw];
 
   const int wg = blockIdx.x;
   int jb = 0;
@@ -538,11 +592,10 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c = lane & 7;
   const int W = J.waves;
-  const int nthreads = blockDim.x;
   const bool wave_on = w < W;  // wave-uniform
   const int CB = args.chunk_blocks;
   const int nchunks = (J.KB + CB - 1) / CB;
-  int staged = -1;  // chunk currently held in LDS
+  uint32_t* const xw = xw_all[wave_on ? w : 0];
 
   for (int rg = wg - J.wg_begin; rg < J.nrg; rg += J.nwg) {
     const int row0 = rg * 8 * TQ;
@@ -555,72 +608,31 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
       const int nb = min(CB, J.KB - jc0);
       const __amdgpu_buffer_rsrc_t rs = chunk_rsrc(sblob + (size_t)jc0 * kBytes, nb * kBytes);
       const int kvalid = J.K - jc0 * kBlockCols;  // columns of this chunk inside K
-      // The first pieces of this chunk's x are requested before the weight
-      // blocks, so that they are not queued behind them (every workgroup
-      // waits for x before it computes anything).
-      constexpr int kXPre = gemv_xpre<TQ>();
-      u32x4 xpre[kXPre];
-      if (staged != ch) {
-#pragma unroll
-        for (int i = 0; i < kXPre; ++i) {
-          const int e = threadIdx.x + i * nthreads;
-          const int k = jc0 * kBlockCols + 8 * e;
-          xpre[i] = (u32x4){0u, 0u, 0u, 0u};
-          if (e < nb * (kBlockCols / 8) && k < J.K) xpre[i] = *reinterpret_cast<const u32x4*>(J.x + k);
-        }
-      }
-      // The wave's first D blocks go in flight before the x staging.
+      const __amdgpu_buffer_rsrc_t xr = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint16_t*>(J.x + (size_t)jc0 * kBlockCols), (short)0, 2 * min(kvalid, nb * kBlockCols),
+          0x00020000);
+      if (!wave_on) continue;
+      // Ring of D register slots: block w + iW lives in slot i % D and the
+      // slot is refilled with block w + (i + D)W right after it is consumed;
+      // each slot carries the block's x with its weights, so a wave starts
+      // on its first block as soon as that block has arrived.
       GemvSlot<TQ> buf[D];
 #pragma unroll
       for (int d = 0; d < D; ++d)
-        if (wave_on && w + d * W < nb) gemv_load<TQ, F>(rs, w + d * W, t0, lane, buf[d]);
-      if (staged != ch) {
-        __syncthreads();  // every wave is done with the previous chunk
-        // Thread e stages columns 8e..8e+7 as the four bf16 pairs
-        // (x0,x2) (x4,x6) (x1,x3) (x5,x7) and adds them to its group's sum
-        // (MXFP4 variant: the pairs in natural order, no sum).
-        const int kbeg = jc0 * kBlockCols;
-        int it = 0;
-        for (int e = threadIdx.x; e < nb * (kBlockCols / 8); e += nthreads, ++it) {
-          const int k = kbeg + 8 * e;
-          u32x4 v = (u32x4){0u, 0u, 0u, 0u};
-          if (it < kXPre) {
-#pragma unroll
-            for (int i = 0; i < kXPre; ++i)
-              if (i == it) v = xpre[i];
-          } else if (k < J.K) {
-            v = *reinterpret_cast<const u32x4*>(J.x + k);
-          }
-          if constexpr (F == kWMX) {
-            *reinterpret_cast<u32x4*>(xs + (e >> 2) * kGroupPadDw + 4 * (e & 3)) = v;
-            continue;
-          }
-          const uint32_t p02 = (v[0] & 0xFFFFu) | (v[1] << 16), p46 = (v[2] & 0xFFFFu) | (v[3] << 16);
-          const uint32_t p13 = (v[0] >> 16) | (v[1] & 0xFFFF0000u), p57 = (v[2] >> 16) | (v[3] & 0xFFFF0000u);
-          const int g = e >> 2;
-          *reinterpret_cast<u32x4*>(xs + g * kGroupPadDw + 4 * (e & 3)) = (u32x4){p02, p46, p13, p57};
-          float sm = 0.0f;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) sm += __uint_as_float(v[i] << 16) + __uint_as_float(v[i] & 0xFFFF0000u);
-          sm += __shfl_xor(sm, 1);
-          sm += __shfl_xor(sm, 2);
-          if ((threadIdx.x & 3) == 0) ssum[g] = sm;
+        if (w + d * W < nb) {
+          gemv_load_x(xr, w + d * W, lane, buf[d].xv);
+          gemv_load<TQ, F>(rs, w + d * W, t0, lane, buf[d]);
         }
-        __syncthreads();
-        staged = ch;
-      }
-      if (wave_on) {
-        // Ring of D register slots: block w + iW lives in slot i % D and the
-        // slot is refilled with block w + (i + D)W right after it is consumed.
-        for (int i0 = 0; w + i0 * W < nb; i0 += D) {
+      for (int i0 = 0; w + i0 * W < nb; i0 += D) {
 #pragma unroll
-          for (int d = 0; d < D; ++d) {
-            const int jj = w + (i0 + d) * W;
-            if (jj < nb) {
-              gemv_compute<TQ, F>(buf[d], jj * kBlockCols + kGroup * c < kvalid,
-                                  xs + (jj * kGroupsPerRow + c) * kGroupPadDw,
-                                  F == kWMX ? 0.0f : ssum[jj * kGroupsPerRow + c], acc);
-              if (jj + D * W < nb) gemv_load<TQ, F>(rs, jj + D * W, t0, lane, buf[d]);
+        for (int d = 0; d < D; ++d) {
+          const int jj = w + (i0 + d) * W;
+          if (jj < nb) {
+            const float S = gemv_stage_x<F>(buf[d].xv, xw, lane);
+            gemv_compute<TQ, F>(buf[d], jj * kBlockCols + kGroup * c < kvalid, xw + c * kGroupPadDw, S, acc);
+            if (jj + D * W < nb) {
+              gemv_load_x(xr, jj + D * W, lane, buf[d].xv);
+              gemv_load<TQ, F>(rs, jj + D * W, t0, lane, buf[d]);
             }
           }
         }
@@ -656,21 +668,19 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
 }
 
 // Persistent streaming form of gemv_kernel, for launches whose K fits one
-// staged piece of x (every Gemma3 K).  A job's row groups are dealt to a
-// bounded number of workgroups, rg = r0, r0 + nwg, ...; a workgroup stages x
-// once and each wave streams its blocks of all its row groups (w, w + W, ...
-// of each) through one ring of D register slots that runs on across row
-// groups, so the next row group's loads are in flight while the current one's
-// rows are added up and stored.  The arithmetic and the order of every sum
-// are those of gemv_kernel (same waves per row group), hence the same bits.
-// Every wave meets the same barriers: two to stage x, two per row group.
+// chunk (every Gemma3 K).  A job's row groups are dealt to a bounded number
+// of workgroups, rg = r0, r0 + nwg, ...; each wave streams its blocks of all
+// its row groups (w, w + W, ... of each), each block with its x, through one
+// ring of D register slots that runs on across row groups, so the next row
+// group's loads are in flight while the current one's rows are added up and
+// stored.  The arithmetic and the order of every sum are those of
+// gemv_kernel (same waves per row group), hence the same bits.  Every wave
+// meets the same barriers: two per row group.
 template <int TQ, int D, int F>
 __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_stream_kernel(const GemvArgs args) {
   constexpr int kBytes = wblock_bytes<F>();
-  extern __shared__ __attribute__((aligned(16))) float lds[];
-  float* red = lds;
-  float* ssum = lds + kRedFloats;
-  uint32_t* xs = reinterpret_cast<uint32_t*>(ssum + args.chunk_blocks * kGroupsPerRow);
+  __shared__ float red[kRedFloats];
+  __shared__ __attribute__((aligned(16))) uint32_t xw_all[kGemvMaxWaves][kGroupsPerRow * kGroupPadDw];
 
   const int wg = blockIdx.x;
   int jb = 0;
@@ -682,7 +692,6 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_stream_kernel(const G
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int c = lane & 7;
   const int W = J.waves, nb = J.KB;
-  const int nthreads = blockDim.x;
   const bool wave_on = w < W;  // wave-uniform
   const int r0 = wg - J.wg_begin;
   const int nrg = r0 < J.nrg ? (J.nrg - 1 - r0) / J.nwg + 1 : 0;  // row groups of this workgroup
@@ -691,12 +700,16 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_stream_kernel(const G
   const int Q = nbw * nrg;
   const int kvalid = J.K;
   const int sbytes = nb * kBytes;  // bytes of one strip
+  uint32_t* const xw = xw_all[wave_on ? w : 0];
+  const __amdgpu_buffer_rsrc_t xr =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(J.x), (short)0, 2 * J.K, 0x00020000);
 
   // Load cursor: row group lk of this workgroup, this wave's block ljq of it.
   int lk = 0, ljq = 0;
   auto load_next = [&](GemvSlot<TQ>& R, int& jj) {
     const int row0 = (r0 + lk * J.nwg) * 8 * TQ;
     jj = w + ljq * W;
+    gemv_load_x(xr, jj, lane, R.xv);
     gemv_load<TQ, F>(chunk_rsrc(J.blob + (size_t)(row0 >> 5) * sbytes, sbytes), jj, (row0 & 31) >> 3, lane, R);
     if (++ljq == nbw) {
       ljq = 0;
@@ -704,18 +717,6 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_stream_kernel(const G
     }
   };
 
-  // The first pieces of x are requested before the weight blocks (every
-  // workgroup waits for x before it computes anything), then the wave's
-  // first D blocks, then x is staged as in gemv_kernel.
-  constexpr int kXPre = gemv_xpre<TQ>();
-  u32x4 xpre[kXPre];
-#pragma unroll
-  for (int i = 0; i < kXPre; ++i) {
-    const int e = threadIdx.x + i * nthreads;
-    const int k = 8 * e;
-    xpre[i] = (u32x4){0u, 0u, 0u, 0u};
-    if (e < nb * (kBlockCols / 8) && k < J.K) xpre[i] = *reinterpret_cast<const u32x4*>(J.x + k);
-  }
   GemvSlot<TQ> buf[D];
   int jjs[D];
 #pragma unroll
@@ -723,35 +724,6 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_stream_kernel(const G
     jjs[d] = 0;
     if (d < Q) load_next(buf[d], jjs[d]);
   }
-  {
-    int it = 0;
-    for (int e = threadIdx.x; e < nb * (kBlockCols / 8); e += nthreads, ++it) {
-      const int k = 8 * e;
-      u32x4 v = (u32x4){0u, 0u, 0u, 0u};
-      if (it < kXPre) {
-#pragma unroll
-        for (int i = 0; i < kXPre; ++i)
-          if (i == it) v = xpre[i];
-      } else if (k < J.K) {
-        v = *reinterpret_cast<const u32x4*>(J.x + k);
-      }
-      if constexpr (F == kWMX) {
-        *reinterpret_cast<u32x4*>(xs + (e >> 2) * kGroupPadDw + 4 * (e & 3)) = v;
-        continue;
-      }
-      const uint32_t p02 = (v[0] & 0xFFFFu) | (v[1] << 16), p46 = (v[2] & 0xFFFFu) | (v[3] << 16);
-      const uint32_t p13 = (v[0] >> 16) | (v[1] & 0xFFFF0000u), p57 = (v[2] >> 16) | (v[3] & 0xFFFF0000u);
-      const int g = e >> 2;
-      *reinterpret_cast<u32x4*>(xs + g * kGroupPadDw + 4 * (e & 3)) = (u32x4){p02, p46, p13, p57};
-      float sm = 0.0f;
-#pragma unroll
-      for (int i = 0; i < 4; ++i) sm += __uint_as_float(v[i] << 16) + __uint_as_float(v[i] & 0xFFFF0000u);
-      sm += __shfl_xor(sm, 1);
-      sm += __shfl_xor(sm, 2);
-      if ((threadIdx.x & 3) == 0) ssum[g] = sm;
-    }
-  }
-  __syncthreads();
 
   // Row group k of this workgroup is complete in every wave: add the 8 groups
   // of each row, then the W waves' sums in wave order, and store.
@@ -797,8 +769,8 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_stream_kernel(const G
       const int q = q0 + d;
       if (q < Q) {
         const int jj = jjs[d];
-        gemv_compute<TQ, F>(buf[d], jj * kBlockCols + kGroup * c < kvalid, xs + (jj * kGroupsPerRow + c) * kGroupPadDw,
-                            F == kWMX ? 0.0f : ssum[jj * kGroupsPerRow + c], acc);
+        const float S = gemv_stage_x<F>(buf[d].xv, xw, lane);
+        gemv_compute<TQ, F>(buf[d], jj * kBlockCols + kGroup * c < kvalid, xw + c * kGroupPadDw, S, acc);
         if (q + D < Q) load_next(buf[d], jjs[d]);
         if (++cjq == nbw) {
           finish(ck);
@@ -1926,13 +1898,14 @@ static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtyp
     max_waves = std::max(max_waves, J.waves);
     args.chunk_blocks = std::max(args.chunk_blocks, std::min(J.KB, kGemvChunkBlocks));
   }
-  const size_t lds = sizeof(float) * ((size_t)kRedFloats + (size_t)args.chunk_blocks * kGroupsPerRow * (1 + kGroupPadDw));
+  // LDS of both kernels (static): the row sums and one x slot per wave.
+  constexpr int64_t lds = sizeof(float) * (kRedFloats + kGemvMaxWaves * kGroupsPerRow * kGroupPadDw);
   const dim3 block(64 * max_waves);
   if (streaming) {
     // Streaming form: a bounded grid (workgroups per CU as the LDS allows, at
     // most kGemvStreamPerCu), dealt to the jobs in proportion to their row
     // groups; each workgroup walks its job's row groups r0, r0 + nwg, ...
-    const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(kGemvStreamPerCu, (160 * 1024) / (int64_t)lds));
+    const int64_t per_cu = std::max<int64_t>(1, std::min<int64_t>(kGemvStreamPerCu, (160 * 1024) / lds));
     const int64_t total_rg = strips * (4 / tq), budget = (int64_t)device_cus() * per_cu;
     int64_t sw = 0;
     for (int i = 0; i < count; ++i) {
@@ -1941,14 +1914,14 @@ static q4nx_status gemv_launch(const q4nx_gemv_desc* descs, int count, q4nx_dtyp
       J.wg_begin = (int)sw;
       sw += J.nwg;
     }
-    hipLaunchKernelGGL((gemv_stream_kernel<2, kGemvDepth2, F>), dim3((unsigned)sw), block, lds, stream, args);
+    hipLaunchKernelGGL((gemv_stream_kernel<2, kGemvDepth2, F>), dim3((unsigned)sw), block, 0, stream, args);
     return check_launch(fn);
   }
   const dim3 grid((unsigned)wg);
-  switch (tq) {
-    case 4: hipLaunchKernelGGL((gemv_kernel<4, kGemvDepth4, F>), grid, block, lds, stream, args); break;
-    case 2: hipLaunchKernelGGL((gemv_kernel<2, kGemvDepth2, F>), grid, block, lds, stream, args); break;
-    default: hipLaunchKernelGGL((gemv_kernel<1, kGemvDepth1, F>), grid, block, lds, stream, args); break;
+  switch (tq) {  // x is staged per wave in static LDS
+    case 4: hipLaunchKernelGGL((gemv_kernel<4, kGemvDepth4, F>), grid, block, 0, stream, args); break;
+    case 2: hipLaunchKernelGGL((gemv_kernel<2, kGemvDepth2, F>), grid, block, 0, stream, args); break;
+    default: hipLaunchKernelGGL((gemv_kernel<1, kGemvDepth1, F>), grid, block, 0, stream, args); break;
   }
   return check_launch(fn);
 }
