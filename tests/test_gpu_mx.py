@@ -79,8 +79,10 @@ def _gemv_case(q4, N, K, seed, mode="model", bf16_out=False, proj=0):
     return oracle.check_close(host_f32(y), oracle.gemv_f64(w32, x), oracle.abs_bound(x, w32), bf16_out=bf16_out)
 
 
+# (2561, 2080) and (5088, 1056): launches of 81 and 159 strips (the persistent
+# streaming form) with a ragged last strip and K tails.
 @pytest.mark.parametrize("N,K", [(1, 32), (32, 256), (33, 288), (64, 512), (1024, 1152), (257, 1184), (8, 4096),
-                                 (3000, 256), (40, 21504), (40, 22560), (33, 51232)])
+                                 (3000, 256), (40, 21504), (40, 22560), (33, 51232), (2561, 2080), (5088, 1056)])
 @pytest.mark.parametrize("mode", ["model", "edge"])
 def test_mx_gemv_parity_small(q4, N, K, mode):
     _say("mx gemv", N, K, mode)

@@ -93,9 +93,13 @@ def _gemv_case(q4, N, K, seed, mode="zp", bf16_out=False, layer=0, proj=0):
     return ok, worst
 
 
-# K = 22560 and 51232 span 89 and 201 blocks: x is staged in more than one chunk.
+# K = 22560 and 51232 span 89 and 201 blocks: the weights are read in more than one chunk.
+# N = 2561, 5088 and 2600 give launches of 81, 159 and 82 strips, which take the
+# persistent streaming form (80-159 strips), here with a ragged last strip and
+# K tails (2080 = 8 blocks + 32 columns, 1056 = 4 blocks + 32 columns) and
+# with the longest K it takes (88 blocks).
 GEMV_SHAPES = [(1, 32), (32, 256), (33, 288), (64, 512), (1024, 1152), (100, 544), (257, 1184), (8, 4096),
-               (3000, 256), (40, 21504), (40, 22560), (33, 51232)]
+               (3000, 256), (40, 21504), (40, 22560), (33, 51232), (2561, 2080), (5088, 1056), (2600, 22528)]
 
 
 @pytest.mark.parametrize("N,K", GEMV_SHAPES)
