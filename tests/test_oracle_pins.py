@@ -278,3 +278,32 @@ def test_tolerance_check_catches_planted_errors():
     assert not oracle.check_close(y2, y, b)[0]
     s_t = s.reshape(N, -1)[:, ::-1].copy()
     assert not oracle.check_close(oracle.gemv_f64(oracle.dequant_f32(codes, s_t, o), x), y, b)[0]
+
+
+def test_abs_bound_and_tolerance_hand_values():
+    """abs_bound, tolerance and check_close on a worked example (bf16-exact
+    values, sums done by hand): bound_n = sum_k |x_k w_nk|; tol = 2e-3 bound
+    + 1e-5 (+ |y_ref| 2^-8 for bf16 outputs); a result passes at 0.999 tol
+    and fails at 1.001 tol, and a NaN never passes."""
+    x = oracle.f32_to_bf16(np.array([1.0, -2.0, 0.5], dtype=np.float32))
+    w = np.array([[1.0, 2.0, -4.0], [0.25, 0.0, 3.0]], dtype=np.float32)
+    # row 0: |1*1| + |-2*2| + |0.5*-4| = 1 + 4 + 2 = 7; row 1: 0.25 + 0 + 1.5 = 1.75
+    assert np.array_equal(oracle.abs_bound(x, w), np.array([7.0, 1.75]))
+    # y = W x: row 0: 1 - 4 - 2 = -5; row 1: 0.25 + 0 + 1.5 = 1.75
+    y = oracle.gemv_f64(w, x)
+    assert np.array_equal(y, np.array([-5.0, 1.75]))
+    tol = oracle.tolerance(np.array([7.0, 1.75]))
+    assert np.allclose(tol, [2e-3 * 7 + 1e-5, 2e-3 * 1.75 + 1e-5], rtol=0, atol=1e-15)
+    tol16 = oracle.tolerance(np.array([7.0, 1.75]), y_ref=y, bf16_out=True)
+    assert np.allclose(tol16 - tol, [5.0 / 256, 1.75 / 256], rtol=0, atol=1e-15)
+    b = oracle.abs_bound(x, w)
+    ok, worst = oracle.check_close(y + 0.999 * tol, y, b)
+    assert ok and abs(worst - 0.999) < 1e-9
+    ok, worst = oracle.check_close(y - 1.001 * tol, y, b)
+    assert not ok and abs(worst - 1.001) < 1e-9
+    assert not oracle.check_close(np.array([np.nan, 1.75]), y, b)[0]
+    # the matrix form: X[m] . W[n] over rows of X
+    X = oracle.f32_to_bf16(np.array([[1.0, -2.0, 0.5], [0.0, 1.0, -1.0]], dtype=np.float32))
+    # row 1 of X: |0| + |1*2| + |-1*-4| = 6 against W row 0; |0| + 0 + |-1*3| = 3 against W row 1
+    assert np.array_equal(oracle.abs_bound(X, w), np.array([[7.0, 1.75], [6.0, 3.0]]))
+    assert np.array_equal(oracle.gemm_f64(X, w), np.array([[-5.0, 1.75], [6.0, -3.0]]))
