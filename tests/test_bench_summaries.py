@@ -130,3 +130,18 @@ def test_kernel_hash_ignores_comments_only():
     src = "int a; // one\n/* two\n three */\nint b;\n\n   \n"
     assert bench.kernel_source_sha256(src) == bench.kernel_source_sha256("int a;\nint b;\n")
     assert bench.kernel_source_sha256(src) != bench.kernel_source_sha256("int a;\nint c;\n")
+
+
+def test_bench_refuses_more_than_one_gpu():
+    """bench.py measures one GPU: --gpus N > 1 (or a WORLD_SIZE above 1) exits
+    with status 2 and says why, before touching any device."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    for extra_env, args in (({}, ["--gpus", "2"]), ({"WORLD_SIZE": "4"}, [])):
+        env = dict(os.environ, **extra_env)
+        r = subprocess.run([sys.executable, os.path.join(root, "bench.py")] + args, cwd=root, env=env,
+                           capture_output=True, text=True, timeout=120)
+        assert r.returncode == 2, (r.returncode, r.stderr[-2000:])
+        assert "one GPU only" in r.stderr
+        assert r.stdout == ""
