@@ -52,7 +52,7 @@ __device__ __forceinline__ float wave_sum(float v) {
 // Phase 1.  grid (chunks, G); CH cache positions per workgroup, D = head
 // dimension, HG = query heads per group.  Partial of (head, chunk) at
 // work[(head * nchunks + chunk) * (D + 4)]: m_c, l_c, -, -, Y_c[D].
-template <int CH, int D, int HG>
+template <int CH, int D, int HG, bool PRE>
 __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_t* __restrict__ q,
                                                                   const uint16_t* __restrict__ K,
                                                                   const uint16_t* __restrict__ V, int64_t L,
@@ -75,15 +75,55 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
   const uint16_t* Kg = K + (size_t)g * L * D + (size_t)k0 * D;
   const uint16_t* Vg = V + (size_t)g * L * D + (size_t)k0 * D;
 
-  for (int e = tid; e < HG * D / 2; e += kFkvThreads) {
-    const int h = e / (D / 2), p = e % (D / 2);
-    qs[h][p] = reinterpret_cast<const uint32_t*>(q + (size_t)(g * HG + h) * D)[p];
+  // Lane roles: scores use 8 lanes per position (8 x 16 B = one 128-byte
+  // piece of the row per load; lane u of the 8 takes dims 64i + 8u .. +7),
+  // the weighted values R lanes per row (16 bytes, 8 dims, each).
+  const int u = lane & 7, kw = lane >> 3;
+  const int rs = lane / R, db = lane % R;
+  // PRE: the whole chunk's K and V pieces of this lane are requested before
+  // the query is staged, so the three round trips overlap (the chunk's rows
+  // sit in registers: CH / 32 x D / 64 K pieces and CH / (4P) V pieces).
+  constexpr int kQPer = (HG * D / 2 + kFkvThreads - 1) / kFkvThreads;
+  constexpr int kKIt = PRE ? CH / 32 : 1, kKPc = PRE ? D / 64 : 1, kVIt = PRE ? CH / (4 * P) : 1;
+  uint4 kreg[kKIt][kKPc], vreg[kVIt];
+  uint32_t qreg[kQPer];
+  if constexpr (PRE) {
+#pragma unroll
+    for (int o = 0; o < kQPer; ++o) {
+      const int e = tid + o * kFkvThreads;
+      if (e < HG * D / 2) {
+        const int h = e / (D / 2), p = e % (D / 2);
+        qreg[o] = reinterpret_cast<const uint32_t*>(q + (size_t)(g * HG + h) * D)[p];
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < kKIt; ++r) {
+      const int pl = (r * 4 + wave) * 8 + kw;
+#pragma unroll
+      for (int i = 0; i < kKPc; ++i)
+        kreg[r][i] = pl < n ? reinterpret_cast<const uint4*>(Kg + (size_t)pl * D)[8 * i + u] : uint4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int it = 0; it < kVIt; ++it) {
+      const int pl = wave * P + rs + it * 4 * P;
+      vreg[it] = pl < n ? reinterpret_cast<const uint4*>(Vg + (size_t)pl * D)[db] : uint4{0, 0, 0, 0};
+    }
+#pragma unroll
+    for (int o = 0; o < kQPer; ++o) {
+      const int e = tid + o * kFkvThreads;
+      if (e < HG * D / 2) qs[e / (D / 2)][e % (D / 2)] = qreg[o];
+    }
+  } else {
+    for (int e = tid; e < HG * D / 2; e += kFkvThreads) {
+      const int h = e / (D / 2), p = e % (D / 2);
+      qs[h][p] = reinterpret_cast<const uint32_t*>(q + (size_t)(g * HG + h) * D)[p];
+    }
   }
   __syncthreads();
 
-  // Scores (Eq. 6): 8 lanes per position (8 x 16 B = one 128-byte piece of
-  // the row per load); lane u of the 8 takes dims 64i + 8u .. +7.
-  const int u = lane & 7, kw = lane >> 3;
+  // Scores (Eq. 6).  (With PRE, CH / 32 <= kFkvUnroll: the loop unrolls
+  // fully and kreg is indexed by constants.)
+  static_assert(!PRE || CH / 32 <= kFkvUnroll, "PRE needs the score loop fully unrolled");
 #pragma unroll kFkvUnroll
   for (int r = 0; r < CH / 32; ++r) {
     const int pl = (r * 4 + wave) * 8 + kw;
@@ -94,7 +134,9 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
       const uint4* row = reinterpret_cast<const uint4*>(Kg + (size_t)pl * D);
 #pragma unroll
       for (int i = 0; i < D / 64; ++i) {
-        const uint4 kv = row[8 * i + u];
+        uint4 kv;
+        if constexpr (PRE) kv = kreg[r][i];
+        else kv = row[8 * i + u];
 #pragma unroll
         for (int h = 0; h < HG; ++h) {
           const uint4 qv = *reinterpret_cast<const uint4*>(&qs[h][32 * i + 4 * u]);
@@ -152,17 +194,14 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
 #pragma unroll
   for (int h = 0; h < HG; ++h) l[h] = (red[0][h] + red[1][h]) + (red[2][h] + red[3][h]);
 
-  // Weighted values (Eq. 11): R lanes per row, 16 bytes (8 dims) each; wave
-  // w reads rows w*P + rs, then every 4P rows.
-  const int rs = lane / R, db = lane % R;
+  // Weighted values (Eq. 11): wave w takes rows w*P + rs, then every 4P rows.
   float y[HG][8];
 #pragma unroll
   for (int h = 0; h < HG; ++h)
 #pragma unroll
     for (int e = 0; e < 8; ++e) y[h][e] = 0.0f;
-#pragma unroll kFkvUnroll
-  for (int pl = wave * P + rs; pl < n; pl += 4 * P) {
-    const uint4 w = reinterpret_cast<const uint4*>(Vg + (size_t)pl * D)[db];
+  // One V row piece (8 dims) of position pl into the weighted sums.
+  const auto vrow = [&](int pl, const uint4 w) __attribute__((always_inline)) {
     const float v[8] = {bf16lo(w.x), bf16hi(w.x), bf16lo(w.y), bf16hi(w.y),
                         bf16lo(w.z), bf16hi(w.z), bf16lo(w.w), bf16hi(w.w)};
 #pragma unroll
@@ -171,6 +210,16 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
 #pragma unroll
       for (int e = 0; e < 8; ++e) y[h][e] = fmaf(f, v[e], y[h][e]);
     }
+  };
+  if constexpr (PRE) {
+#pragma unroll
+    for (int it = 0; it < kVIt; ++it) {
+      const int pl = wave * P + rs + it * 4 * P;
+      if (pl < n) vrow(pl, vreg[it]);
+    }
+  } else {
+#pragma unroll kFkvUnroll
+    for (int pl = wave * P + rs; pl < n; pl += 4 * P) vrow(pl, reinterpret_cast<const uint4*>(Vg + (size_t)pl * D)[db]);
   }
   // Sum the P row slots of the wave (lanes db, db + R, ...), then the 4 waves.
 #pragma unroll
@@ -259,8 +308,25 @@ template <int CH, int D, int HG>
 static void launch_flowkv(const uint16_t* q, const uint16_t* K, const uint16_t* V, int64_t L, int G, int j0, int j1,
                           float scale, float* work, void* out, int out_bf16, hipStream_t stream) {
   const int nchunks = (int)ceil_div(j1 - j0, CH);
-  hipLaunchKernelGGL((flowkv_chunk_kernel<CH, D, HG>), dim3(nchunks, G), dim3(kFkvThreads), 0, stream, q, K, V, L,
-                     j0, j1, scale, work);
+  // Short ranges (at most 4096 positions, so 64-position chunks: the
+  // sliding-window layers), which are latency-bound, request each chunk's K
+  // and V with the query when there are at least 64 workgroups.  Measured on
+  // MI355X over the Gemma3 layer stacks at 32K, same bits: 27B (256
+  // workgroups per windowed layer) 3% and 4B (64) 2% faster.  Not with fewer
+  // workgroups (1B's windowed layers, 16: the V requests then delay the
+  // scores on each CU's own bandwidth) nor on long ranges (1B's global layers
+  // also take 64-position chunks, 512 workgroups: 2-5% slower with the early
+  // requests).
+  bool pre = false;
+  if constexpr (CH == kMinChunk) {
+    pre = (int64_t)nchunks * G >= 64 && j1 - j0 <= 4096;
+    if (pre)
+      hipLaunchKernelGGL((flowkv_chunk_kernel<CH, D, HG, true>), dim3(nchunks, G), dim3(kFkvThreads), 0, stream, q,
+                         K, V, L, j0, j1, scale, work);
+  }
+  if (!pre)
+    hipLaunchKernelGGL((flowkv_chunk_kernel<CH, D, HG, false>), dim3(nchunks, G), dim3(kFkvThreads), 0, stream, q, K,
+                       V, L, j0, j1, scale, work);
   // Dims per merge workgroup: halved (down to 16) until there are at least
   // 128 workgroups.
   const int H = G * HG;

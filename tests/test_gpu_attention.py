@@ -53,6 +53,11 @@ CASES = [
     (8, 1, 64, 1024, 777, 0),
     (8, 4, 256, 32768, 32767, 0),
     (32, 16, 128, 32768, 20000, 0),
+    # sliding windows of 1000 positions (a ragged last chunk of 40) with at
+    # least 64 chunk workgroups: K and V requested with the query
+    (32, 16, 128, 4096, 1500, 1000),
+    (64, 16, 64, 2048, 1500, 1000),
+    (8, 4, 256, 4096, 3000, 1000),
     # many heads: the merge takes 64, 128 and 256 dims per workgroup
     (64, 16, 128, 2048, 1999, 0),
     (128, 16, 128, 1024, 900, 0),
