@@ -1097,8 +1097,9 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
   // written to the other stage and step s+3 is loaded into Rs.
   //
   // Placement of the LDS accesses.  A slot is one MFMA, 32 clocks, in which
-  // the CU's LDS serves about four 1 KiB wave accesses -- one per wave -- and
-  // every slice reads its 8 fragments of the next slice.  The writes of the
+  // the CU's LDS serves about six 1 KiB wave reads or two and a half wave
+  // writes (measured on MI355X: ~190 and ~78 bytes per clock), and every
+  // slice reads its 8 fragments of the next slice.  The writes of the
   // other stage must land before the barrier, so they are spread over the
   // slices before it instead of being packed into one:
   //   bf16 W (16 writes: x0..x7, w0..w7), odd slots from 1: slice 0 x0..x5,
