@@ -52,6 +52,9 @@ CASES = [
     (32, 16, 128, 4096, 3000, 1024),
     (8, 1, 64, 1024, 777, 0),
     (8, 4, 256, 32768, 32767, 0),
+    # 1B geometry at 30K: 469 chunks of 64, more than a merge slice holds in
+    # registers (the two-pass merge)
+    (4, 1, 256, 32768, 30000, 0),
     (32, 16, 128, 32768, 20000, 0),
     # sliding windows of 1000 positions (a ragged last chunk of 40) with at
     # least 64 chunk workgroups: K and V requested with the query
