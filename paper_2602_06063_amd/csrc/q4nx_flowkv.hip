@@ -22,6 +22,7 @@
 
 #include "q4nx_device.h"
 #include "q4nx_internal.h"
+#include "q4nx_xlane.h"
 
 namespace q4nx {
 
@@ -39,16 +40,32 @@ __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
 __device__ __forceinline__ float bf16lo(uint32_t v) { return __uint_as_float(v << 16); }
 __device__ __forceinline__ float bf16hi(uint32_t v) { return __uint_as_float(v & 0xFFFF0000u); }
 
-// Wave-wide reductions in a fixed order (deterministic).
+// Wave-wide reductions in a fixed order (deterministic): exchanges with lane
+// l ^ 32, then ^ 16, ..., ^ 1.
 __device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
+  v = fmaxf(v, xor_lane<32>(v));
+  v = fmaxf(v, xor_lane<16>(v));
+  v = fmaxf(v, xor_lane<8>(v));
+  v = fmaxf(v, xor_lane<4>(v));
+  v = fmaxf(v, xor_lane<2>(v));
+  return fmaxf(v, xor_lane<1>(v));
 }
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+  v += xor_lane<32>(v);
+  v += xor_lane<16>(v);
+  v += xor_lane<8>(v);
+  v += xor_lane<4>(v);
+  v += xor_lane<2>(v);
+  return v + xor_lane<1>(v);
+}
+
+// Sum over the lanes l ^ m for m = R, 2R, ..., 32 (R a power of two, 8 to
+// 32), in that order.
+template <int R>
+__device__ __forceinline__ float sum_lanes_from(float v) {
+  if constexpr (R <= 8) v += xor_lane<8>(v);
+  if constexpr (R <= 16) v += xor_lane<16>(v);
+  return v + xor_lane<32>(v);
 }
 
 // Phase 1.  grid (chunks, G); CH cache positions per workgroup, D = head
@@ -152,9 +169,9 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
 #pragma unroll
     for (int h = 0; h < HG; ++h) {
       float v = acc[h];
-      v += __shfl_xor(v, 1);
-      v += __shfl_xor(v, 2);
-      v += __shfl_xor(v, 4);
+      v += xor_lane<1>(v);
+      v += xor_lane<2>(v);
+      v += xor_lane<4>(v);
       if (u == 0) fs[pl][h] = pl < n ? v * scale : -INFINITY;
     }
   }
@@ -229,8 +246,7 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       float v = y[h][e];
-#pragma unroll
-      for (int o = R; o < 64; o <<= 1) v += __shfl_xor(v, o);
+      v = sum_lanes_from<R>(v);
       y[h][e] = v;
     }
   if (rs == 0) {

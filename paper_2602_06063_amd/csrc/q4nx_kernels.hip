@@ -17,6 +17,7 @@
 
 #include "q4nx_device.h"
 #include "q4nx_internal.h"
+#include "q4nx_xlane.h"
 
 namespace q4nx {
 
@@ -521,15 +522,15 @@ __device__ __forceinline__ float gemv_stage_x(const uint32_t (&xv)[2], uint32_t*
   __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
   const float s01 = __uint_as_float(xv[0] << 16) + __uint_as_float(xv[0] & 0xFFFF0000u);
   const float s23 = __uint_as_float(xv[1] << 16) + __uint_as_float(xv[1] & 0xFFFF0000u);
-  const float o01 = __shfl_xor(s01, 8), o23 = __shfl_xor(s23, 8);  // the odd lane's (x4+x5), (x6+x7)
+  const float o01 = xor_lane<8>(s01), o23 = xor_lane<8>(s23);  // the odd lane's (x4+x5), (x6+x7)
   float sm = 0.0f;
   sm += s01;
   sm += s23;
   sm += o01;
   sm += o23;                       // the run's sum, on the even lanes
-  sm += __shfl_xor(sm, 16);
-  sm += __shfl_xor(sm, 32);
-  const float se = __shfl_xor(sm, 8);
+  sm += xor_lane<16>(sm);
+  sm += xor_lane<32>(sm);
+  const float se = xor_lane<8>(sm);
   return (r & 1) ? se : sm;
 }
 
@@ -642,9 +643,9 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_kernel(const GemvArgs
     // Add the 8 groups of each row: lanes 8r'..8r'+7 hold row octet t, row r'.
 #pragma unroll
     for (int t = 0; t < TQ; ++t) {
-      acc[t] += __shfl_xor(acc[t], 1);
-      acc[t] += __shfl_xor(acc[t], 2);
-      acc[t] += __shfl_xor(acc[t], 4);
+      acc[t] += xor_lane<1>(acc[t]);
+      acc[t] += xor_lane<2>(acc[t]);
+      acc[t] += xor_lane<4>(acc[t]);
     }
     // Lane with c == t (t < TQ) holds row 8t + l/8 of the row group.
     if (wave_on && c < TQ) {
@@ -731,9 +732,9 @@ __global__ __launch_bounds__(64 * kGemvMaxWaves) void gemv_stream_kernel(const G
   auto finish = [&](int k) {
 #pragma unroll
     for (int t = 0; t < TQ; ++t) {
-      acc[t] += __shfl_xor(acc[t], 1);
-      acc[t] += __shfl_xor(acc[t], 2);
-      acc[t] += __shfl_xor(acc[t], 4);
+      acc[t] += xor_lane<1>(acc[t]);
+      acc[t] += xor_lane<2>(acc[t]);
+      acc[t] += xor_lane<4>(acc[t]);
     }
     if (wave_on && c < TQ) {
       const float v = (c == 0) ? acc[0] : (c == 1) ? acc[1] : (c == 2) ? acc[2] : acc[3];
@@ -1970,8 +1971,12 @@ __global__ __launch_bounds__(256) void stream_read_kernel(const uint8_t* __restr
 #pragma unroll
     for (int u = 0; u < 4; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
   }
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) acc ^= (uint32_t)__shfl_xor((int)acc, o);
+  acc ^= (uint32_t)xor_lane_bits<32>((int)acc);
+  acc ^= (uint32_t)xor_lane_bits<16>((int)acc);
+  acc ^= (uint32_t)xor_lane_bits<8>((int)acc);
+  acc ^= (uint32_t)xor_lane_bits<4>((int)acc);
+  acc ^= (uint32_t)xor_lane_bits<2>((int)acc);
+  acc ^= (uint32_t)xor_lane_bits<1>((int)acc);
   if ((threadIdx.x & 63) == 0) sink[blockIdx.x * 4 + (threadIdx.x >> 6)] = __uint_as_float(acc & 0x3FFFFFFFu);
 }
 
