@@ -904,6 +904,7 @@ __device__ __forceinline__ void store_wave_tile(const f32x16 (&acc)[TI][TJ], voi
 // rows past M and W strips past the matrix are clamped to the last valid one;
 // their outputs are never stored.
 constexpr int kWideThreads = 256;
+constexpr int kMaxSplit = 4;  // K segments of a split-K launch, at most
 constexpr int kWideLdsBytes = 2 * 2 * 256 * kLdsStride * 2;  // two stages of X and W
 constexpr int64_t kWideMaxK = int64_t(1) << 22;               // 256 rows x K x 2 B < 2^31
 
@@ -1294,15 +1295,36 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
 
 // Sum of the split-K partial products part[0..ks-1][M][N] (row stride N), in
 // segment order, to Y (row stride ldy) in float32 or bf16.  Thread t handles
-// four consecutive columns of one row.
+// four consecutive columns of one row.  With vec (N and ldy multiples of 4,
+// Y 16-byte aligned) a full quad is read as one 16-byte load per segment --
+// every segment's load issued before the adds -- and written as one store;
+// the order of the adds, hence every bit, is that of the scalar path.
 __global__ __launch_bounds__(256) void splitk_sum_kernel(const float* __restrict__ part, int ks, int M, int N,
-                                                         void* __restrict__ Y, int64_t ldy, int y_bf16) {
+                                                         void* __restrict__ Y, int64_t ldy, int y_bf16, int vec) {
   const int q = (N + 3) >> 2;  // column quads per row
   const int64_t id = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (id >= (int64_t)M * q) return;
   const int row = (int)(id / q), col = (int)(id - (int64_t)row * q) * 4;
   const int64_t MN = (int64_t)M * N;
   const float* p = part + (int64_t)row * N + col;
+  if (vec && col + 3 < N) {
+    f32x4 seg[kMaxSplit];
+#pragma unroll
+    for (int s = 0; s < kMaxSplit; ++s)
+      if (s < ks) seg[s] = __builtin_nontemporal_load(reinterpret_cast<const f32x4*>(p + s * MN));
+    f32x4 v = seg[0];
+#pragma unroll
+    for (int s = 1; s < kMaxSplit; ++s)
+      if (s < ks) v += seg[s];
+    if (y_bf16) {
+      typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+      *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(Y) + row * ldy + col) =
+          (u32x2){pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+    } else {
+      *reinterpret_cast<f32x4*>(static_cast<float*>(Y) + row * ldy + col) = v;
+    }
+    return;
+  }
   float v[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) v[j] = col + j < N ? p[j] : 0.0f;
@@ -1611,7 +1633,7 @@ static int gemm_plan(int64_t M, int64_t N, int64_t K, int cus, bool split_ok, Ge
   };
   double best = 1e300;
   int count = 0;
-  for (int ks = 2; ks <= 4; ++ks) {
+  for (int ks = 2; ks <= kMaxSplit; ++ks) {
     const double c = split_cost(M, N, ks);
     if (c < best) {
       best = c;
@@ -1646,7 +1668,7 @@ static int gemm_plan(int64_t M, int64_t N, int64_t K, int cus, bool split_ok, Ge
           count = 2;
         }
       }
-      for (int ks = 2; ks <= 4; ++ks) {
+      for (int ks = 2; ks <= kMaxSplit; ++ks) {
         const double c2 = rounds(a, ma, na) * kGemmTiles[a].round_cost + split_cost(mb, nb, ks) + 0.02 + 0.001 * dir;
         if (c2 < best) {
           best = c2;
@@ -1761,8 +1783,9 @@ static q4nx_status launch_region(const GemmRegion& r, int64_t N, int64_t K, cons
                                : launch_gemm256<false, WF>(r.M, r.N, K, Xr, Wr, Yr, r.N, y_bf16, stream, r.ks, work);
     if (st != Q4NX_OK) return st;
     const int64_t threads = r.M * ceil_div(r.N, 4);
+    const int vec = r.N % 4 == 0 && N % 4 == 0 && aligned(Yr, 16);
     hipLaunchKernelGGL(splitk_sum_kernel, dim3((unsigned)ceil_div(threads, 256)), dim3(256), 0, stream, work, r.ks,
-                       (int)r.M, (int)r.N, Yr, N, y_bf16);
+                       (int)r.M, (int)r.N, Yr, N, y_bf16, vec);
     return Q4NX_OK;
   }
   switch (r.tile) {
