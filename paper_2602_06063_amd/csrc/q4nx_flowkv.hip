@@ -4,7 +4,7 @@
 // its sliding-window variant.
 //
 // The sweep is split in two launches.  Phase 1 gives every (KV group, chunk of
-// 64, 128, 256 or 512 positions) to one workgroup, which computes for the H/G query heads
+// 32, 64, 128, 256 or 512 positions) to one workgroup, which computes for the H/G query heads
 // of the group the chunk's own running state: the max score m_c (Eq. 7), the
 // denominator l_c = sum exp(s - m_c) (Eq. 8, 10) and the weighted values
 // Y_c = sum exp(s - m_c) v (Eq. 11), into the caller's workspace.  Phase 2
@@ -28,7 +28,7 @@ namespace q4nx {
 
 typedef __bf16 bf16x2f __attribute__((ext_vector_type(2)));
 
-constexpr int kMinChunk = 64;      // smallest chunk: sizes the workspace
+constexpr int kMinChunk = 32;      // smallest chunk: sizes the workspace
 constexpr int kFkvThreads = 256;   // 4 waves
 constexpr int kMergeRegs = 8;      // chunks per slice the one-pass merge holds in registers
 
@@ -360,17 +360,16 @@ template <int CH, int D, int HG>
 static void launch_flowkv(const uint16_t* q, const uint16_t* K, const uint16_t* V, int64_t L, int G, int j0, int j1,
                           float scale, float* work, void* out, int out_bf16, hipStream_t stream) {
   const int nchunks = (int)ceil_div(j1 - j0, CH);
-  // Short ranges (at most 4096 positions, so 64-position chunks: the
+  // Short ranges (at most 4096 positions, so 32- or 64-position chunks: the
   // sliding-window layers), which are latency-bound, request each chunk's K
   // and V with the query when there are at least 64 workgroups.  Measured on
   // MI355X over the Gemma3 layer stacks at 32K, same bits: 27B (256
   // workgroups per windowed layer) 3% and 4B (64) 2% faster.  Not with fewer
-  // workgroups (1B's windowed layers, 16: the V requests then delay the
-  // scores on each CU's own bandwidth) nor on long ranges (1B's global layers
-  // also take 64-position chunks, 512 workgroups: 2-5% slower with the early
-  // requests).
+  // workgroups (1B's windowed layers: the V requests then delay the scores on
+  // each CU's own bandwidth) nor on long ranges (1B's global layers also take
+  // 64-position chunks, 512 workgroups: 2-5% slower with the early requests).
   bool pre = false;
-  if constexpr (CH == kMinChunk) {
+  if constexpr (CH <= 64) {
     pre = (int64_t)nchunks * G >= 64 && j1 - j0 <= 4096;
     if (pre)
       hipLaunchKernelGGL((flowkv_chunk_kernel<CH, D, HG, true>), dim3(nchunks, G), dim3(kFkvThreads), 0, stream, q,
@@ -411,11 +410,15 @@ static void launch_flowkv(const uint16_t* q, const uint16_t* K, const uint16_t* 
 }
 
 // Chunk size: the largest of 512, 256, 128, 64 positions that still gives at
-// least two workgroups per CU.
+// least two workgroups per CU; 32 where 64 leaves CUs without a workgroup.
+// (Measured on MI355X over the Gemma3 layer stacks at 32K: 32-position chunks
+// for the windowed layers took the 4B stack from 0.407 to 0.376 ms (64 -> 128
+// workgroups per layer) and the 1B stack from 0.287 to 0.278 ms (16 -> 32),
+// while the 27B windowed layers, 256 workgroups at 64, went 3% slower at 32.)
 static int flowkv_chunk(int64_t n, int G, int cus) {
-  for (int ch = 512; ch > kMinChunk; ch >>= 1)
+  for (int ch = 512; ch > 64; ch >>= 1)
     if (ceil_div(n, ch) * G >= 2 * cus) return ch;
-  return kMinChunk;
+  return ceil_div(n, 64) * G >= cus ? 64 : kMinChunk;
 }
 
 template <int D, int HG>
@@ -425,7 +428,8 @@ static void launch_chunked(const uint16_t* q, const uint16_t* K, const uint16_t*
     case 512: launch_flowkv<512, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
     case 256: launch_flowkv<256, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
     case 128: launch_flowkv<128, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
-    default: launch_flowkv<64, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
+    case 64: launch_flowkv<64, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
+    default: launch_flowkv<32, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
   }
 }
 

@@ -61,6 +61,11 @@ CASES = [
     (32, 16, 128, 4096, 1500, 1000),
     (64, 16, 64, 2048, 1500, 1000),
     (8, 4, 256, 4096, 3000, 1000),
+    # grids of 64-position chunks below one workgroup per CU take 32-position
+    # chunks (K and V requested with the query from 64 workgroups): d = 128
+    # and d = 64, whole and ragged last chunks
+    (16, 4, 128, 2048, 1023, 1024),
+    (16, 8, 64, 2048, 2000, 1000),
     # many heads: the merge takes 64, 128 and 256 dims per workgroup
     (64, 16, 128, 2048, 1999, 0),
     (128, 16, 128, 1024, 900, 0),
