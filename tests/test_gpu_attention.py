@@ -56,8 +56,9 @@ CASES = [
     # registers (the two-pass merge)
     (4, 1, 256, 32768, 30000, 0),
     (32, 16, 128, 32768, 20000, 0),
-    # sliding windows of 1000 positions (a ragged last chunk of 40) with at
-    # least 64 chunk workgroups: K and V requested with the query
+    # sliding windows of 1000 positions (a ragged last chunk: 40 positions
+    # of a 64-position chunk, or 8 of a 32-position one) with at least 64
+    # chunk workgroups: K and V requested with the query
     (32, 16, 128, 4096, 1500, 1000),
     (64, 16, 64, 2048, 1500, 1000),
     (8, 4, 256, 4096, 3000, 1000),
