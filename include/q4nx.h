@@ -218,12 +218,12 @@ q4nx_status q4nx_gemm_bf16(int64_t M, int64_t N, int64_t K, const uint16_t* d_X,
                            void* d_Y, q4nx_dtype y_dtype, hipStream_t stream);
 
 /* Smallest chunk (cache positions per workgroup) of q4nx_flowkv_decode. */
-#define Q4NX_FLOWKV_MIN_CHUNK 32
+#define Q4NX_FLOWKV_MIN_CHUNK 16
 
 /*
  * Bytes of the workspace q4nx_flowkv_decode needs for H query heads of
  * dimension d attending to n_keys cache positions:
- * H * ceil(n_keys / 32) * (d + 4) * 4.  Returns 0 for a non-positive or
+ * H * ceil(n_keys / 16) * (d + 4) * 4.  Returns 0 for a non-positive or
  * out-of-range argument.
  */
 size_t q4nx_flowkv_workspace_size(int64_t H, int64_t d, int64_t n_keys);
@@ -271,7 +271,7 @@ q4nx_status q4nx_flowkv_decode(const uint16_t* d_q, const uint16_t* d_k, const u
  * in the array needs to start at zero (each call writes every partial it
  * reads).  Errors: as q4nx_flowkv_decode; Q4NX_ERR_BUFFER_TOO_SMALL when the
  * partials of the attended range, H * ceil(n / chunk) * (d + 4) * 4 bytes
- * (chunk = the launch's chunk length, 32-512), exceed the array -- e.g. the
+ * (chunk = the launch's chunk length, 16-512), exceed the array -- e.g. the
  * Gemma3-27B geometry (H = 32, d = 128) up to about 64K attended positions
  * at any chunk length; Q4NX_ERR_HIP if the array cannot be located.
  */

@@ -4,7 +4,7 @@
 // its sliding-window variant.
 //
 // The sweep is split in two launches.  Phase 1 gives every (KV group, chunk of
-// 32, 64, 128, 256 or 512 positions) to one workgroup, which computes for the H/G query heads
+// 16, 32, 64, 128, 256 or 512 positions) to one workgroup, which computes for the H/G query heads
 // of the group the chunk's own running state: the max score m_c (Eq. 7), the
 // denominator l_c = sum exp(s - m_c) (Eq. 8, 10) and the weighted values
 // Y_c = sum exp(s - m_c) v (Eq. 11), into the caller's workspace.  Phase 2
@@ -28,7 +28,7 @@ namespace q4nx {
 
 typedef __bf16 bf16x2f __attribute__((ext_vector_type(2)));
 
-constexpr int kMinChunk = 32;      // smallest chunk: sizes the workspace
+constexpr int kMinChunk = 16;      // smallest chunk: sizes the workspace
 constexpr int kFkvThreads = 256;   // 4 waves
 constexpr int kMergeRegs = 8;      // chunks per slice the one-pass merge holds in registers
 
@@ -101,9 +101,11 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
   const int rs = lane / R, db = lane % R;
   // PRE: the whole chunk's K and V pieces of this lane are requested before
   // the query is staged, so the three round trips overlap (the chunk's rows
-  // sit in registers: CH / 32 x D / 64 K pieces and CH / (4P) V pieces).
+  // sit in registers: kSIt x D / 64 K pieces and CH / (4P) V pieces, rounded
+  // up; pieces past the chunk are not loaded).
+  constexpr int kSIt = (CH + 31) / 32;  // score passes of 32 positions (one, partly used, for CH = 16)
   constexpr int kQPer = (HG * D / 2 + kFkvThreads - 1) / kFkvThreads;
-  constexpr int kKIt = PRE ? CH / 32 : 1, kKPc = PRE ? D / 64 : 1, kVIt = PRE ? CH / (4 * P) : 1;
+  constexpr int kKIt = PRE ? kSIt : 1, kKPc = PRE ? D / 64 : 1, kVIt = PRE ? (CH + 4 * P - 1) / (4 * P) : 1;
   uint4 kreg[kKIt][kKPc], vreg[kVIt];
   uint32_t qreg[kQPer];
   if constexpr (PRE) {
@@ -140,11 +142,11 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
   }
   __syncthreads();
 
-  // Scores (Eq. 6).  (With PRE, CH / 32 <= kFkvUnroll: the loop unrolls
-  // fully and kreg is indexed by constants.)
-  static_assert(!PRE || CH / 32 <= kFkvUnroll, "PRE needs the score loop fully unrolled");
+  // Scores (Eq. 6).  (With PRE, kSIt <= kFkvUnroll: the loop unrolls fully
+  // and kreg is indexed by constants.)
+  static_assert(!PRE || kSIt <= kFkvUnroll, "PRE needs the score loop fully unrolled");
 #pragma unroll kFkvUnroll
-  for (int r = 0; r < CH / 32; ++r) {
+  for (int r = 0; r < kSIt; ++r) {
     const int pl = (r * 4 + wave) * 8 + kw;
     float acc[HG];
 #pragma unroll
@@ -172,7 +174,7 @@ __global__ __launch_bounds__(kFkvThreads) void flowkv_chunk_kernel(const uint16_
       v += xor_lane<1>(v);
       v += xor_lane<2>(v);
       v += xor_lane<4>(v);
-      if (u == 0) fs[pl][h] = pl < n ? v * scale : -INFINITY;
+      if (u == 0 && pl < CH) fs[pl][h] = pl < n ? v * scale : -INFINITY;
     }
   }
   __syncthreads();
@@ -360,8 +362,8 @@ template <int CH, int D, int HG>
 static void launch_flowkv(const uint16_t* q, const uint16_t* K, const uint16_t* V, int64_t L, int G, int j0, int j1,
                           float scale, float* work, void* out, int out_bf16, hipStream_t stream) {
   const int nchunks = (int)ceil_div(j1 - j0, CH);
-  // Short ranges (at most 4096 positions, so 32- or 64-position chunks: the
-  // sliding-window layers), which are latency-bound, request each chunk's K
+  // Short ranges (at most 4096 positions, so chunks of 64 positions or fewer:
+  // the sliding-window layers), which are latency-bound, request each chunk's K
   // and V with the query when there are at least 64 workgroups.  Measured on
   // MI355X over the Gemma3 layer stacks at 32K, same bits: 27B (256
   // workgroups per windowed layer) 3% and 4B (64) 2% faster.  Not with fewer
@@ -410,15 +412,18 @@ static void launch_flowkv(const uint16_t* q, const uint16_t* K, const uint16_t* 
 }
 
 // Chunk size: the largest of 512, 256, 128, 64 positions that still gives at
-// least two workgroups per CU; 32 where 64 leaves CUs without a workgroup.
-// (Measured on MI355X over the Gemma3 layer stacks at 32K: 32-position chunks
-// for the windowed layers took the 4B stack from 0.407 to 0.376 ms (64 -> 128
-// workgroups per layer) and the 1B stack from 0.287 to 0.278 ms (16 -> 32),
-// while the 27B windowed layers, 256 workgroups at 64, went 3% slower at 32.)
+// least two workgroups per CU; 32 where 64 leaves CUs without a workgroup,
+// and 16 where 32 still gives fewer than 64 workgroups.  (Measured on MI355X
+// over the Gemma3 layer stacks at 32K, windowed layers: the 4B stack 0.407 ms
+// at 64 positions (64 workgroups per layer), 0.376 at 32 (128), 0.378 at 16
+// (256); the 1B stack 0.287 ms at 64 (16 workgroups), 0.277 at 32 (32),
+// 0.255 at 16 (64); the 27B windowed layers, 256 workgroups at 64, went 3%
+// slower at 32.)
 static int flowkv_chunk(int64_t n, int G, int cus) {
   for (int ch = 512; ch > 64; ch >>= 1)
     if (ceil_div(n, ch) * G >= 2 * cus) return ch;
-  return ceil_div(n, 64) * G >= cus ? 64 : kMinChunk;
+  if (ceil_div(n, 64) * G >= cus) return 64;
+  return ceil_div(n, 32) * G >= 64 ? 32 : kMinChunk;
 }
 
 template <int D, int HG>
@@ -429,7 +434,8 @@ static void launch_chunked(const uint16_t* q, const uint16_t* K, const uint16_t*
     case 256: launch_flowkv<256, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
     case 128: launch_flowkv<128, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
     case 64: launch_flowkv<64, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
-    default: launch_flowkv<32, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
+    case 32: launch_flowkv<32, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
+    default: launch_flowkv<16, D, HG>(q, K, V, L, G, j0, j1, scale, work, out, out_bf16, stream); break;
   }
 }
 

@@ -363,8 +363,8 @@ def test_flowkv_workspace_size_and_validation():
     import paper_2602_06063_amd as q4
     L = q4.lib
     assert L.q4nx_flowkv_workspace_size(8, 256, 1) == 8 * 1 * 260 * 4
-    assert L.q4nx_flowkv_workspace_size(8, 256, 257) == 8 * 9 * 260 * 4
-    assert L.q4nx_flowkv_workspace_size(32, 128, 32768) == 32 * 1024 * 132 * 4
+    assert L.q4nx_flowkv_workspace_size(8, 256, 257) == 8 * 17 * 260 * 4
+    assert L.q4nx_flowkv_workspace_size(32, 128, 32768) == 32 * 2048 * 132 * 4
     assert L.q4nx_flowkv_workspace_size(0, 256, 10) == 0 and L.q4nx_flowkv_workspace_size(8, 256, 0) == 0
     A = ctypes.c_void_p(1 << 20)      # aligned, never dereferenced: every call below fails validation
     MIS = ctypes.c_void_p((1 << 20) + 2)

@@ -67,6 +67,11 @@ CASES = [
     # and d = 64, whole and ragged last chunks
     (16, 4, 128, 2048, 1023, 1024),
     (16, 8, 64, 2048, 2000, 1000),
+    # one KV group: 16-position chunks, with K and V requested early (64
+    # chunks) and without (63, a ragged last chunk of 8), d = 256 and 128
+    (4, 1, 256, 2048, 2047, 1024),
+    (4, 1, 256, 2048, 1500, 1000),
+    (8, 1, 128, 4096, 3000, 1024),
     # many heads: the merge takes 64, 128 and 256 dims per workgroup
     (64, 16, 128, 2048, 1999, 0),
     (128, 16, 128, 1024, 900, 0),
