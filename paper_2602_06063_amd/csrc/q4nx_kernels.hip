@@ -1293,6 +1293,313 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
     }
 }
 
+// ---- 256 x 128 tile, one wave per SIMD ------------------------------------
+// The 256 x 256 kernel's scheme on half the columns: four waves in a 2 x 2
+// grid, each owning a 128 x 64 sub-tile (8 MFMA accumulators), so a 16-deep
+// K slice is 8 MFMAs against 6 fragment reads.  A K step is four blocks of 8
+// MFMA slots:
+//   slices 0-1  fragment reads of the next slice at slots 0-5; the next step's
+//               X rows written on odd slots (bf16 W: x0-x3, x4-x7; packed W:
+//               two per slice, between the dequantized W writes at slots 3
+//               and 7), its weight group dequantized a quarter of 8 columns
+//               per slot (packed W)
+//   slice 2     reads; the rest of the writes (bf16 W: w0-w3; packed W: x4-x7)
+//   barrier
+//   slice 3     reads of slice 0 of the next step
+// with each global load of step + 3 issued one slot after the write that
+// frees its register.  The MFMA chain of every output is the same as in the
+// other kernels, hence the same bits.  K must be a multiple of 64 (shapes
+// with a K tail take the general kernel).  Against the general kernel's
+// 256 x 128 tiles (16 or 8 waves, the compiler's schedule), measured on MI355X
+// with the same bits: Gemma3-4B o 41.6 -> 38.2 us (Q4NX weights), the 4B
+// gate/up remainder 50.2 -> 44.7 us and the 27B o remainder 72.4 -> 55.1 us
+// (bf16 weights), an MXFP4-variant 4B q/k/v product 54.9 -> 44.5 us.
+constexpr int kW128LdsBytes = 2 * (256 + 128) * kLdsStride * 2;  // two stages of X (256 rows) and W (128 rows)
+
+template <int WF>
+struct Wide128Regs {
+  u32x4 x[8];
+  u32x4 q;
+  uint32_t s, m;
+};
+template <>
+struct Wide128Regs<kWBf16> {
+  u32x4 x[8];
+  u32x4 w[4];
+};
+
+template <int WF>
+__global__ __launch_bounds__(kWideThreads) void gemm256x128_kernel(const uint16_t* __restrict__ X,
+                                                                   const uint8_t* __restrict__ wsrc,
+                                                                   void* __restrict__ Y, int M, int N, int K, int ldy,
+                                                                   int KB, int NS, int tiles_n, int y_bf16) {
+  constexpr int TI = 4, TJ = 2;
+  extern __shared__ __attribute__((aligned(16))) uint16_t gl[];
+  uint16_t* const xs0 = gl;                          // [2][256][72]
+  uint16_t* const ws0 = gl + 2 * 256 * kLdsStride;   // [2][128][72]
+
+  int bm, bn;
+  gemm_tile_of(blockIdx.x, gridDim.x, tiles_n, bm, bn);
+  const int m0 = bm * 256, n0 = bn * 128;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 1, wn = wave & 1;
+
+  const int rows_x = min(256, M - m0);
+  const __amdgpu_buffer_rsrc_t rsx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(X + (size_t)m0 * K), (short)0, rows_x * K * 2, 0x00020000);
+  constexpr bool WQ4 = WF != kWBf16;
+  constexpr int kBB = wblock_bytes<WF>();
+  const int s0 = n0 >> 5, nst = min(4, NS - s0), rows_w = min(128, N - n0);
+  const __amdgpu_buffer_rsrc_t rsw =
+      WQ4 ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wsrc + (size_t)s0 * KB * kBB), (short)0,
+                                              nst * KB * kBB, 0x00020000)
+          : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(wsrc + (size_t)n0 * K * 2), (short)0,
+                                              rows_w * K * 2, 0x00020000);
+  constexpr int kLoads = WF == kWQ4NX ? 11 : WF == kWMX ? 10 : 12;
+
+  const int c8 = tid & 7, half = tid & 1;
+  int vx[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) vx[i] = (min((tid >> 3) + 32 * i, rows_x - 1) * K + 8 * c8) * 2;
+  int vq = 0, vs = 0, vw[4];
+  if constexpr (WQ4) {
+    const int r = tid >> 1;
+    const int st = min(r >> 5, nst - 1), rr = r & 31;
+    vq = st * KB * kBB + 128 * rr + 16 * half;
+    vs = st * KB * kBB + kCodeBytes + (WF == kWMX ? 1 : 2) * (8 * rr + half);
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) vw[i] = (min((tid >> 3) + 32 * i, rows_w - 1) * K + 8 * c8) * 2;
+  }
+  const int nsteps = K / kBK;
+
+  f32x16 acc[TI][TJ];
+#pragma unroll
+  for (int a = 0; a < TI; ++a)
+#pragma unroll
+    for (int b = 0; b < TJ; ++b)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[a][b][e] = 0.0f;
+
+  // Global load i of step t (clamped to the last step) into R.
+  auto load1 = [&](Wide128Regs<WF>& R, int t, int i) {
+    const int k0 = min(t, nsteps - 1) * kBK;
+    const int sq = (k0 >> 8) * kBB + 16 * ((k0 & 255) >> 5);
+    const int ss = (k0 >> 8) * kBB + (WF == kWMX ? 1 : 2) * ((k0 & 255) >> 5);
+    if (i < 8) {
+      R.x[i] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsx, vx[i], 2 * k0, 0));
+      return;
+    }
+    if constexpr (!WQ4) {
+      R.w[i - 8] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsw, vw[i - 8], 2 * k0, 0));
+    } else if (i == 8) {
+      R.q = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsw, vq + sq, 0, kNtLoad));
+    } else if (i == 9) {
+      if constexpr (WF == kWMX)
+        R.s = __builtin_amdgcn_raw_buffer_load_b8(rsw, vs + ss, 0, kNtLoad);
+      else
+        R.s = __builtin_amdgcn_raw_buffer_load_b16(rsw, vs + ss, 0, kNtLoad);
+    } else {
+      R.m = __builtin_amdgcn_raw_buffer_load_b16(rsw, vs + ss + kScaleBytes, 0, kNtLoad);
+    }
+  };
+  auto xs_row = [&](int st) { return xs0 + st * 256 * kLdsStride + (tid >> 3) * kLdsStride + 8 * c8; };
+  auto ws_row = [&](int st) { return ws0 + st * 128 * kLdsStride + (tid >> 1) * kLdsStride + kGroup * half; };
+  // Fragment i of K slice kq, in first-use order A0, B0, B1, A1, A2, A3.
+  const int fa = (128 * wm + (lane & 31)) * kLdsStride + 8 * (lane >> 5);
+  const int fb = (64 * wn + (lane & 31)) * kLdsStride + 8 * (lane >> 5);
+  auto read1 = [&](int st, int kq, bf16x8 (&A)[TI], bf16x8 (&B)[TJ], int i) {
+    const uint16_t* xs = xs0 + st * 256 * kLdsStride + fa + 16 * kq;
+    const uint16_t* ws = ws0 + st * 128 * kLdsStride + fb + 16 * kq;
+    if (i == 0) A[0] = *reinterpret_cast<const bf16x8*>(xs);
+    else if (i <= 2) B[i - 1] = *reinterpret_cast<const bf16x8*>(ws + 32 * (i - 1) * kLdsStride);
+    else A[i - 2] = *reinterpret_cast<const bf16x8*>(xs + 32 * (i - 2) * kLdsStride);
+  };
+  auto mma1 = [&](const bf16x8 (&A)[TI], const bf16x8 (&B)[TJ], int i) {
+    acc[i >> 1][i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[i >> 1], B[i & 1], acc[i >> 1][i & 1], 0, 0, 0);
+  };
+  // Dequantization of the thread's weight group in 16 pieces (p = 0..15: a
+  // quarter of the 8 columns 8(p/4)..+7), as in the 256 x 256 kernel.
+  uint32_t wlo = 0, whi = 0;
+  float wd = 0.0f, wmo = 0.0f;
+  f32x2 wa, we, wb, wg;
+  u32x4 wo;
+  auto wpiece = [&](const Wide128Regs<WF>& R, int st, int p) {
+    if constexpr (WF == kWMX) {
+      const int u = p >> 2, qt = p & 3;
+      if (p == 0) wd = e8m0_f32(R.s);
+      const uint32_t w = R.q[u];
+      if (qt == 0) wo[0] = fp4x2_bf16<0>(w, wd);
+      else if (qt == 1) wo[1] = fp4x2_bf16<1>(w, wd);
+      else if (qt == 2) wo[2] = fp4x2_bf16<2>(w, wd);
+      else {
+        wo[3] = fp4x2_bf16<3>(w, wd);
+        *reinterpret_cast<u32x4*>(ws_row(st) + 8 * u) = wo;
+      }
+    } else if constexpr (WQ4) {
+      const int u = p >> 2, qt = p & 3;
+      if (qt == 0) {
+        if (u == 0) {
+          wd = bf16_to_f32(R.s) * 512.0f;
+          wmo = bf16_to_f32(R.m);
+        }
+        wlo = opaque(R.q[u] & 0x0F0F0F0Fu);
+        whi = opaque((R.q[u] >> 4) & 0x0F0F0F0Fu);
+        wa = codes2_f32<false>(wlo);
+      } else if (qt == 1) {
+        we = codes2_f32<false>(whi);
+        wo[0] = pack_bf16x2(eq3(wa[0], wd, wmo), eq3(we[0], wd, wmo));
+        wo[1] = pack_bf16x2(eq3(wa[1], wd, wmo), eq3(we[1], wd, wmo));
+      } else if (qt == 2) {
+        wb = codes2_f32<true>(wlo);
+        wg = codes2_f32<true>(whi);
+        wo[2] = pack_bf16x2(eq3(wb[0], wd, wmo), eq3(wg[0], wd, wmo));
+      } else {
+        wo[3] = pack_bf16x2(eq3(wb[1], wd, wmo), eq3(wg[1], wd, wmo));
+        *reinterpret_cast<u32x4*>(ws_row(st) + 8 * u) = wo;
+      }
+    }
+  };
+  auto xwrite = [&](const Wide128Regs<WF>& R, uint16_t* xsn, int k) {
+    *reinterpret_cast<u32x4*>(xsn + 32 * k * kLdsStride) = R.x[k];
+  };
+  auto wwrite = [&](const Wide128Regs<WF>& R, int st, int k) {
+    if constexpr (!WQ4)
+      *reinterpret_cast<u32x4*>(xs0 + 2 * 256 * kLdsStride + st * 128 * kLdsStride +
+                                ((tid >> 3) + 32 * k) * kLdsStride + 8 * c8) = R.w[k];
+  };
+
+  bf16x8 A0[TI], B0[TJ], A1[TI], B1[TJ];
+  // Work of slot i of slice sl besides the MFMA and the fragment read: the
+  // stage writes of step s+1 (from Rs) and the loads of step s+3 (into Rs).
+  auto side = [&](Wide128Regs<WF>& Rs, uint16_t* xsn, int nxt, int s, int sl, int i) {
+    if constexpr (!WQ4) {
+      // writes: slice 0 x0-x3, slice 1 x4-x7, slice 2 w0-w3 on odd slots;
+      // load k one slot after write k (slot 0 of the next slice after slot 7)
+      if (sl < 3 && (i & 1)) {
+        const int k = 4 * sl + (i >> 1);
+        if (k < 8) xwrite(Rs, xsn, k);
+        else wwrite(Rs, nxt, k - 8);
+      }
+      if (!(i & 1)) {
+        const int k = i == 0 ? 4 * sl - 1 : 4 * sl + (i >> 1) - 1;  // the write one slot back
+        if (k >= 0 && k < 12 && !(sl == 3 && i > 0)) load1(Rs, s + 3, k);
+      }
+    } else {
+      // dequant pieces 0-7 in slice 0, 8-15 in slice 1 (W writes at slots 3
+      // and 7); X writes: slice 0 slots 1, 5; slice 1 slots 1, 5; slice 2
+      // odd slots; loads: x one slot after its write, the scale (and offset)
+      // after piece 0 consumed them, the codes in slice 2 after piece 15.
+      if (sl < 2) wpiece(Rs, nxt, 8 * sl + i);
+      int kx = -1;
+      if (sl < 2 && (i == 1 || i == 5)) kx = 2 * sl + (i >> 2);
+      if (sl == 2 && (i & 1)) kx = 4 + (i >> 1);
+      if (kx >= 0) xwrite(Rs, xsn, kx);
+      int kl = -1;
+      if (sl < 2 && (i == 2 || i == 6)) kl = 2 * sl + (i >> 2);
+      if (sl == 2 && !(i & 1) && i > 0) kl = 4 + (i >> 1) - 1;
+      if (sl == 3 && i == 0) kl = 7;
+      if (kl >= 0) load1(Rs, s + 3, kl);
+      if (sl == 0 && i == 4) load1(Rs, s + 3, 9);                         // scale
+      if (WF == kWQ4NX && sl == 0 && i == 6) load1(Rs, s + 3, 10);        // offset
+      if (sl == 2 && i == 0) load1(Rs, s + 3, 8);                         // codes
+    }
+  };
+  auto step = [&](int s, Wide128Regs<WF>& Rs) {
+    const int cur = s & 1, nxt = cur ^ 1;
+    uint16_t* xsn = xs_row(nxt);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      mma1(A0, B0, i);
+      if (i < 6) read1(cur, 1, A1, B1, i);
+      side(Rs, xsn, nxt, s, 0, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      mma1(A1, B1, i);
+      if (i < 6) read1(cur, 2, A0, B0, i);
+      side(Rs, xsn, nxt, s, 1, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      mma1(A0, B0, i);
+      if (i < 6) read1(cur, 3, A1, B1, i);
+      side(Rs, xsn, nxt, s, 2, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      mma1(A1, B1, i);
+      if (i < 6) read1(nxt, 0, A0, B0, i);
+      side(Rs, xsn, nxt, s, 3, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  Wide128Regs<WF> R0, R1;
+#pragma unroll
+  for (int i = 0; i < kLoads; ++i) load1(R0, 0, i);
+#pragma unroll
+  for (int i = 0; i < kLoads; ++i) load1(R1, 1, i);
+  {
+    uint16_t* xs = xs_row(0);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) xwrite(R0, xs, i);
+    if constexpr (WF == kWMX) {
+      const float Xs = e8m0_f32(R0.s);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) *reinterpret_cast<u32x4*>(ws_row(0) + 8 * u) = mx8_bf16(R0.q[u], Xs);
+    } else if constexpr (WQ4) {
+      const float d512 = bf16_to_f32(R0.s) * 512.0f, m = bf16_to_f32(R0.m);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) *reinterpret_cast<u32x4*>(ws_row(0) + 8 * u) = dequant8_bf16(R0.q[u], d512, m);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) wwrite(R0, 0, i);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < kLoads; ++i) load1(R0, 2, i);
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < 6; ++i) read1(0, 0, A0, B0, i);
+  int s = 0;
+  for (; s + 1 < nsteps; s += 2) {
+    step(s, R1);
+    step(s + 1, R0);
+  }
+  if (s < nsteps) step(s, R1);
+
+  const bool full = m0 + 256 <= M && n0 + 128 <= N;
+  if (full && ldy < kFastStoreMaxLdy) {
+    store_wave_tile(acc,
+                    static_cast<char*>(Y) + ((size_t)(unsigned)(m0 + 128 * wm) * (unsigned)ldy +
+                                             (unsigned)(n0 + 64 * wn)) * (y_bf16 ? 2u : 4u),
+                    ldy, y_bf16);
+    return;
+  }
+#pragma unroll
+  for (int a = 0; a < TI; ++a)
+#pragma unroll
+    for (int b = 0; b < TJ; ++b) {
+      const int col = n0 + 64 * wn + 32 * b + (lane & 31);
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = m0 + 128 * wm + 32 * a + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        if (full || (row < M && col < N)) {
+          if (y_bf16)
+            static_cast<uint16_t*>(Y)[(size_t)row * ldy + col] = f32_to_bf16_bits(acc[a][b][e]);
+          else
+            static_cast<float*>(Y)[(size_t)row * ldy + col] = acc[a][b][e];
+        }
+      }
+    }
+}
+
 // Sum of the split-K partial products part[0..ks-1][M][N] (row stride N), in
 // segment order, to Y (row stride ldy) in float32 or bf16.  Thread t handles
 // four consecutive columns of one row.  With vec (N and ldy multiples of 4,
@@ -1343,8 +1650,9 @@ __global__ __launch_bounds__(256) void splitk_sum_kernel(const float* __restrict
 }
 
 // ---- general tiles, two waves per SIMD --------------------------------------
-// Workgroup tile BM (tokens) x BN (outputs) for the shapes the 256 x 256 tile
-// does not fill.  WAVES_M x WAVES_N waves; each owns a (BM/WAVES_M) x
+// Workgroup tile BM (tokens) x BN (outputs) for the shapes the 256 x 256 and
+// 256 x 128 hand-scheduled tiles do not serve (128 x 128 and 128 x 64 tiles,
+// 256 x 128 tiles with a K tail).  WAVES_M x WAVES_N waves; each owns a (BM/WAVES_M) x
 // (BN/WAVES_N) sub-tile.  LDS holds two stages of the X tile and of the
 // dequantized W tile; a K step runs the MFMAs of step k from one stage while
 // the same waves dequantize step k+1 into the other, with the raw global data
@@ -1564,7 +1872,11 @@ __global__ __launch_bounds__(64 * WAVES_M * WAVES_N) void gemm_kernel(
 
 // ---- launch planning ----------------------------------------------------------
 // Tile shapes: 0 = 256 x 256 (gemm256_kernel; the general kernel past
-// kWideMaxK), 1 = 256 x 128, 2 = 128 x 128, 3 = 128 x 64.
+// kWideMaxK), 1 = 256 x 128 (gemm256x128_kernel; the general kernel with a K
+// tail or past kWideMaxK), 2 = 128 x 128, 3 = 128 x 64 (the general kernel).
+// The round costs below were measured with the general kernel's 256 x 128
+// tiles; the one-wave-per-SIMD form is faster on the Gemma3 shapes it serves,
+// which only favours the plans that use it.
 struct GemmTile {
   int bm, bn;
   float round_cost;  // time of one full round (a tile on every CU), relative to shape 0
@@ -1764,6 +2076,20 @@ static q4nx_status launch_gemm256(int64_t M, int64_t N, int64_t K, const uint16_
   return Q4NX_OK;
 }
 
+template <int WF>
+static q4nx_status launch_gemm256x128(int64_t M, int64_t N, int64_t K, const uint16_t* X, const void* blob, void* Y,
+                                      int64_t ldy, int y_bf16, hipStream_t stream) {
+  auto kern = gemm256x128_kernel<WF>;
+  static LdsReservation lds_res;
+  if (!lds_res.ensure(reinterpret_cast<const void*>(kern), kW128LdsBytes))
+    return fail(Q4NX_ERR_HIP, "q4nx_gemm: cannot reserve LDS");
+  const int64_t tiles_n = ceil_div(N, 128), tiles_m = ceil_div(M, 256);
+  hipLaunchKernelGGL(kern, dim3((unsigned)(tiles_n * tiles_m)), dim3(kWideThreads), kW128LdsBytes, stream, X,
+                     static_cast<const uint8_t*>(blob), Y, (int)M, (int)N, (int)K, (int)ldy,
+                     (int)ceil_div(K, kBlockCols), (int)ceil_div(N, kBlockRows), (int)tiles_n, y_bf16);
+  return Q4NX_OK;
+}
+
 // One region of the output: X rows m0.., W rows n0.. (strips n0/32.. of a
 // packed matrix) and Y at (m0, n0) with row stride N, so each launch sees an
 // ordinary smaller problem.
@@ -1794,11 +2120,13 @@ static q4nx_status launch_region(const GemmRegion& r, int64_t N, int64_t K, cons
       if (K % kBK != 0) return launch_gemm256<true, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
       return launch_gemm256<false, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
     case 1:
-      // Q4NX weights: 16 waves of 32 x 64 (four per SIMD), which hide the
-      // dequantization in the tile loads better than 8 waves of 64 x 64
-      // (measured on MI355X: Gemma3 4B q/k/v 56.8 -> 55.5 us, o 42.2 -> 39.2
-      // us); bf16 and MXFP4-variant weights keep 8 waves (the 4B bf16 gate/up
-      // remainder ran 2.6% slower with 16).  Same MFMA chains, same bits.
+      if (K % kBK == 0 && K < kWideMaxK) return launch_gemm256x128<WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
+      // A K tail: the general kernel.  Q4NX weights as 16 waves of 32 x 64
+      // (four per SIMD), which hide the dequantization in the tile loads
+      // better than 8 waves of 64 x 64 (measured on MI355X: Gemma3 4B q/k/v
+      // 56.8 -> 55.5 us, o 42.2 -> 39.2 us with K a multiple of 64); bf16 and
+      // MXFP4-variant weights keep 8 waves (the 4B bf16 gate/up remainder ran
+      // 2.6% slower with 16).  Same MFMA chains, same bits.
       if constexpr (WF == kWQ4NX) return launch_gemm<256, 128, 8, 2, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
       else return launch_gemm<256, 128, 4, 2, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);
     case 2: return launch_gemm<128, 128, 2, 4, WF>(r.M, r.N, K, Xr, Wr, Yr, N, y_bf16, stream);

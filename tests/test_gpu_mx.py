@@ -210,7 +210,7 @@ def test_mx_gemm_launch_plans_sampled_rows(q4, M, N, K, bf16_out):
 
 
 @pytest.mark.parametrize("M,N,K", [(5, 33, 288), (130, 200, 1152), (300, 96, 5376), (3996, 4080, 544),
-                                   (4000, 5344, 224), (4096, 21472, 96)])
+                                   (4000, 5344, 224), (4096, 21472, 96), (2040, 4000, 2560)])
 def test_mx_gemm_equals_dequant_then_gemm_bf16_bitwise(q4, M, N, K):
     """Same bf16 weights, same MFMA chain over K: the same bits."""
     _say("mx two-phase", M, N, K)

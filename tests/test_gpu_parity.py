@@ -351,7 +351,7 @@ def test_gemm_wide_rows_either_side_of_the_fast_store_stride(q4, N):
 # structure.  Same bf16 weights and the same MFMA chain over K as the fused
 # q4nx_gemm, hence the same bits.
 TWO_PHASE_SHAPES = [(5, 33, 288), (130, 200, 1152), (300, 96, 5376), (4096, 2048, 256), (3996, 4080, 544),
-                    (4000, 5344, 224), (4096, 21472, 96)]
+                    (4000, 5344, 224), (4096, 21472, 96), (2040, 4000, 2560)]
 
 
 @pytest.mark.parametrize("M,N,K", TWO_PHASE_SHAPES)
