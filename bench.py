@@ -580,11 +580,15 @@ def traffic_file(config):
     return os.path.join(PROFILES, f"hbm-traffic_{WORKLOAD_SLUG.get(config, f'config{config}')}.md")
 
 
+# The prefill step's launches: the products, their partial sums and the
+# dequant pass of products that dequantize first.
+PREFILL_KERNELS = ("gemm256_kernel", "gemm256x128_kernel", "gemm_kernel", "splitk_sum_kernel", "dequant_kernel")
+
+
 def kernel_family(name):
-    # The prefill step's launches: the products, their partial sums and the
-    # dequant pass of products that dequantize first (the counter passes run
-    # only the decode and prefill steps, so no other step launches these).
-    if any(k in name for k in ("gemm256_kernel", "gemm_kernel", "splitk_sum_kernel", "dequant_kernel")):
+    # (The counter passes run only the decode and prefill steps, so no other
+    # step launches these.)
+    if any(k in name for k in PREFILL_KERNELS):
         return "gemm"
     if re.search(r"gemv(_stream)?_kernel<", name):
         return "gemv"
@@ -625,7 +629,7 @@ def trace_summary(trace_dir, bench_json):
     if pf.get("two_phase") or pf.get("bf16_outputs") or pf.get("fused_only") or "prefill" in (r.get("mxfp4") or {}):
         raise SystemExit("profile with --two-phase 0 --mx 0 --bf16-out 0 --fused 0: those steps launch the same "
                          "kernels")
-    fam = ("gemm256_kernel", "gemm_kernel", "splitk_sum_kernel", "dequant_kernel")
+    fam = PREFILL_KERNELS
     gemm = [(n, c, t) for n, c, t in kern if any(f in n.split("(")[0] for f in fam)]
     gemm_t, gemm_c = sum(k[2] for k in gemm), sum(k[1] for k in gemm)
     if "prefill" in r:
@@ -1349,16 +1353,16 @@ def main():
             result["value_gemm"] = round(pre_tflops, 2)
     # Dominant kernel by time: the GEMM when the step has a prefill chunk.
     if do_prefill:
-        result["roofline"] = {"kernel": "the prefill step's q4nx_gemm_ex launches (gemm256_kernel, gemm_kernel, "
-                                        "splitk_sum_kernel, dequant_kernel)", "bound": "mfma",
+        result["roofline"] = {"kernel": "the prefill step's q4nx_gemm_ex launches (" + ", ".join(PREFILL_KERNELS) +
+                                        ")", "bound": "mfma",
                               "achieved": round(pre_tflops, 2), "peak": BF16_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                               "frac": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4), "traffic": None,
                               "algorithmic_bytes": round(alg_pre)}
         if gemm_only_ms:
             t = gemm_only_ms
             result["roofline"]["dominant_kernel"] = {
-                "what": "the same products' bf16 MFMA launches alone (gemm256_kernel, gemm_kernel and the split-K "
-                        "sum, the dequantization pass excluded): HIP events around every q4nx_gemm_bf16 call of "
+                "what": "the same products' bf16 MFMA launches alone (gemm256_kernel, gemm256x128_kernel, "
+                        "gemm_kernel and the split-K sum, the dequantization pass excluded): HIP events around every q4nx_gemm_bf16 call of "
                         "the two-phase step, summed per step, median over the steps",
                 "ms_median": round(t, 4), "achieved": round(pre_flops / (t * 1e-3) / 1e12, 2),
                 "frac": round(pre_flops / (t * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4)}
