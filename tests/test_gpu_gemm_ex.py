@@ -191,10 +191,10 @@ def test_gemm_ex_dequantize_then_multiply(q4, M, N, K, split):
 # Ragged prefill-sized shapes; the planner takes a different plan for each:
 # dequantize-once with a partial last wave of tiles (the first two), the
 # direct fused launch (the third and fifth), split K (the fourth), and one
-# round of 256 x 128 tiles with M and N ragged (the sixth: the
-# one-wave-per-SIMD 256 x 128 kernel's edge tiles).
+# round of 256 x 128 tiles with M and N ragged (the sixth and seventh, N a
+# multiple of 32 or not: the one-wave-per-SIMD 256 x 128 kernel's edge tiles).
 PLANNED_SHAPES = [(4352, 4096, 2560, 32), (4352, 8448, 2560, 32), (2048, 2560, 2048, 48), (2000, 1100, 6912, 48),
-                  (1999, 2500, 2016, 48), (2040, 4000, 2560, 48)]
+                  (1999, 2500, 2016, 48), (2040, 4000, 2560, 48), (2040, 3999, 2560, 48)]
 
 
 @pytest.mark.parametrize("M,N,K,nrows", PLANNED_SHAPES)
