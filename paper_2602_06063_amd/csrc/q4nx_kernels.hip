@@ -924,6 +924,55 @@ struct WideRegs<kWBf16> {
   u32x4 w[8];
 };
 
+// Dequantization of one packed weight group (16 code bytes, its scale s and
+// offset m as loaded) in 16 pieces: piece p handles a quarter of the 8
+// columns 8(p/4)..+7 (Eq. 3, as in dequant8_bf16; for the MXFP4 variant one
+// FP4 x scale conversion of a code byte, as in mx8_bf16), and the last
+// quarter stores the 8 bf16 weights at dst + 8(p/4).  The hand-scheduled
+// GEMM kernels spread the pieces over their MFMA slots, one per slot.
+template <int WF>
+struct GroupDequant {
+  uint32_t lo = 0, hi = 0;
+  float d = 0.0f, m = 0.0f;
+  f32x2 a, e, b, g;
+  u32x4 o;
+  __device__ __forceinline__ void piece(const u32x4& q, uint32_t s, uint32_t mo, int p, uint16_t* dst) {
+    const int u = p >> 2, qt = p & 3;
+    if constexpr (WF == kWMX) {
+      if (p == 0) d = e8m0_f32(s);
+      const uint32_t w = q[u];
+      if (qt == 0) o[0] = fp4x2_bf16<0>(w, d);
+      else if (qt == 1) o[1] = fp4x2_bf16<1>(w, d);
+      else if (qt == 2) o[2] = fp4x2_bf16<2>(w, d);
+      else {
+        o[3] = fp4x2_bf16<3>(w, d);
+        *reinterpret_cast<u32x4*>(dst + 8 * u) = o;
+      }
+    } else {
+      if (qt == 0) {
+        if (u == 0) {
+          d = bf16_to_f32(s) * 512.0f;
+          m = bf16_to_f32(mo);
+        }
+        lo = opaque(q[u] & 0x0F0F0F0Fu);
+        hi = opaque((q[u] >> 4) & 0x0F0F0F0Fu);
+        a = codes2_f32<false>(lo);
+      } else if (qt == 1) {
+        e = codes2_f32<false>(hi);
+        o[0] = pack_bf16x2(eq3(a[0], d, m), eq3(e[0], d, m));
+        o[1] = pack_bf16x2(eq3(a[1], d, m), eq3(e[1], d, m));
+      } else if (qt == 2) {
+        b = codes2_f32<true>(lo);
+        g = codes2_f32<true>(hi);
+        o[2] = pack_bf16x2(eq3(b[0], d, m), eq3(g[0], d, m));
+      } else {
+        o[3] = pack_bf16x2(eq3(b[1], d, m), eq3(g[1], d, m));
+        *reinterpret_cast<u32x4*>(dst + 8 * u) = o;
+      }
+    }
+  }
+};
+
 // WF: W is a packed Q4NX or MXFP4-variant matrix (dequantized on the fly), or
 // bf16 [N][K], whose tile is staged exactly like the X tile.
 // Split K: workgroup (x, y) computes tile x over K steps [y*ksteps,
@@ -1046,48 +1095,10 @@ __global__ __launch_bounds__(kWideThreads) void gemm256_kernel(const uint16_t* _
   auto mma1 = [&](const bf16x8 (&A)[TI], const bf16x8 (&B)[TJ], int i) {
     acc[i >> 2][i & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[i >> 2], B[i & 3], acc[i >> 2][i & 3], 0, 0, 0);
   };
-  // Dequantization of weight group g in 16 pieces: piece p handles a quarter
-  // of the 8 columns 8(p/4)..+7 (Eq. 3, as in dequant8_bf16; for the MXFP4
-  // variant one FP4 x scale conversion of a code byte, as in mx8_bf16).
-  uint32_t wlo = 0, whi = 0;
-  float wd = 0.0f, wmo = 0.0f;
-  f32x2 wa, we, wb, wg;
-  u32x4 wo;
+  // Weight group g of the next step dequantized piece by piece.
+  GroupDequant<WF> gdq;
   auto wpiece = [&](const WideRegs<WF>& R, int st, int g, int p) {
-    if constexpr (WF == kWMX) {
-      const int u = p >> 2, qt = p & 3;
-      if (p == 0) wd = e8m0_f32(R.s[g]);
-      const uint32_t w = R.q[g][u];
-      if (qt == 0) wo[0] = fp4x2_bf16<0>(w, wd);
-      else if (qt == 1) wo[1] = fp4x2_bf16<1>(w, wd);
-      else if (qt == 2) wo[2] = fp4x2_bf16<2>(w, wd);
-      else {
-        wo[3] = fp4x2_bf16<3>(w, wd);
-        *reinterpret_cast<u32x4*>(ws_row(st, g) + 8 * u) = wo;
-      }
-    } else if constexpr (WQ4) {
-    const int u = p >> 2, qt = p & 3;
-    if (qt == 0) {
-      if (u == 0) {
-        wd = bf16_to_f32(R.s[g]) * 512.0f;
-        wmo = bf16_to_f32(R.m[g]);
-      }
-      wlo = opaque(R.q[g][u] & 0x0F0F0F0Fu);
-      whi = opaque((R.q[g][u] >> 4) & 0x0F0F0F0Fu);
-      wa = codes2_f32<false>(wlo);
-    } else if (qt == 1) {
-      we = codes2_f32<false>(whi);
-      wo[0] = pack_bf16x2(eq3(wa[0], wd, wmo), eq3(we[0], wd, wmo));
-      wo[1] = pack_bf16x2(eq3(wa[1], wd, wmo), eq3(we[1], wd, wmo));
-    } else if (qt == 2) {
-      wb = codes2_f32<true>(wlo);
-      wg = codes2_f32<true>(whi);
-      wo[2] = pack_bf16x2(eq3(wb[0], wd, wmo), eq3(wg[0], wd, wmo));
-    } else {
-      wo[3] = pack_bf16x2(eq3(wb[1], wd, wmo), eq3(wg[1], wd, wmo));
-      *reinterpret_cast<u32x4*>(ws_row(st, g) + 8 * u) = wo;
-    }
-    }
+    if constexpr (WQ4) gdq.piece(R.q[g], R.s[g], WF == kWMX ? 0u : R.m[g], p, ws_row(st, g));
   };
   // bf16 W: chunk i of the thread's W rows, staged like X.
   auto wchunk = [&](const WideRegs<WF>& R, int st, int i) {
@@ -1419,47 +1430,10 @@ __global__ __launch_bounds__(kWideThreads) void gemm256x128_kernel(const uint16_
   auto mma1 = [&](const bf16x8 (&A)[TI], const bf16x8 (&B)[TJ], int i) {
     acc[i >> 1][i & 1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A[i >> 1], B[i & 1], acc[i >> 1][i & 1], 0, 0, 0);
   };
-  // Dequantization of the thread's weight group in 16 pieces (p = 0..15: a
-  // quarter of the 8 columns 8(p/4)..+7), as in the 256 x 256 kernel.
-  uint32_t wlo = 0, whi = 0;
-  float wd = 0.0f, wmo = 0.0f;
-  f32x2 wa, we, wb, wg;
-  u32x4 wo;
+  // The thread's weight group of the next step dequantized piece by piece.
+  GroupDequant<WF> gdq;
   auto wpiece = [&](const Wide128Regs<WF>& R, int st, int p) {
-    if constexpr (WF == kWMX) {
-      const int u = p >> 2, qt = p & 3;
-      if (p == 0) wd = e8m0_f32(R.s);
-      const uint32_t w = R.q[u];
-      if (qt == 0) wo[0] = fp4x2_bf16<0>(w, wd);
-      else if (qt == 1) wo[1] = fp4x2_bf16<1>(w, wd);
-      else if (qt == 2) wo[2] = fp4x2_bf16<2>(w, wd);
-      else {
-        wo[3] = fp4x2_bf16<3>(w, wd);
-        *reinterpret_cast<u32x4*>(ws_row(st) + 8 * u) = wo;
-      }
-    } else if constexpr (WQ4) {
-      const int u = p >> 2, qt = p & 3;
-      if (qt == 0) {
-        if (u == 0) {
-          wd = bf16_to_f32(R.s) * 512.0f;
-          wmo = bf16_to_f32(R.m);
-        }
-        wlo = opaque(R.q[u] & 0x0F0F0F0Fu);
-        whi = opaque((R.q[u] >> 4) & 0x0F0F0F0Fu);
-        wa = codes2_f32<false>(wlo);
-      } else if (qt == 1) {
-        we = codes2_f32<false>(whi);
-        wo[0] = pack_bf16x2(eq3(wa[0], wd, wmo), eq3(we[0], wd, wmo));
-        wo[1] = pack_bf16x2(eq3(wa[1], wd, wmo), eq3(we[1], wd, wmo));
-      } else if (qt == 2) {
-        wb = codes2_f32<true>(wlo);
-        wg = codes2_f32<true>(whi);
-        wo[2] = pack_bf16x2(eq3(wb[0], wd, wmo), eq3(wg[0], wd, wmo));
-      } else {
-        wo[3] = pack_bf16x2(eq3(wb[1], wd, wmo), eq3(wg[1], wd, wmo));
-        *reinterpret_cast<u32x4*>(ws_row(st) + 8 * u) = wo;
-      }
-    }
+    if constexpr (WQ4) gdq.piece(R.q, R.s, WF == kWMX ? 0u : R.m, p, ws_row(st));
   };
   auto xwrite = [&](const Wide128Regs<WF>& R, uint16_t* xsn, int k) {
     *reinterpret_cast<u32x4*>(xsn + 32 * k * kLdsStride) = R.x[k];
